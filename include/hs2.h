@@ -1,0 +1,155 @@
+/*
+ * hs2.h -- C ABI of libhs2.so: decode-time attention of one HySparse2 hybrid
+ * block on MI355X (gfx950).
+ *
+ * A hybrid block is one full-attention (FA) layer followed by sparse-attention
+ * (SA) layers (HySparse2, Sec. "HySparse2 Overview").  The FA layer attends
+ * over the whole KV cache and doubles as the indexer: its exact softmax
+ * probabilities are the token scores (Sec. "The Role of Full Attention").
+ * Per query, the most recent `window` tokens are always selected and the `k`
+ * highest-scoring tokens before that window are added (Sec. "Cross-Layer KV
+ * Reuse", removal of the separate SWA branch; token-level selection in the
+ * same section).  The SA layers reuse the FA layer's KV cache and those
+ * indices (KV Reuse, same section).  FA and SA use no positional encoding
+ * (Sec. "Experimental Setup").
+ *
+ * Readings where the paper is silent, fixed by this ABI:
+ *   - score of token t for KV head g and query c: the sum, over the query
+ *     heads h of g, of head h's softmax probability of t (each head
+ *     normalised over its own causal range);
+ *   - top-k is drawn only from tokens outside the window; equal scores go to
+ *     the lower token index; scores below FLT_MIN rank as zero;
+ *   - the cache of sequence b holds tokens [0, len[b]) including the decode
+ *     tokens; query c of a C-token chunk sits at pos = len[b] - C + c and sees
+ *     tokens [0, pos]; its window is [max(0, pos - window + 1), pos];
+ *   - query head h reads KV head h / G with G = n_q_heads / n_kv_heads;
+ *   - SA layers use a plain softmax over the selected tokens (no sink).
+ *
+ * Conventions for every entry point:
+ *   - tensor pointers are DEVICE pointers (HIP device memory of the current
+ *     device) unless stated otherwise; bf16 tensors are passed as uint16_t
+ *     bit patterns; every work-issuing call is asynchronous on `stream`
+ *     (a hipStream_t; NULL = the default stream) and results are valid once
+ *     the caller synchronises that stream;
+ *   - the caller owns every buffer, including the workspace; the library
+ *     never allocates or frees device memory and never synchronises;
+ *   - inputs are read-only; outputs must not alias inputs or the workspace;
+ *   - every condition checkable on the host is checked before anything is
+ *     launched; on error nothing is launched, outputs are untouched and a
+ *     negative status is returned (hs2_status_string / hs2_last_error give a
+ *     message).  Nothing throws across this ABI.
+ *   - len[] lives on the device and is not read by the host.  Precondition:
+ *     n_queries <= len[b] <= max_len.  The kernels clamp len[b] to
+ *     [0, max_len]; a query whose position is negative gets an all -1 index
+ *     row and a zero output.
+ */
+#ifndef HS2_H
+#define HS2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hs2_status {
+  HS2_OK = 0,
+  HS2_ERR_NULL = -1,        /* a required pointer is NULL                         */
+  HS2_ERR_SHAPE = -2,       /* inconsistent or out-of-range dimensions / budgets  */
+  HS2_ERR_UNSUPPORTED = -3, /* valid request this build does not implement        */
+  HS2_ERR_WORKSPACE = -4,   /* workspace smaller than hs2_workspace_bytes()       */
+  HS2_ERR_ALIGN = -5,       /* pointer or stride not 16-byte aligned              */
+  HS2_ERR_HIP = -6          /* a HIP runtime call or a kernel launch failed       */
+} hs2_status;
+
+/* Shapes shared by every call of one hybrid block.
+ *   q, out:  [batch, n_queries, n_q_heads, head_dim] contiguous bf16
+ *   K, V:    element (b, g, t, d) at b*kv_stride_b + g*kv_stride_h + t*kv_stride_t + d
+ *            (bf16; K and V share this layout; each token row is contiguous)    */
+typedef struct hs2_dims {
+  int32_t batch;       /* B >= 1                                                  */
+  int32_t n_queries;   /* C: decode tokens per sequence, 1 .. 16                  */
+  int32_t n_q_heads;   /* Hq >= 1                                                 */
+  int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, G = Hq / Hkv <= 64,            */
+                       /*   C * (G rounded up to a power of two) <= 128           */
+  int32_t head_dim;    /* D: 128 (other values: HS2_ERR_UNSUPPORTED)              */
+  int32_t max_len;     /* Lmax: cache capacity per sequence, 1 .. 2^27 tokens     */
+  int64_t kv_stride_b; /* elements; multiple of 8                                 */
+  int64_t kv_stride_h; /* elements; multiple of 8                                 */
+  int64_t kv_stride_t; /* elements; >= head_dim, multiple of 8                    */
+  float scale;         /* softmax scale; <= 0 selects 1/sqrt(head_dim)            */
+} hs2_dims;
+
+/* Bytes of device workspace that every call below needs for these dims and
+ * budgets (the same buffer may serve all calls of a block, one at a time).
+ * Host-only, launches nothing.  Returns 0 if the dims or budgets are invalid. */
+size_t hs2_workspace_bytes(const hs2_dims* dims, int32_t k, int32_t window);
+
+/* Full-attention layer + token scores + selection (the block's first layer).
+ *
+ *   q       [B, C, Hq, D] bf16         FA-layer queries
+ *   K, V    cache, layout of hs2_dims  (read over [0, len[b]) per sequence)
+ *   len     [B] int32 (device)         tokens in each sequence's cache
+ *   k       >= 0                       top-k budget outside the window
+ *   window  >= 0                       forced recent window; k + window >= 1
+ *   out     [B, C, Hq, D] bf16         attention output (fp32 accumulation,
+ *                                      rounded to nearest even)
+ *   idx     [B, Hkv, C, k + window] int32   selected token indices of each
+ *           (sequence, KV head, query): ascending, then -1 padding.  Row
+ *           length min(pos + 1, k + window): min(k, N) top-k tokens of the
+ *           N = max(0, pos - window + 1) tokens before the window, then the
+ *           window itself.
+ *   stats   [B, C, Hq, 2] float or NULL: per head (M, Z) with M the largest
+ *           logit scale*<q, k_t> over [0, pos] and Z = sum_t exp(logit_t - M)
+ *   scores  [B, Hkv, C, max_len] float or NULL: pooled scores of the
+ *           candidate tokens [0, N); entries from N on are unspecified
+ *   workspace / workspace_bytes: device scratch, >= hs2_workspace_bytes()
+ *   stream  hipStream_t                                                        */
+hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, const uint16_t* K,
+                                      const uint16_t* V, const int32_t* len, int32_t k, int32_t window,
+                                      uint16_t* out, int32_t* idx, float* stats, float* scores,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sparse-attention layer reusing the FA layer's cache and selection.
+ *
+ *   q       [B, C, Hq, D] bf16         this SA layer's own queries
+ *   K, V    the same cache the FA layer read
+ *   len     [B] int32 (device)         as for the FA call
+ *   idx     [B, Hkv, C, n_slots] int32 (device) selection rows; entries < 0
+ *           or >= len[b] are skipped.  Query head h uses row (b, h / G, c).
+ *   out     [B, C, Hq, D] bf16         softmax attention over the selected
+ *           tokens only (a row with no valid entry gives 0)                    */
+hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                           const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Selection alone, from caller-given pooled scores (test and diagnostics).
+ * Runs exactly the selection kernels of hs2_full_attn_score_select on
+ * scores [B, Hkv, C, max_len] float (device; entries [0, N) of each row are
+ * read, must be >= 0 and finite) and writes idx as described there.          */
+hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
+                                  int32_t window, int32_t* idx, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/* Static description of a status code. */
+const char* hs2_status_string(int32_t status);
+
+/* Message of the last failed call on this host thread ("" if none). */
+const char* hs2_last_error(void);
+
+/* Per-kernel timing (diagnostics).  While enabled, every kernel launch of this
+ * library is bracketed by a pair of HIP events recorded on the launch stream
+ * (up to a fixed number of launches).  hs2_timing_read() waits for the
+ * recorded events, then fills, for up to `max_kernels` kernel kinds that ran,
+ * their names (NUL-separated into `names`), launch counts and total
+ * milliseconds; it returns the number of kinds written, or a negative status.
+ * hs2_timing_reset() discards the records.  Not thread-safe.                  */
+hs2_status hs2_timing_enable(int32_t on);
+void hs2_timing_reset(void);
+int32_t hs2_timing_read(char* names, size_t names_len, int32_t* counts, double* total_ms, int32_t max_kernels);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HS2_H */

@@ -1,0 +1,529 @@
+// C ABI of libhs2.so: argument checks, work planning, workspace layout and the
+// launch sequence of each call.  Declarations and contracts: include/hs2.h.
+#include "../../include/hs2.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "hs2_launch.h"
+
+namespace {
+
+using namespace hs2;
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxQueries = 16;
+constexpr int kMaxRows = 128;           // C * Gp
+constexpr int kMaxGroup = 64;
+constexpr int32_t kMaxLen = 1 << 27;
+constexpr int kNBins = 2048;
+constexpr int kSelChunk = 16384;        // tokens per workgroup of the selection scans
+constexpr size_t kAlign = 256;
+
+thread_local std::string g_last_error;
+
+hs2_status fail(hs2_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+int next_pow2(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return atoi(v);
+}
+
+// ---------------------------------------------------------------- planning
+struct Plan {
+  int B, C, Hq, Hkv, G, Gp, D, Lmax, k, W, S;
+  float c2;
+  int RT, TG;                 // full-attention / pooling row tiles
+  int fa_split, fa_nsplit;
+  int pool_split, pool_nsplit;
+  int64_t units;              // B * Hkv
+  int64_t rows;               // selection rows B * Hkv * C
+  int64_t score_stride, bitmap_words, cand_cap;
+  int sel_nchunks;
+  // workspace layout of hs2_full_attn_score_select / hs2_select_from_scores
+  size_t off_part_o, off_part_ml, off_stats, off_scores, off_hist, off_state, off_bitmap, off_ckey, off_cidx;
+  size_t fa_bytes;
+};
+
+struct SaPlan {
+  int RT, TG, split, nsplit, n_slots;
+  size_t off_part_o, off_part_ml, bytes;
+};
+
+hs2_status check_dims(const hs2_dims* d) {
+  if (!d) return fail(HS2_ERR_NULL, "dims is NULL");
+  if (d->batch < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1)
+    return fail(HS2_ERR_SHAPE, "batch, n_q_heads and n_kv_heads must be >= 1");
+  if (d->n_queries < 1 || d->n_queries > kMaxQueries)
+    return fail(HS2_ERR_SHAPE, "n_queries must be in [1, %d] (got %d)", kMaxQueries, d->n_queries);
+  if (d->n_q_heads % d->n_kv_heads)
+    return fail(HS2_ERR_SHAPE, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", d->n_q_heads, d->n_kv_heads);
+  if (d->max_len < 1 || d->max_len > kMaxLen) return fail(HS2_ERR_SHAPE, "max_len must be in [1, 2^27]");
+  if (d->head_dim != kHeadDim) return fail(HS2_ERR_UNSUPPORTED, "head_dim %d not supported (only 128)", d->head_dim);
+  const int G = d->n_q_heads / d->n_kv_heads;
+  if (G > kMaxGroup) return fail(HS2_ERR_UNSUPPORTED, "query heads per KV head %d > %d", G, kMaxGroup);
+  if (d->n_queries * next_pow2(G) > kMaxRows)
+    return fail(HS2_ERR_UNSUPPORTED, "n_queries * pow2(G) = %d exceeds %d query rows per KV head",
+                d->n_queries * next_pow2(G), kMaxRows);
+  if (d->kv_stride_t < d->head_dim || d->kv_stride_t % 8 || d->kv_stride_h < 0 || d->kv_stride_h % 8 ||
+      d->kv_stride_b < 0 || d->kv_stride_b % 8)
+    return fail(HS2_ERR_ALIGN, "KV strides must be non-negative multiples of 8 elements, kv_stride_t >= head_dim");
+  if (!std::isfinite(d->scale)) return fail(HS2_ERR_SHAPE, "scale must be finite");
+  return HS2_OK;
+}
+
+hs2_status check_budget(int32_t k, int32_t window) {
+  if (k < 0 || window < 0) return fail(HS2_ERR_SHAPE, "k and window must be >= 0");
+  if ((int64_t)k + window < 1) return fail(HS2_ERR_SHAPE, "k + window must be >= 1");
+  if ((int64_t)k + window > kMaxLen) return fail(HS2_ERR_SHAPE, "k + window too large");
+  return HS2_OK;
+}
+
+size_t carve(size_t& cur, size_t bytes) {
+  cur = (size_t)round_up((int64_t)cur, kAlign);
+  const size_t at = cur;
+  cur += bytes;
+  return at;
+}
+
+void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
+  p.B = d->batch;
+  p.C = d->n_queries;
+  p.Hq = d->n_q_heads;
+  p.Hkv = d->n_kv_heads;
+  p.G = p.Hq / p.Hkv;
+  p.Gp = next_pow2(p.G);
+  p.D = d->head_dim;
+  p.Lmax = d->max_len;
+  p.k = k;
+  p.W = window;
+  p.S = k + window;
+  const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
+  p.c2 = (float)(scale * 1.4426950408889634);
+  const int rows16 = (int)cdiv(p.C * p.Gp, 16);
+  p.RT = next_pow2(rows16);
+  p.TG = p.RT >= 4 ? 1 : 4 / p.RT;
+  p.units = (int64_t)p.B * p.Hkv;
+  p.rows = p.units * p.C;
+  // token splits: about 1024 workgroups over the whole cache, whole 64-token tiles
+  const int64_t total = p.units * (int64_t)p.Lmax;
+  int split = (int)std::max<int64_t>(256, round_up(cdiv(total, 1024), 64));
+  split = env_int("HS2_FA_SPLIT", split);
+  split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, p.Lmax), 64));
+  p.fa_split = split;
+  p.fa_nsplit = (int)cdiv(p.Lmax, split);
+  int psplit = env_int("HS2_POOL_SPLIT", split);
+  psplit = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(std::min(psplit, 32768), p.Lmax), 64));
+  p.pool_split = psplit;
+  p.pool_nsplit = (int)cdiv(p.Lmax, psplit);
+  p.score_stride = round_up(p.Lmax, 64);
+  p.bitmap_words = cdiv(p.Lmax, 64);
+  p.cand_cap = p.Lmax;
+  p.sel_nchunks = (int)cdiv(p.Lmax, kSelChunk);
+
+  const int64_t prow = 16 * p.RT;
+  const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
+  size_t cur = 0;
+  p.off_part_o = carve(cur, sizeof(float) * p.units * nslot * prow * kHeadDim);
+  p.off_part_ml = carve(cur, sizeof(float) * p.units * nslot * prow * 2);
+  p.off_stats = carve(cur, sizeof(float) * (size_t)p.B * p.C * p.Hq * 2);
+  p.off_scores = carve(cur, sizeof(float) * p.rows * p.score_stride);
+  p.off_hist = carve(cur, sizeof(uint32_t) * p.rows * kNBins);
+  p.off_state = carve(cur, sizeof(int32_t) * p.rows * 8);
+  p.off_bitmap = carve(cur, sizeof(uint64_t) * p.rows * p.bitmap_words);
+  p.off_ckey = carve(cur, sizeof(uint32_t) * p.rows * p.cand_cap);
+  p.off_cidx = carve(cur, sizeof(int32_t) * p.rows * p.cand_cap);
+  p.fa_bytes = (size_t)round_up((int64_t)cur, kAlign);
+}
+
+void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
+  s.n_slots = n_slots;
+  s.RT = next_pow2((int)cdiv(p.Gp, 16));
+  s.TG = s.RT >= 4 ? 1 : 4 / s.RT;
+  int split = (int)std::max<int64_t>(64, round_up(cdiv(p.rows * (int64_t)n_slots, 1024), 64));
+  split = env_int("HS2_SA_SPLIT", split);
+  split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, n_slots), 64));
+  s.split = split;
+  s.nsplit = (int)cdiv(n_slots, split);
+  const int64_t prow = 16 * s.RT;
+  size_t cur = 0;
+  s.off_part_o = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * kHeadDim);
+  s.off_part_ml = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * 2);
+  s.bytes = (size_t)round_up((int64_t)cur, kAlign);
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// ---------------------------------------------------------------- timing
+enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_THRESH, KK_SEL_FILTER,
+                  KK_SEL_RESOLVE, KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
+const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "sel_init", "sel_hist", "sel_threshold",
+                                    "sel_filter", "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
+constexpr int kMaxTimed = 16384;
+struct Timing {
+  bool on = false;
+  int n = 0;
+  std::vector<hipEvent_t> ev0, ev1;
+  std::vector<int> kind;
+} g_timing;
+
+struct TimedLaunch {
+  hipStream_t s;
+  int slot = -1;
+  TimedLaunch(KernelKind kk, hipStream_t st) : s(st) {
+    if (g_timing.on && g_timing.n < (int)g_timing.ev0.size()) {
+      slot = g_timing.n++;
+      g_timing.kind[slot] = kk;
+      (void)hipEventRecord(g_timing.ev0[slot], s);
+    }
+  }
+  ~TimedLaunch() {
+    if (slot >= 0) (void)hipEventRecord(g_timing.ev1[slot], s);
+  }
+};
+
+std::mutex g_init_mu;
+bool g_pool_attr_done[64] = {};
+
+hs2_status ensure_device_init() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(HS2_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= 64) return fail(HS2_ERR_HIP, "device index out of range");
+  std::lock_guard<std::mutex> lk(g_init_mu);
+  if (!g_pool_attr_done[dev]) {
+    hipError_t e = set_pool_smem_limits();
+    if (e != hipSuccess) return fail(HS2_ERR_HIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    g_pool_attr_done[dev] = true;
+  }
+  return HS2_OK;
+}
+
+#define HS2_TRY_LAUNCH(kind, stream, call)                                                        \
+  do {                                                                                              \
+    hipError_t e_;                                                                                  \
+    {                                                                                               \
+      TimedLaunch tl_(kind, stream);                                                                \
+      e_ = (call);                                                                                  \
+    }                                                                                               \
+    if (e_ != hipSuccess) return fail(HS2_ERR_HIP, "%s launch: %s", kKindNames[kind], hipGetErrorString(e_)); \
+  } while (0)
+
+SelArgs sel_args(const Plan& p, char* ws, const float* scores, int64_t score_stride, const int32_t* len,
+                 int32_t* idx) {
+  SelArgs a{};
+  a.scores = scores;
+  a.len = len;
+  a.hist = (uint32_t*)(ws + p.off_hist);
+  a.state = (int32_t*)(ws + p.off_state);
+  a.bitmap = (uint64_t*)(ws + p.off_bitmap);
+  a.cand_key = (uint32_t*)(ws + p.off_ckey);
+  a.cand_idx = (int32_t*)(ws + p.off_cidx);
+  a.idx = idx;
+  a.rows = p.rows;
+  a.score_stride = score_stride;
+  a.bitmap_words = p.bitmap_words;
+  a.cand_cap = p.cand_cap;
+  a.B = p.B;
+  a.C = p.C;
+  a.Hkv = p.Hkv;
+  a.max_len = p.Lmax;
+  a.k = p.k;
+  a.W = p.W;
+  a.S = p.S;
+  a.chunk = kSelChunk;
+  return a;
+}
+
+hs2_status run_selection_tail(const Plan& p, const SelArgs& sa, hipStream_t s) {
+  HS2_TRY_LAUNCH(KK_SEL_THRESH, s, launch_sel_threshold(sa, s));
+  HS2_TRY_LAUNCH(KK_SEL_FILTER, s, launch_sel_filter(sa, p.sel_nchunks, s));
+  HS2_TRY_LAUNCH(KK_SEL_RESOLVE, s, launch_sel_resolve(sa, s));
+  HS2_TRY_LAUNCH(KK_SEL_EMIT, s, launch_sel_emit(sa, s));
+  return HS2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hs2_status_string(int32_t status) {
+  switch (status) {
+    case HS2_OK: return "ok";
+    case HS2_ERR_NULL: return "required pointer is NULL";
+    case HS2_ERR_SHAPE: return "invalid dimensions or budgets";
+    case HS2_ERR_UNSUPPORTED: return "unsupported configuration";
+    case HS2_ERR_WORKSPACE: return "workspace too small";
+    case HS2_ERR_ALIGN: return "pointer or stride misaligned";
+    case HS2_ERR_HIP: return "HIP runtime or launch failure";
+    default: return "unknown status";
+  }
+}
+
+const char* hs2_last_error(void) { return g_last_error.c_str(); }
+
+size_t hs2_workspace_bytes(const hs2_dims* dims, int32_t k, int32_t window) {
+  if (check_dims(dims) != HS2_OK || check_budget(k, window) != HS2_OK) return 0;
+  Plan p;
+  make_plan(dims, k, window, p);
+  SaPlan sp;
+  make_sa_plan(p, k + window, sp);
+  return std::max(p.fa_bytes, sp.bytes);
+}
+
+hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                      const int32_t* len, int32_t k, int32_t window, uint16_t* out, int32_t* idx,
+                                      float* stats, float* scores, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+  hs2_status st = check_dims(dims);
+  if (st != HS2_OK) return st;
+  if ((st = check_budget(k, window)) != HS2_OK) return st;
+  if (!q || !K || !V || !len || !out || !idx || !workspace)
+    return fail(HS2_ERR_NULL, "q, K, V, len, out, idx and workspace are required");
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
+      !aligned(len, 4) || !aligned(workspace, kAlign) || (stats && !aligned(stats, 8)) || (scores && !aligned(scores, 4)))
+    return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len/scores 4-byte alignment");
+  Plan p;
+  make_plan(dims, k, window, p);
+  if (workspace_bytes < p.fa_bytes)
+    return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
+  if ((st = ensure_device_init()) != HS2_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  float* stats_log2 = (float*)(ws + p.off_stats);
+  float* sc = scores ? scores : (float*)(ws + p.off_scores);
+  const int64_t sc_stride = scores ? (int64_t)p.Lmax : p.score_stride;
+
+  SelArgs sa = sel_args(p, ws, sc, sc_stride, len, idx);
+  HS2_TRY_LAUNCH(KK_SEL_INIT, s, launch_sel_init(sa, s));
+
+  FaArgs fa{};
+  fa.q = q;
+  fa.K = K;
+  fa.V = V;
+  fa.len = len;
+  fa.part_o = (float*)(ws + p.off_part_o);
+  fa.part_ml = (float*)(ws + p.off_part_ml);
+  fa.stride_b = dims->kv_stride_b;
+  fa.stride_h = dims->kv_stride_h;
+  fa.stride_t = dims->kv_stride_t;
+  fa.c2 = p.c2;
+  fa.B = p.B;
+  fa.C = p.C;
+  fa.Hq = p.Hq;
+  fa.Hkv = p.Hkv;
+  fa.G = p.G;
+  fa.Gp = p.Gp;
+  fa.max_len = p.Lmax;
+  fa.split_tokens = p.fa_split;
+  fa.n_split = p.fa_nsplit;
+  HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, s));
+
+  CombineArgs ca{};
+  ca.part_o = fa.part_o;
+  ca.part_ml = fa.part_ml;
+  ca.len = len;
+  ca.out = out;
+  ca.stats_log2 = stats_log2;
+  ca.stats_user = stats;
+  ca.B = p.B;
+  ca.C = p.C;
+  ca.Hq = p.Hq;
+  ca.Hkv = p.Hkv;
+  ca.G = p.G;
+  ca.Gp = p.Gp;
+  ca.max_len = p.Lmax;
+  ca.rows = 16 * p.RT;
+  ca.nslot = p.fa_nsplit * p.TG;
+  ca.tg = p.TG;
+  ca.split_tokens = p.fa_split;
+  ca.sa_mode = 0;
+  HS2_TRY_LAUNCH(KK_COMBINE, s, launch_combine(ca, std::min(16 * p.RT, p.C * p.Gp), p.units, s));
+
+  PoolArgs pa{};
+  pa.q = q;
+  pa.K = K;
+  pa.len = len;
+  pa.stats_log2 = stats_log2;
+  pa.scores = sc;
+  pa.hist = sa.hist;
+  pa.stride_b = dims->kv_stride_b;
+  pa.stride_h = dims->kv_stride_h;
+  pa.stride_t = dims->kv_stride_t;
+  pa.score_stride = sc_stride;
+  pa.c2 = p.c2;
+  pa.B = p.B;
+  pa.C = p.C;
+  pa.Hq = p.Hq;
+  pa.Hkv = p.Hkv;
+  pa.G = p.G;
+  pa.Gp = p.Gp;
+  pa.max_len = p.Lmax;
+  pa.W = p.W;
+  pa.split_tokens = p.pool_split;
+  pa.n_split = p.pool_nsplit;
+  HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
+
+  return run_selection_tail(p, sa, s);
+}
+
+hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
+                                  int32_t window, int32_t* idx, void* workspace, size_t workspace_bytes, void* stream) {
+  hs2_status st = check_dims(dims);
+  if (st != HS2_OK) return st;
+  if ((st = check_budget(k, window)) != HS2_OK) return st;
+  if (!scores || !len || !idx || !workspace) return fail(HS2_ERR_NULL, "scores, len, idx and workspace are required");
+  if (!aligned(scores, 4) || !aligned(len, 4) || !aligned(idx, 4) || !aligned(workspace, kAlign))
+    return fail(HS2_ERR_ALIGN, "scores/len/idx need 4-byte, workspace 256-byte alignment");
+  Plan p;
+  make_plan(dims, k, window, p);
+  if (workspace_bytes < p.fa_bytes)
+    return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
+  if ((st = ensure_device_init()) != HS2_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  SelArgs sa = sel_args(p, (char*)workspace, scores, p.Lmax, len, idx);
+  HS2_TRY_LAUNCH(KK_SEL_INIT, s, launch_sel_init(sa, s));
+  HS2_TRY_LAUNCH(KK_SEL_HIST, s, launch_sel_hist(sa, p.sel_nchunks, s));
+  return run_selection_tail(p, sa, s);
+}
+
+hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                           const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  hs2_status st = check_dims(dims);
+  if (st != HS2_OK) return st;
+  if (n_slots < 1 || n_slots > kMaxLen) return fail(HS2_ERR_SHAPE, "n_slots must be in [1, 2^27]");
+  if (!q || !K || !V || !len || !idx || !out || !workspace)
+    return fail(HS2_ERR_NULL, "q, K, V, len, idx, out and workspace are required");
+  if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
+      !aligned(len, 4) || !aligned(workspace, kAlign))
+    return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len 4-byte alignment");
+  Plan p;
+  make_plan(dims, 0, n_slots, p);
+  SaPlan sp;
+  make_sa_plan(p, n_slots, sp);
+  if (workspace_bytes < sp.bytes)
+    return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, sp.bytes);
+  if ((st = ensure_device_init()) != HS2_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  SaArgs a{};
+  a.q = q;
+  a.K = K;
+  a.V = V;
+  a.len = len;
+  a.idx = idx;
+  a.part_o = (float*)(ws + sp.off_part_o);
+  a.part_ml = (float*)(ws + sp.off_part_ml);
+  a.stride_b = dims->kv_stride_b;
+  a.stride_h = dims->kv_stride_h;
+  a.stride_t = dims->kv_stride_t;
+  a.idx_stride = n_slots;
+  a.c2 = p.c2;
+  a.B = p.B;
+  a.C = p.C;
+  a.Hq = p.Hq;
+  a.Hkv = p.Hkv;
+  a.G = p.G;
+  a.max_len = p.Lmax;
+  a.n_slots = n_slots;
+  a.split_slots = sp.split;
+  a.n_split = sp.nsplit;
+  HS2_TRY_LAUNCH(KK_SA, s, launch_sa_split(a, sp.RT, s));
+
+  CombineArgs ca{};
+  ca.part_o = a.part_o;
+  ca.part_ml = a.part_ml;
+  ca.len = len;
+  ca.out = out;
+  ca.stats_log2 = nullptr;
+  ca.stats_user = nullptr;
+  ca.B = p.B;
+  ca.C = p.C;
+  ca.Hq = p.Hq;
+  ca.Hkv = p.Hkv;
+  ca.G = p.G;
+  ca.Gp = p.Gp;
+  ca.max_len = p.Lmax;
+  ca.rows = 16 * sp.RT;
+  ca.nslot = sp.nsplit * sp.TG;
+  ca.tg = sp.TG;
+  ca.split_tokens = 0;
+  ca.sa_mode = 1;
+  HS2_TRY_LAUNCH(KK_SA_COMBINE, s, launch_combine(ca, p.G, p.rows, s));
+  return HS2_OK;
+}
+
+hs2_status hs2_timing_enable(int32_t on) {
+  if (on && g_timing.ev0.empty()) {
+    g_timing.ev0.resize(kMaxTimed);
+    g_timing.ev1.resize(kMaxTimed);
+    g_timing.kind.resize(kMaxTimed);
+    for (int i = 0; i < kMaxTimed; ++i) {
+      if (hipEventCreate(&g_timing.ev0[i]) != hipSuccess || hipEventCreate(&g_timing.ev1[i]) != hipSuccess) {
+        g_timing.ev0.clear();
+        g_timing.ev1.clear();
+        g_timing.kind.clear();
+        return fail(HS2_ERR_HIP, "hipEventCreate failed");
+      }
+    }
+  }
+  g_timing.on = on != 0;
+  return HS2_OK;
+}
+
+void hs2_timing_reset(void) { g_timing.n = 0; }
+
+int32_t hs2_timing_read(char* names, size_t names_len, int32_t* counts, double* total_ms, int32_t max_kernels) {
+  double tot[KK_COUNT] = {};
+  int cnt[KK_COUNT] = {};
+  for (int i = 0; i < g_timing.n; ++i) {
+    if (hipEventSynchronize(g_timing.ev1[i]) != hipSuccess) return fail(HS2_ERR_HIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g_timing.ev0[i], g_timing.ev1[i]) != hipSuccess)
+      return fail(HS2_ERR_HIP, "hipEventElapsedTime failed");
+    tot[g_timing.kind[i]] += ms;
+    cnt[g_timing.kind[i]] += 1;
+  }
+  int n = 0;
+  size_t pos = 0;
+  for (int kk = 0; kk < KK_COUNT && n < max_kernels; ++kk) {
+    if (!cnt[kk]) continue;
+    const size_t L = strlen(kKindNames[kk]) + 1;
+    if (names && pos + L <= names_len) {
+      memcpy(names + pos, kKindNames[kk], L);
+      pos += L;
+    }
+    if (counts) counts[n] = cnt[kk];
+    if (total_ms) total_ms[n] = tot[kk];
+    ++n;
+  }
+  return n;
+}
+
+}  // extern "C"

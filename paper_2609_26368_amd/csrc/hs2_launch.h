@@ -1,0 +1,92 @@
+// Internal interface between the C ABI (hs2_api.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hs2 {
+
+struct FaArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  const uint16_t* V;
+  const int32_t* len;
+  float* part_o;   // [B*Hkv][n_split*TG][16 RT][HD]
+  float* part_ml;  // [B*Hkv][n_split*TG][16 RT][2]
+  int64_t stride_b, stride_h, stride_t;
+  float c2;        // softmax scale * log2(e)
+  int B, C, Hq, Hkv, G, Gp, max_len;
+  int split_tokens, n_split;
+};
+
+struct CombineArgs {
+  const float* part_o;
+  const float* part_ml;
+  const int32_t* len;
+  uint16_t* out;        // [B, C, Hq, HD] bf16
+  float* stats_log2;    // [B, C, Hq, 2] (M in log2 units, Z) or null
+  float* stats_user;    // [B, C, Hq, 2] (M in natural units, Z) or null
+  int B, C, Hq, Hkv, G, Gp, max_len;
+  int rows;             // partial rows per slot
+  int nslot;            // partial slots per unit
+  int tg;               // slots per split (FA)
+  int split_tokens;     // FA split size (FA only)
+  int sa_mode;
+};
+
+struct PoolArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  const int32_t* len;
+  const float* stats_log2;
+  float* scores;        // [rows][score_stride]
+  uint32_t* hist;       // [rows][NBINS]
+  int64_t stride_b, stride_h, stride_t;
+  int64_t score_stride;
+  float c2;
+  int B, C, Hq, Hkv, G, Gp, max_len, W;
+  int split_tokens, n_split;
+};
+
+struct SelArgs {
+  const float* scores;
+  const int32_t* len;
+  uint32_t* hist;       // [rows][NBINS]
+  int32_t* state;       // [rows][8]
+  uint64_t* bitmap;     // [rows][bitmap_words]
+  uint32_t* cand_key;   // [rows][cand_cap]
+  int32_t* cand_idx;    // [rows][cand_cap]
+  int32_t* idx;         // [rows][S]
+  int64_t rows, score_stride, bitmap_words, cand_cap;
+  int B, C, Hkv, max_len, k, W, S;
+  int chunk;
+};
+
+struct SaArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  const uint16_t* V;
+  const int32_t* len;
+  const int32_t* idx;   // [B*Hkv*C][idx_stride]
+  float* part_o;
+  float* part_ml;
+  int64_t stride_b, stride_h, stride_t, idx_stride;
+  float c2;
+  int B, C, Hq, Hkv, G, max_len;
+  int n_slots, split_slots, n_split;
+};
+
+hipError_t launch_fa_split(const FaArgs& a, int RT, hipStream_t s);
+hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
+hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
+size_t pool_smem_bytes(int RT, int C);
+hipError_t set_pool_smem_limits();
+hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
+hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
+hipError_t launch_sel_threshold(const SelArgs& a, hipStream_t s);
+hipError_t launch_sel_filter(const SelArgs& a, int nchunks, hipStream_t s);
+hipError_t launch_sel_resolve(const SelArgs& a, hipStream_t s);
+hipError_t launch_sel_emit(const SelArgs& a, hipStream_t s);
+hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s);
+
+}  // namespace hs2

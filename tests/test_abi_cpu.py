@@ -1,0 +1,136 @@
+"""The C ABI without a GPU: the library loads, exports what include/hs2.h
+declares, sizes workspaces and rejects invalid calls before launching."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_26368_amd import hs2
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hs2.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hs2.LIB_PATH):
+        from paper_2609_26368_amd import _build
+        _build.build()
+    return hs2.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hs2_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_names():
+    assert declared_functions() == sorted(hs2.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def dims(**kw):
+    base = dict(batch=2, n_queries=1, n_q_heads=32, n_kv_heads=4, head_dim=128, max_len=4096)
+    base.update(kw)
+    strides = kw.pop("kv_strides", None)
+    d = hs2.make_dims(base["batch"], base["n_queries"], base["n_q_heads"], base["n_kv_heads"], base["head_dim"],
+                      base["max_len"], strides)
+    return d
+
+
+def test_workspace_bytes(lib):
+    d = dims()
+    n = hs2.hs2_workspace_bytes(d, 256, 64)
+    assert n > 0 and n % 256 == 0
+    # grows with the cache capacity and the chunk
+    assert hs2.hs2_workspace_bytes(dims(max_len=8192), 256, 64) > n
+    assert hs2.hs2_workspace_bytes(dims(n_queries=8), 256, 64) > n
+    # invalid requests size to 0
+    assert hs2.hs2_workspace_bytes(dims(n_q_heads=30), 256, 64) == 0
+    assert hs2.hs2_workspace_bytes(d, 0, 0) == 0
+    assert hs2.hs2_workspace_bytes(d, -1, 5) == 0
+    assert hs2.hs2_workspace_bytes(dims(head_dim=64), 8, 8) == 0
+
+
+FAKE = 1 << 20  # a 256-byte aligned non-null address; never dereferenced on the error paths
+
+
+def call_full(lib, d, k=16, w=8, ptrs=None, ws_bytes=1 << 40):
+    p = dict(q=FAKE, K=FAKE, V=FAKE, len=FAKE, out=FAKE, idx=FAKE, stats=None, scores=None, ws=FAKE)
+    p.update(ptrs or {})
+    vp = ctypes.c_void_p
+    return lib.hs2_full_attn_score_select(ctypes.byref(d) if d is not None else None, vp(p["q"]), vp(p["K"]),
+                                          vp(p["V"]), vp(p["len"]), k, w, vp(p["out"]), vp(p["idx"]),
+                                          vp(p["stats"]), vp(p["scores"]), vp(p["ws"]), ws_bytes, None)
+
+
+def test_full_attn_rejects_before_launch(lib):
+    d = dims()
+    assert call_full(lib, None) == hs2.HS2_ERR_NULL
+    assert call_full(lib, dims(n_q_heads=30)) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, dims(n_queries=0)) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, dims(n_queries=17)) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, dims(head_dim=64)) == hs2.HS2_ERR_UNSUPPORTED
+    assert call_full(lib, dims(n_q_heads=128, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED  # G = 128
+    assert call_full(lib, dims(n_q_heads=64, n_kv_heads=2, n_queries=8)) == hs2.HS2_ERR_UNSUPPORTED  # 256 rows
+    assert call_full(lib, dims(max_len=0)) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, d, k=0, w=0) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, d, k=-3, w=8) == hs2.HS2_ERR_SHAPE
+    assert call_full(lib, d, ptrs={"q": None}) == hs2.HS2_ERR_NULL
+    assert call_full(lib, d, ptrs={"idx": None}) == hs2.HS2_ERR_NULL
+    assert call_full(lib, d, ptrs={"ws": None}) == hs2.HS2_ERR_NULL
+    assert call_full(lib, d, ptrs={"K": FAKE + 2}) == hs2.HS2_ERR_ALIGN
+    assert call_full(lib, d, ptrs={"ws": FAKE + 16}) == hs2.HS2_ERR_ALIGN
+    assert call_full(lib, dims(kv_strides=(4096 * 128 * 4, 4096 * 128, 130))) == hs2.HS2_ERR_ALIGN
+    need = hs2.hs2_workspace_bytes(d, 16, 8)
+    assert call_full(lib, d, ws_bytes=need - 256) == hs2.HS2_ERR_WORKSPACE
+    assert "workspace" in hs2.hs2_last_error()
+
+
+def test_sparse_and_select_reject_before_launch(lib):
+    d = dims()
+    vp = ctypes.c_void_p
+    st = lib.hs2_sparse_attn(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), 0, vp(FAKE),
+                             vp(FAKE), 1 << 40, None)
+    assert st == hs2.HS2_ERR_SHAPE
+    st = lib.hs2_sparse_attn(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), None, 64, vp(FAKE),
+                             vp(FAKE), 1 << 40, None)
+    assert st == hs2.HS2_ERR_NULL
+    st = lib.hs2_sparse_attn(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), 64, vp(FAKE),
+                             vp(FAKE), 16, None)
+    assert st == hs2.HS2_ERR_WORKSPACE
+    st = lib.hs2_select_from_scores(ctypes.byref(d), None, vp(FAKE), 8, 8, vp(FAKE), vp(FAKE), 1 << 40, None)
+    assert st == hs2.HS2_ERR_NULL
+    st = lib.hs2_select_from_scores(ctypes.byref(d), vp(FAKE + 2), vp(FAKE), 8, 8, vp(FAKE), vp(FAKE), 1 << 40,
+                                    None)
+    assert st == hs2.HS2_ERR_ALIGN
+
+
+def test_status_strings(lib):
+    for code in (hs2.HS2_OK, hs2.HS2_ERR_NULL, hs2.HS2_ERR_SHAPE, hs2.HS2_ERR_UNSUPPORTED, hs2.HS2_ERR_WORKSPACE,
+                 hs2.HS2_ERR_ALIGN, hs2.HS2_ERR_HIP):
+        s = hs2.hs2_status_string(code)
+        assert s and s != "unknown status"
+    assert hs2.hs2_status_string(-99) == "unknown status"
+
+
+def test_binding_checks_shapes_before_calling():
+    import torch
+    d = dims(batch=1, max_len=64)
+    q = torch.zeros((1, 1, 32, 128), dtype=torch.bfloat16)
+    K = torch.zeros((1, 4, 64, 128), dtype=torch.bfloat16)
+    lens = torch.full((1,), 64, dtype=torch.int32)
+    out = torch.zeros((1, 1, 32, 128), dtype=torch.bfloat16)
+    idx_bad = torch.zeros((1, 4, 1, 7), dtype=torch.int32)
+    with pytest.raises(ValueError):
+        hs2.hs2_full_attn_score_select(d, q, K, K, lens, 4, 4, out, idx_bad, workspace=torch.zeros(16))
+    K_short = torch.zeros((1, 4, 32, 128), dtype=torch.bfloat16)
+    idx = torch.zeros((1, 4, 1, 8), dtype=torch.int32)
+    with pytest.raises(ValueError):
+        hs2.hs2_full_attn_score_select(d, q, K_short, K_short, lens, 4, 4, out, idx, workspace=torch.zeros(16))

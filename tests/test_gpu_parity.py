@@ -1,0 +1,224 @@
+"""GPU parity: libhs2.so (through its C ABI) against the CPU oracle.
+
+Every case draws seeded bf16 inputs, runs the hybrid block on the GPU and the
+oracle on the same bits, and checks out / stats / pooled scores / index rows
+/ sparse-layer outputs to the bar in tests/checker.py.  The sparse layers are
+checked twice: chained on the GPU's own selection (when it equals the
+oracle's) and fed the oracle's selection (always).
+"""
+from __future__ import annotations
+
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hs2_oracle as O
+from paper_2609_26368_amd import workloads as W
+from tests import checker as CK
+
+pytestmark = pytest.mark.gpu
+
+
+def _hs2():
+    from paper_2609_26368_amd import hs2
+    return hs2
+
+
+def dev_bf16(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to("cuda").view(torch.bfloat16)
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def note(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(inp, oracle_idx=None):
+    """Hybrid block on the GPU; returns host copies of every result."""
+    hs2 = _hs2()
+    w = inp.w
+    B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
+    Lmax = inp.K.shape[2]
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window)
+    K, V = dev_bf16(inp.K), dev_bf16(inp.V)
+    lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
+    stats = torch.empty((B, C, Hq, 2), dtype=torch.float32, device="cuda")
+    scores = torch.zeros((B, Hkv, C, Lmax), dtype=torch.float32, device="cuda")
+    out, idx = blk.full(dev_bf16(inp.q_fa), K, V, lens, stats=stats, scores=scores)
+    sa = [blk.sparse(dev_bf16(qs), K, V, lens, idx) for qs in inp.q_sa]
+    sa_ref_idx = None
+    if oracle_idx is not None:
+        ridx = torch.from_numpy(oracle_idx).cuda()
+        sa_ref_idx = [blk.sparse(dev_bf16(qs), K, V, lens, ridx) for qs in inp.q_sa]
+    torch.cuda.synchronize()
+    res = {"out": CK.bf16_bits_to_f64(host_bits(out)), "idx": idx.cpu().numpy(), "stats": stats.cpu().numpy(),
+           "scores": scores.cpu().numpy(), "sa": [CK.bf16_bits_to_f64(host_bits(t)) for t in sa]}
+    if sa_ref_idx is not None:
+        res["sa_ref_idx"] = [CK.bf16_bits_to_f64(host_bits(t)) for t in sa_ref_idx]
+    return res
+
+
+def compare(inp, ref, gpu, groups=None):
+    w = inp.w
+    G = w.group
+    rows = None
+    if groups is not None:
+        rows = np.zeros((w.batch, w.n_queries, w.n_q_heads), dtype=bool)
+        for b, g in groups:
+            rows[b, :, g * G:(g + 1) * G] = True
+    r_out = CK.check_out(gpu["out"], ref["out"], "full-attention out", rows)
+    # stats: M natural-log units, Z
+    M, Z = gpu["stats"][..., 0], gpu["stats"][..., 1]
+    sel = rows if rows is not None else np.ones(M.shape, dtype=bool)
+    assert np.allclose(M[sel], ref["M"][sel], rtol=1e-5, atol=1e-5), "stats M"
+    assert np.allclose(Z[sel], ref["Z"][sel], rtol=1e-4), "stats Z"
+    r_sc = CK.check_scores(gpu["scores"], ref["P"], inp.lens, w.n_queries, w.window, groups)
+    r_idx = CK.check_idx(gpu["idx"], ref["idx"], ref["P"], inp.lens, w.n_queries, w.window, groups)
+    for li, qs in enumerate(inp.q_sa):
+        ref_sa = O.sparse_attention(qs, inp.K, inp.V, ref["idx"], groups=groups)
+        CK.check_out(gpu["sa_ref_idx"][li], ref_sa, f"sparse layer {li} (oracle selection)", rows)
+        if r_idx["swaps"] == 0:
+            CK.check_out(gpu["sa"][li], ref_sa, f"sparse layer {li} (own selection)", rows)
+    return {**r_out, **r_sc, **r_idx}
+
+
+def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None):
+    inp = W.make_inputs(w, seed=seed, lmax=lmax)
+    note(f"[parity] {w.name} seed={seed} lens={inp.lens.tolist()} C={w.n_queries} Hq={w.n_q_heads} "
+         f"Hkv={w.n_kv_heads} k={w.k} W={w.window}")
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, groups=groups)
+    gpu = run_gpu(inp, oracle_idx=ref["idx"])
+    r = compare(inp, ref, gpu, groups)
+    note(f"[parity] {w.name}: {r}")
+    return inp, ref, gpu
+
+
+WL = W.WORKLOADS
+SMALL = [
+    WL["decode_4k_16q2kv"],
+    W.shrink(WL["block_32k_32q4kv"], 6173, name="block_32q4kv@6173"),
+    W.shrink(WL["ragged_16k_128k_b8_needles"], 9000, ctx_min=1500, k=512, name="ragged_b8_needles@1.5k-9k"),
+    W.shrink(WL["chunk8_128k_b4"], 5000, k=1024, batch=2, name="chunk8_b2@5000"),
+    W.shrink(WL["stress_512k_b2_64q8kv"], 6001, k=1024, batch=1, name="64q8kv@6001"),
+]
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_parity_small(w):
+    inp, ref, gpu = parity_case(w)
+    if w.needles:
+        for b in range(w.batch):
+            for g in range(w.n_kv_heads):
+                assert set(inp.needles[b].tolist()) <= set(gpu["idx"][b, g, 0].tolist())
+
+
+HEADS = [  # (Hq, Hkv, C): group sizes incl. non-powers of two and the 128-row maximum
+    (12, 4, 1), (8, 8, 3), (16, 1, 2), (32, 1, 4), (64, 1, 2), (8, 1, 16), (6, 2, 5),
+]
+
+
+@pytest.mark.parametrize("Hq,Hkv,C", HEADS, ids=[f"{a}q{b}kv_C{c}" for a, b, c in HEADS])
+def test_parity_head_layouts(Hq, Hkv, C):
+    w = W.Workload(f"heads_{Hq}_{Hkv}_{C}", 2, 1500, C, Hq, Hkv, 128, 200, 48, 2, ctx_min=700)
+    parity_case(w, seed=5)
+
+
+EDGES = [
+    # (name, batch, ctx, ctx_min, C, k, window)
+    ("window_covers_all", 2, 100, 40, 1, 64, 128),
+    ("len_equals_chunk", 1, 4, 0, 4, 8, 2),
+    ("single_token", 1, 1, 0, 1, 5, 3),
+    ("no_window", 1, 777, 0, 2, 100, 0),
+    ("window_only", 1, 900, 0, 3, 0, 50),
+    ("k_exceeds_candidates", 2, 300, 150, 2, 400, 16),
+    ("one_tile_plus_one", 1, 65, 0, 1, 10, 5),
+]
+
+
+@pytest.mark.parametrize("name,B,ctx,ctx_min,C,k,win", EDGES, ids=[e[0] for e in EDGES])
+def test_parity_edges(name, B, ctx, ctx_min, C, k, win):
+    w = W.Workload(name, B, ctx, C, 16, 2, 128, k, win, 1, ctx_min=ctx_min)
+    parity_case(w, seed=7)
+
+
+def test_parity_padded_capacity():
+    """Cache capacity larger than every length (rows past len are never read)."""
+    w = W.Workload("capacity", 3, 1000, 2, 16, 4, 128, 96, 32, 1, ctx_min=300)
+    parity_case(w, seed=9, lmax=1531)
+
+
+def test_strided_cache_layout():
+    """A [B, Lmax, Hkv, D] cache passed through strides gives the same results."""
+    hs2 = _hs2()
+    w = W.Workload("strided", 2, 800, 2, 16, 4, 128, 64, 32, 1, ctx_min=500)
+    inp = W.make_inputs(w, seed=3)
+    B, C, Hq, Hkv, D, L = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim, inp.K.shape[2]
+    Kt = np.ascontiguousarray(inp.K.transpose(0, 2, 1, 3))
+    Vt = np.ascontiguousarray(inp.V.transpose(0, 2, 1, 3))
+    strides = (L * Hkv * D, D, Hkv * D)
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, L, w.k, w.window, kv_strides=strides)
+    K, V = dev_bf16(Kt), dev_bf16(Vt)
+    lens = torch.from_numpy(inp.lens).cuda()
+    out, idx = blk.full(dev_bf16(inp.q_fa), K, V, lens)
+    sa = blk.sparse(dev_bf16(inp.q_sa[0]), K, V, lens, idx)
+    torch.cuda.synchronize()
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window)
+    CK.check_out(CK.bf16_bits_to_f64(host_bits(out)), ref["out"])
+    CK.check_idx(idx.cpu().numpy(), ref["idx"], ref["P"], inp.lens, C, w.window)
+    if (idx.cpu().numpy() == ref["idx"]).all():
+        CK.check_out(CK.bf16_bits_to_f64(host_bits(sa)), O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"]))
+
+
+# ---------------------------------------------------------------- selection alone: bit-exact
+def _select_case(B, Hkv, C, Lmax, lens, k, win, scores):
+    hs2 = _hs2()
+    dims = hs2.make_dims(B, C, 8 * Hkv, Hkv, 128, Lmax)
+    ws = torch.empty(hs2.hs2_workspace_bytes(dims, k, win), dtype=torch.uint8, device="cuda")
+    idx = torch.empty((B, Hkv, C, k + win), dtype=torch.int32, device="cuda")
+    hs2.hs2_select_from_scores(dims, torch.from_numpy(scores).cuda(), torch.from_numpy(lens).cuda(), k, win, idx, ws)
+    torch.cuda.synchronize()
+    got = idx.cpu().numpy()
+    for b in range(B):
+        for g in range(Hkv):
+            for c in range(C):
+                pos = int(lens[b]) - C + c
+                want = O.select_row(scores[b, g, c], pos, k, win)
+                assert np.array_equal(got[b, g, c], want), (b, g, c, got[b, g, c][:20], want[:20])
+
+
+SEL = [
+    # (name, B, Hkv, C, Lmax, k, window, score kind)
+    ("random", 2, 3, 2, 5000, 300, 40, "uniform"),
+    ("heavy_ties", 2, 2, 1, 7000, 500, 16, "ties"),
+    ("all_equal", 1, 2, 1, 3000, 700, 8, "const"),
+    ("denormals_and_zeros", 1, 1, 3, 2000, 100, 10, "tiny"),
+    ("lognormal_long", 1, 2, 1, 200000, 4096, 256, "lognormal"),
+    ("k_equals_N", 1, 1, 1, 1000, 990, 10, "uniform"),
+    ("k_zero", 1, 1, 2, 1000, 0, 10, "uniform"),
+]
+
+
+@pytest.mark.parametrize("name,B,Hkv,C,Lmax,k,win,kind", SEL, ids=[s[0] for s in SEL])
+def test_select_from_scores_exact(name, B, Hkv, C, Lmax, k, win, kind):
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    shape = (B, Hkv, C, Lmax)
+    if kind == "uniform":
+        s = rng.random(shape, dtype=np.float32)
+    elif kind == "ties":
+        s = (rng.integers(0, 50, size=shape) / 64.0).astype(np.float32)
+    elif kind == "const":
+        s = np.full(shape, 0.25, dtype=np.float32)
+    elif kind == "tiny":
+        s = rng.choice(np.array([0.0, 1e-40, 3e-39, 1e-38, 2e-38, 1.0], dtype=np.float32), size=shape)
+    else:
+        s = (np.exp(rng.standard_normal(shape)) / Lmax).astype(np.float32)
+    lens = np.array([Lmax - 17 * b for b in range(B)], dtype=np.int32)
+    note(f"[select] {name} shape={shape} k={k} W={win}")
+    _select_case(B, Hkv, C, Lmax, lens, k, win, s)
