@@ -1,0 +1,195 @@
+"""Benchmark: decode steps of one HySparse2 hybrid block on one MI355X.
+
+A step is the whole hot path over one batch of resident synthetic inputs:
+one full-attention layer with pooled scores and forced-window + top-k
+selection (hs2_full_attn_score_select), then the block's sparse layers
+(hs2_sparse_attn), each with its own queries, reusing the cache and indices.
+
+Default workload: 8-query verify chunk per sequence, batch 4, 131072-token
+context, 32 query / 4 KV heads, head_dim 128, top-k 4096 + window 256,
+1 full + 3 sparse layers (bf16 cache, fp32 accumulation).
+
+Prints one JSON line (rank 0, N = 1).  Extra fields: achieved algorithmic
+GB/s of the step, the roofline of the dominant kernel (full-attention split
+kernel) from HIP events around its launches, per-kernel averages, and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "hybrid-block decode tokens/sec and achieved HBM GB/s at 128K ctx, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "chunk8_128k_b4"
+KERNEL_SOURCES = ["paper_2609_26368_amd/csrc/hs2_kernels.hip", "paper_2609_26368_amd/csrc/hs2_device.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fa_split_traffic_{workload}.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_26368_amd import hs2
+    from paper_2609_26368_amd import workloads as W
+
+    if not os.path.exists(hs2.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    w = W.WORKLOADS[args.workload]
+    t = time.perf_counter()
+    inp = W.make_inputs(w)
+    log(f"[bench] inputs {w.name} generated in {time.perf_counter() - t:.1f}s lens={inp.lens.tolist()}")
+    B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
+    Lmax = inp.K.shape[2]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    K, V = to_dev(inp.K), to_dev(inp.V)
+    q_fa = to_dev(inp.q_fa)
+    q_sa = [to_dev(x) for x in inp.q_sa]
+    lens = torch.from_numpy(inp.lens).to(dev)
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window, device=dev)
+    out = torch.empty((B, C, Hq, D), dtype=torch.bfloat16, device=dev)
+    idx = torch.empty((B, Hkv, C, w.slots), dtype=torch.int32, device=dev)
+    sa_out = [torch.empty_like(out) for _ in q_sa]
+    stream = torch.cuda.current_stream()
+
+    def step():
+        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream)
+        for qs, o in zip(q_sa, sa_out):
+            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} steps done")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = e0.elapsed_time(e1)
+    ms_per_step = ev_ms / args.steps
+    tokens = B * C
+    value = tokens * args.steps / wall
+    log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms")
+
+    # per-kernel durations (HIP events recorded by the library around each launch, same stream)
+    hs2.hs2_timing_enable(True)
+    hs2.hs2_timing_reset()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per = hs2.hs2_timing_read()
+    hs2.hs2_timing_enable(False)
+    kernels = {name: {"launches": n, "avg_us": 1e3 * ms / n} for name, (n, ms) in per.items()}
+
+    # algorithmic bytes (what the method must move; scratch and partials excluded)
+    L = inp.lens.astype(np.int64)
+    kv_row = 2 * D * 2
+    q_bytes = B * C * Hq * D * 2
+    fa_bytes = int(L.sum()) * Hkv * kv_row + q_bytes
+    idx_h = idx.cpu().numpy()
+    uniq = sum(np.unique(idx_h[b, g][idx_h[b, g] >= 0]).size for b in range(B) for g in range(Hkv))
+    step_bytes = (fa_bytes + q_bytes + idx_h.nbytes) + w.n_sparse * (uniq * kv_row + 2 * q_bytes + idx_h.nbytes)
+    fa_avg_s = kernels["fa_split"]["avg_us"] * 1e-6
+    achieved = fa_bytes / fa_avg_s / 1e9
+    traffic = None
+    tf = TRAFFIC_FILE.format(workload=w.name)
+    if os.path.exists(tf):
+        with open(tf) as f:
+            rec = json.load(f)
+        if rec.get("source_hash") == kernel_source_hash():
+            traffic = rec.get("bytes_per_launch")
+    roofline = {"kernel": "fa_split", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": fa_bytes}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, inp, args.cpu_seconds)
+
+    rec = {"metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": w.name, "batch": B, "ctx": w.ctx, "ctx_min": w.ctx_min or w.ctx,
+                      "queries_per_seq": C, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D, "k": w.k,
+                      "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles},
+           "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+           "algorithmic_bytes_per_step": int(step_bytes),
+           "roofline": roofline,
+           "kernels_avg_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
+           "cpu_baseline": cpu}
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(w, inp, budget_s: float) -> dict:
+    """The oracle on (sequence, KV head) groups of the same inputs until the
+    budget is spent; scaled to tokens/s of whole steps."""
+    from oracle import hs2_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        threads = 1
+    groups_all = [(b, g) for b in range(w.batch) for g in range(w.n_kv_heads)]
+    done, t0 = [], time.perf_counter()
+    for bg in groups_all:
+        O.hybrid_block(inp.q_fa, inp.q_sa, inp.K, inp.V, inp.lens, w.k, w.window, groups=[bg])
+        done.append(bg)
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    step_s = el * len(groups_all) / len(done)
+    log(f"[bench] oracle: {len(done)} of {len(groups_all)} groups in {el:.1f}s")
+    return {"value": round(w.batch * w.n_queries / step_s, 4), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{len(done)} of {len(groups_all)} (sequence, KV head) groups of one step, full context, "
+                      f"{el:.1f}s; scaled by {len(groups_all)}/{len(done)}"}
+
+
+if __name__ == "__main__":
+    main()

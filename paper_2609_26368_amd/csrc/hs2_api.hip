@@ -14,6 +14,7 @@
 #include <string>
 #include <vector>
 
+#include "hs2_device.h"
 #include "hs2_launch.h"
 
 namespace {
@@ -25,8 +26,8 @@ constexpr int kMaxQueries = 16;
 constexpr int kMaxRows = 128;           // C * Gp
 constexpr int kMaxGroup = 64;
 constexpr int32_t kMaxLen = 1 << 27;
-constexpr int kNBins = 2048;
-constexpr int kSelChunk = 16384;        // tokens per workgroup of the selection scans
+constexpr int kNBins = 1024;          // must match the kernels' first-level radix bins
+constexpr int kSelChunk = hs2::SEL_CHUNK;  // tokens per workgroup of the selection scans
 constexpr size_t kAlign = 256;
 
 thread_local std::string g_last_error;
@@ -60,6 +61,7 @@ struct Plan {
   int B, C, Hq, Hkv, G, Gp, D, Lmax, k, W, S;
   float c2;
   int RT, TG;                 // full-attention / pooling row tiles
+  int fa_variant;             // 0: one-wave ring kernel (RT <= 4), 1: workgroup kernel
   int fa_split, fa_nsplit;
   int pool_split, pool_nsplit;
   int64_t units;              // B * Hkv
@@ -128,12 +130,15 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
   p.c2 = (float)(scale * 1.4426950408889634);
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
-  p.TG = p.RT >= 4 ? 1 : 4 / p.RT;
+  p.fa_variant = env_int("HS2_FA_VARIANT", 0);
+  p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
   p.rows = p.units * p.C;
-  // token splits: about 1024 workgroups over the whole cache, whole 64-token tiles
+  // token splits over the whole cache: about 4096 / RT one-wave workgroups
+  // (partials cost 16 RT rows per split), whole 64-token tiles
   const int64_t total = p.units * (int64_t)p.Lmax;
-  int split = (int)std::max<int64_t>(256, round_up(cdiv(total, 1024), 64));
+  const int target_wgs = p.fa_variant == 1 || p.RT >= 8 ? 1024 : 4096 / p.RT;
+  int split = (int)std::max<int64_t>(256, round_up(cdiv(total, target_wgs), 64));
   split = env_int("HS2_FA_SPLIT", split);
   split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, p.Lmax), 64));
   p.fa_split = split;
@@ -151,7 +156,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
   const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
   size_t cur = 0;
   p.off_part_o = carve(cur, sizeof(float) * p.units * nslot * prow * kHeadDim);
-  p.off_part_ml = carve(cur, sizeof(float) * p.units * nslot * prow * 2);
+  p.off_part_ml = carve(cur, sizeof(float) * p.units * nslot * prow * 4);
   p.off_stats = carve(cur, sizeof(float) * (size_t)p.B * p.C * p.Hq * 2);
   p.off_scores = carve(cur, sizeof(float) * p.rows * p.score_stride);
   p.off_hist = carve(cur, sizeof(uint32_t) * p.rows * kNBins);
@@ -174,7 +179,7 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
   const int64_t prow = 16 * s.RT;
   size_t cur = 0;
   s.off_part_o = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * kHeadDim);
-  s.off_part_ml = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * 2);
+  s.off_part_ml = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * 4);
   s.bytes = (size_t)round_up((int64_t)cur, kAlign);
 }
 
@@ -342,7 +347,7 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   fa.max_len = p.Lmax;
   fa.split_tokens = p.fa_split;
   fa.n_split = p.fa_nsplit;
-  HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, s));
+  HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, p.fa_variant, s));
 
   CombineArgs ca{};
   ca.part_o = fa.part_o;

@@ -26,9 +26,11 @@ constexpr int TILE = 64;        // cache rows per LDS stage
 constexpr int NT = 256;         // threads per workgroup
 constexpr int KPAD = HD + 8;    // K / Q row stride in LDS (bf16): 272 B, conflict-free 16-B reads
 constexpr int VPAD = TILE + 4;  // Vt row stride in LDS (bf16): 136 B
-constexpr int NBINS = 2048;     // first-level radix bins of the pooled-score keys
-constexpr int DIGIT_SHIFT = 18; // key >> 18 = 8 exponent bits + 5 mantissa bits
-constexpr int DIGIT_BASE = 2240;// (exp 133, mant 31) -> bin 2047; P <= 64 < 128 always fits
+constexpr int SEL_CHUNK = 4096;  // tokens per workgroup of the selection scans
+constexpr int NBINS = 1024;     // first-level radix bins of the pooled-score keys
+constexpr int DIGIT_SHIFT = 19; // key >> 19 = 8 exponent bits + 4 mantissa bits (1/16 binade)
+constexpr int DIGIT_BASE = 1120;// (exp 133, mant 15) -> bin 1023: 64 binades below 128 > P;
+                                // P < 2^-56 all fall into bin 0
 
 struct TileLds {
   uint16_t k[TILE * KPAD];
@@ -44,6 +46,13 @@ __device__ inline uint32_t f32_to_bf16_bits(float f) {
   uint32_t u = __float_as_uint(f);
   u += 0x7FFFu + ((u >> 16) & 1u);
   return u >> 16;
+}
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// two fp32 -> packed bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32)
+__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
 __device__ inline f32x4 mfma_k32(const uint4& a, const uint4& b, f32x4 c) {
@@ -121,19 +130,22 @@ __device__ inline void store_tile(TileLds& s, const TileRegs& r, int tid) {
 }
 
 // ---------------------------------------------------------------- wave-level attention state
-// One wave, RPW row tiles of 16 query rows.  m: running max of log2-domain
-// logits of row (lane & 15) (same in all four lane groups); l: this lane's
-// share of the running sum; o: unnormalised output rows 4(lane/16)+i,
-// columns 16*nb + (lane & 15).
+// One wave, RPW row tiles of 16 query rows, for row (lane & 15) (same in all
+// four lane groups): m is the reference the probabilities exp2(s - m) are
+// taken against, mt the true running maximum of the log2-domain logits; l is
+// this lane's share of the running sum; o holds the unnormalised output rows
+// 4(lane/16)+i, columns 16*nb + (lane & 15).
 template <int RPW>
 struct WaveState {
-  float m[RPW];
+  float m[RPW];   // reference maximum the probabilities are taken against
+  float mt[RPW];  // true running maximum (for the reported statistics)
   float l[RPW];
   f32x4 o[RPW][8];
   __device__ inline void init() {
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
       m[r] = -INFINITY;
+      mt[r] = -INFINITY;
       l[r] = 0.f;
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) o[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -158,25 +170,38 @@ __device__ inline void qk_block(const TileLds& s, int blk, const uint4 (&q)[RPW]
   }
 }
 
-// Online-softmax update with BPW blocks of log2-domain logits (masked = -inf),
-// then O += P . V over those blocks.
+// Online-softmax update of a wave's state with BPW blocks of log2-domain
+// logits (masked = -inf); returns the bf16 probabilities as P.V A operands.
+// The reference maximum m is raised only when a logit exceeds it by more
+// than LAZY_MARGIN, so probabilities stay <= 2^LAZY_MARGIN and the
+// accumulators are rescaled rarely; the true maximum is tracked in mt.
+constexpr float LAZY_MARGIN = 8.f;
+
 template <int RPW, int BPW>
-__device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const int (&blk)[BPW],
-                                  f32x4 (&S)[BPW][RPW], int lane) {
-  uint2 pa[BPW][RPW];
+__device__ inline void online_softmax(WaveState<RPW>& st, f32x4 (&S)[BPW][RPW], uint2 (&pa)[BPW][RPW], int lane) {
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     float mx = -INFINITY;
 #pragma unroll
     for (int bi = 0; bi < BPW; ++bi)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S[bi][rr][i]);
+      mx = fmaxf(mx, fmaxf(fmaxf(S[bi][rr][0], S[bi][rr][1]), fmaxf(S[bi][rr][2], S[bi][rr][3])));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(st.m[rr], mx);
-    const float msub = (mnew == -INFINITY) ? 0.f : mnew;
-    const float alpha = fast_exp2(st.m[rr] - msub);  // m = -inf -> 0; unchanged max -> 1
-    st.m[rr] = mnew;
+    st.mt[rr] = fmaxf(st.mt[rr], mx);
+    if (__ballot(mx > st.m[rr] + LAZY_MARGIN)) {
+      const float mnew = fmaxf(st.m[rr], mx);
+      const float alpha = mnew == -INFINITY ? 1.f : fast_exp2(st.m[rr] - mnew);  // m = -inf -> 0
+      st.m[rr] = mnew;
+      st.l[rr] *= alpha;
+      float a4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * (lane >> 4) + i);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st.o[rr][nb][i] *= a4[i];
+    }
+    const float msub = st.m[rr] == -INFINITY ? 0.f : st.m[rr];
     float psum = 0.f;
 #pragma unroll
     for (int bi = 0; bi < BPW; ++bi) {
@@ -186,20 +211,19 @@ __device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const in
         p[i] = fast_exp2(S[bi][rr][i] - msub);
         psum += p[i];
       }
-      pa[bi][rr].x = f32_to_bf16_bits(p[0]) | (f32_to_bf16_bits(p[1]) << 16);
-      pa[bi][rr].y = f32_to_bf16_bits(p[2]) | (f32_to_bf16_bits(p[3]) << 16);
+      pa[bi][rr].x = pack_bf16x2(p[0], p[1]);
+      pa[bi][rr].y = pack_bf16x2(p[2], p[3]);
     }
-    st.l[rr] = st.l[rr] * alpha + psum;
-    if (__ballot(alpha != 1.f)) {
-      float a4[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * (lane >> 4) + i);
-#pragma unroll
-      for (int nb = 0; nb < 8; ++nb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) st.o[rr][nb][i] *= a4[i];
-    }
+    st.l[rr] += psum;
   }
+}
+
+// Online softmax + O += P . V with V transposed in LDS (Vt[d][row]).
+template <int RPW, int BPW>
+__device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const int (&blk)[BPW],
+                                  f32x4 (&S)[BPW][RPW], int lane) {
+  uint2 pa[BPW][RPW];
+  online_softmax<RPW, BPW>(st, S, pa, lane);
 #pragma unroll
   for (int bi = 0; bi < BPW; ++bi) {
     const uint16_t* vp = &s.vt[(lane & 15) * VPAD + 16 * blk[bi] + 4 * (lane >> 4)];
@@ -212,7 +236,7 @@ __device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const in
   }
 }
 
-// Write one wave's partial (m, l, O) for its RPW row tiles.
+// Write one wave's partial for its RPW row tiles: (m ref, l, m true, 0) and O.
 template <int RPW>
 __device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict__ part_o,
                                      float* __restrict__ part_ml, int64_t slot_base_row, int rt0, int lane) {
@@ -222,10 +246,7 @@ __device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict
     l += __shfl_xor(l, 16);
     l += __shfl_xor(l, 32);
     const int64_t row0 = slot_base_row + 16 * (rt0 + rr);
-    if (lane < 16) {
-      part_ml[(row0 + lane) * 2] = st.m[rr];
-      part_ml[(row0 + lane) * 2 + 1] = l;
-    }
+    if (lane < 16) *(float4*)(part_ml + (row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float* dst = part_o + (row0 + 4 * (lane >> 4) + i) * HD + (lane & 15);
@@ -234,5 +255,151 @@ __device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict
     }
   }
 }
+
+
+// ---------------------------------------------------------------- direct-to-LDS staging (swizzled)
+// One stage holds TILE cache rows of K then TILE rows of V, 256 bytes each,
+// row-major; the 16-byte chunk c of row r sits at position c ^ (r & 15) of
+// the row, which makes both the MFMA K-operand reads and the transposing V
+// reads free of bank conflicts.  A wave's 16-byte direct LDS load writes
+// 64 consecutive 16-byte slots (lane order): load n = 4 * wave + u fills
+// slots 64 n + lane, i.e. row 4 n + lane / 16, position lane % 16.
+constexpr int STAGE_ROW_BYTES = HD * 2;
+constexpr int STAGE_KV_BYTES = TILE * STAGE_ROW_BYTES;  // 16 KB
+constexpr int STAGE_BYTES = 2 * STAGE_KV_BYTES;         // K + V
+constexpr int FA_STAGES = 4;
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) const void* global_cvoid_ptr;
+typedef short i16x4_lds __attribute__((ext_vector_type(4)));
+
+// NW waves share the loads of a stage: LPW = 16 / NW loads of 1 KB per
+// matrix per wave; load n = LPW * wave + u fills rows 4 n .. 4 n + 3.
+template <int NW>
+__device__ inline int stage_row(int wave, int u, int lane) {
+  return 4 * ((16 / NW) * wave + u) + (lane >> 4);
+}
+
+// One 16-byte-per-lane direct LDS load: lane i's 16 bytes from `src` land at
+// LDS byte address lds_base + 16 i.  Issued as inline assembly so that the
+// compiler does not guard every later LDS read with a wait for all
+// outstanding loads; the caller waits explicitly (wait_stage_loads) and
+// then synchronises the workgroup before reading the stage.
+__device__ inline void dma16(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_base) : "memory");
+}
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Issue this wave's share of one stage: rows tok[u] (u < 16 / NW) of K and V.
+template <int NW>
+__device__ inline void issue_stage_loads(unsigned char* stage, const uint16_t* Kbg, const uint16_t* Vbg,
+                                         int64_t stride_t, const int* tok, int wave, int lane) {
+  constexpr int LPW = 16 / NW;
+  const uint32_t base = lds_addr(stage);
+#pragma unroll
+  for (int u = 0; u < LPW; ++u) {
+    const int n = LPW * wave + u;
+    const int r = stage_row<NW>(wave, u, lane);
+    const int c = (lane & 15) ^ (r & 15);
+    const int64_t off = (int64_t)tok[u] * stride_t + 8 * c;
+    dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+    dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + STAGE_KV_BYTES + 1024 * n));
+  }
+}
+
+// s_waitcnt until at most `tiles` stages of this wave's loads (2 * 16 / NW
+// each) are outstanding.  gfx9 encoding: vmcnt = bits [3:0] | [15:14];
+// expcnt [6:4] and lgkmcnt [11:8] stay at their maxima.
+template <int NW>
+__device__ inline void wait_stage_loads(int tiles) {
+  if (NW == 4) {
+    if (tiles <= 0) __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
+    else if (tiles == 1) __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+    else __builtin_amdgcn_s_waitcnt(0x4F70);                  // vmcnt(16)
+  } else {
+    if (tiles <= 0) __builtin_amdgcn_s_waitcnt(0x0F70);       // vmcnt(0)
+    else if (tiles == 1) __builtin_amdgcn_s_waitcnt(0x0F74);  // vmcnt(4)
+    else __builtin_amdgcn_s_waitcnt(0x0F78);                  // vmcnt(8)
+  }
+}
+
+template <int RPW>
+__device__ inline void qk_block_swz(const unsigned char* stg, int blk, const uint4 (&q)[RPW][4], f32x4 (&S)[RPW],
+                                    int lane) {
+  const int row = 16 * blk + (lane & 15);
+  const unsigned char* rp = stg + row * STAGE_ROW_BYTES;
+  uint4 a4[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) a4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(a4[kk], q[rr][kk], acc);
+    S[rr] = acc;
+  }
+}
+
+// V operand of P.V for block blk, columns 16 nb .. 16 nb + 15 (16x16x16 B layout),
+// read transposed from the row-major stage.
+__device__ inline uint2 v_operand_tr(const unsigned char* stg, int blk, int nb, int lane) {
+  const int kq = lane & 15;
+  const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
+  const int col = 16 * nb + 4 * (kq & 3);
+  const int pos = (col >> 3) ^ (row & 15);
+  const unsigned char* p = stg + STAGE_KV_BYTES + row * STAGE_ROW_BYTES + 16 * pos + 2 * (col & 7);
+  const i16x4_lds v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_lds*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+template <int RPW, int BPW>
+__device__ inline void softmax_pv_swz(WaveState<RPW>& st, const unsigned char* stg, const int (&blk)[BPW],
+                                      f32x4 (&S)[BPW][RPW], int lane) {
+  uint2 pa[BPW][RPW];
+  online_softmax<RPW, BPW>(st, S, pa, lane);
+#pragma unroll
+  for (int bi = 0; bi < BPW; ++bi) {
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) {
+      const uint2 vb = v_operand_tr(stg, blk[bi], nb, lane);
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+    }
+  }
+}
+
+
+// ---------------------------------------------------------------- wave-private staging
+// A one-wave workgroup streams its own token range through a private ring of
+// NS stages, each holding TW rows of K then TW rows of V (swizzled as above).
+// No workgroup barrier: the wave only waits for its own direct LDS loads.
+constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+// s_waitcnt vmcnt(per_stage * stages) for stages in [0, 3]
+template <int PER_STAGE>
+__device__ inline void wait_ring(int stages) {
+  switch (stages) {
+    case 0: __builtin_amdgcn_s_waitcnt(vmcnt_enc(0)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(vmcnt_enc(PER_STAGE)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(vmcnt_enc(2 * PER_STAGE)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_enc(3 * PER_STAGE)); break;
+  }
+}
+
+// V operand of P.V for block blk, columns 16 nb .. 16 nb + 15, read
+// transposed from the row-major swizzled V rows at `vbase`.
+__device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int nb, int lane) {
+  const int kq = lane & 15;
+  const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
+  const int col = 16 * nb + 4 * (kq & 3);
+  const int pos = (col >> 3) ^ (row & 15);
+  const unsigned char* p = vbase + row * STAGE_ROW_BYTES + 16 * pos + 2 * (col & 7);
+  const i16x4_lds v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_lds*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
 
 }  // namespace hs2

@@ -42,16 +42,27 @@ __device__ inline void load_q_tile(uint4 (&q)[4], const uint16_t* __restrict__ q
 }
 
 // ============================================================================ full attention
-// grid (n_split, Hkv, B), 256 threads.  Waves split the work of one LDS tile:
-// RT <= 2: TG = 4 / RT token groups, each wave one row tile and BPW = RT blocks;
-// RT >= 4: each wave RT / 4 row tiles and all four 16-row blocks.
+// grid (n_split, Hkv, B), 64 * NW threads, dynamic LDS = FA_STAGES * STAGE_BYTES.
+// Cache rows stream global -> LDS with no register staging (16-byte direct
+// LDS loads), FA_STAGES - 1 tiles in flight while one is computed; a single
+// barrier per tile.  NW = 4 waves for up to 32 query rows, 8 above (two
+// waves per SIMD).  The waves form RTW row-tile groups x TGN token groups:
+// each wave owns RPW row tiles and BPW of the four 16-row blocks of a tile.
 template <int RT>
-__global__ __launch_bounds__(NT) void k_fa_split(FaArgs a) {
-  constexpr int TG = RT >= 4 ? 1 : 4 / RT;
-  constexpr int RPW = RT >= 4 ? RT / 4 : 1;
-  constexpr int BPW = 4 / TG;
-  constexpr int WPT = 4 / TG;  // waves per token group
-  __shared__ TileLds lds;
+struct FaShape {
+  static constexpr int NW = RT >= 4 ? 8 : 4;
+  static constexpr int RTW = RT < NW ? RT : NW;
+  static constexpr int TGN = NW / RTW;
+  static constexpr int RPW = RT / RTW;
+  static constexpr int BPW = 4 / TGN;
+};
+
+template <int RT>
+__global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
+  using SH = FaShape<RT>;
+  constexpr int NW = SH::NW, RPW = SH::RPW, BPW = SH::BPW, TG = SH::TGN, RTW = SH::RTW;
+  constexpr int LPW = 16 / NW;
+  extern __shared__ __align__(16) unsigned char smem[];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -59,8 +70,9 @@ __global__ __launch_bounds__(NT) void k_fa_split(FaArgs a) {
   const int t_begin = split * a.split_tokens;
   if (t_begin >= Lv) return;
   const int t_end = min(Lv, t_begin + a.split_tokens);
-  const int tg = wave / WPT;
-  const int rt0 = (wave % WPT) * RPW;
+  const int ntiles = (t_end - t_begin + TILE - 1) / TILE;
+  const int tg = wave / RTW;
+  const int rt0 = (wave % RTW) * RPW;
 
   uint4 q[RPW][4];
 #pragma unroll
@@ -77,7 +89,17 @@ __global__ __launch_bounds__(NT) void k_fa_split(FaArgs a) {
   const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
   const uint16_t* Kbg = a.K + kvoff;
   const uint16_t* Vbg = a.V + kvoff;
-  const int cg = tid & 15;
+
+  auto issue = [&](int tile) {
+    const int t0 = t_begin + tile * TILE;
+    int tok[LPW];
+#pragma unroll
+    for (int u = 0; u < LPW; ++u) {
+      const int t = t0 + stage_row<NW>(wave, u, lane);
+      tok[u] = t < t_end ? t : t_end - 1;  // rows past the range repeat a valid row; masked below
+    }
+    issue_stage_loads<NW>(smem + (tile % FA_STAGES) * STAGE_BYTES, Kbg, Vbg, a.stride_t, tok, wave, lane);
+  };
 
   WaveState<RPW> st;
   st.init();
@@ -85,47 +107,34 @@ __global__ __launch_bounds__(NT) void k_fa_split(FaArgs a) {
 #pragma unroll
   for (int bi = 0; bi < BPW; ++bi) blk[bi] = tg * BPW + bi;
 
-  TileRegs regs;
-  {
-    int tok[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int t = t_begin + row_of(tid, u);
-      tok[u] = t < t_end ? t : -1;
-    }
-    load_tile<true>(regs, Kbg, Vbg, a.stride_t, tok, cg);
-  }
-  for (int t0 = t_begin; t0 < t_end; t0 += TILE) {
+  for (int i = 0; i < FA_STAGES - 1; ++i)
+    if (i < ntiles) issue(i);
+  for (int i = 0; i < ntiles; ++i) {
+    // stages issued after tile i by this wave: min(FA_STAGES - 2, ntiles - 1 - i)
+    wait_stage_loads<NW>(min(FA_STAGES - 2, ntiles - 1 - i));
     __syncthreads();
-    store_tile<true>(lds, regs, tid);
-    __syncthreads();
-    if (t0 + TILE < t_end) {
-      int tok[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int t = t0 + TILE + row_of(tid, u);
-        tok[u] = t < t_end ? t : -1;
-      }
-      load_tile<true>(regs, Kbg, Vbg, a.stride_t, tok, cg);
-    }
+    if (i + FA_STAGES - 1 < ntiles) issue(i + FA_STAGES - 1);
+    const unsigned char* stg = smem + (i % FA_STAGES) * STAGE_BYTES;
+    const int t0 = t_begin + i * TILE;
     f32x4 S[BPW][RPW];
 #pragma unroll
-    for (int bi = 0; bi < BPW; ++bi) qk_block<RPW>(lds, blk[bi], q, S[bi], lane);
+    for (int bi = 0; bi < BPW; ++bi) qk_block_swz<RPW>(stg, blk[bi], q, S[bi], lane);
     const bool full = (t0 + TILE <= t_end) && (t0 + TILE - 1 <= min_pos);
 #pragma unroll
     for (int bi = 0; bi < BPW; ++bi)
 #pragma unroll
       for (int rr = 0; rr < RPW; ++rr)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = S[bi][rr][i] * a.c2;
+        for (int ii = 0; ii < 4; ++ii) {
+          float v = S[bi][rr][ii] * a.c2;
           if (!full) {
-            const int t = t0 + 16 * blk[bi] + 4 * (lane >> 4) + i;
+            const int t = t0 + 16 * blk[bi] + 4 * (lane >> 4) + ii;
             if (t >= t_end || t > rpos[rr]) v = -INFINITY;
           }
-          S[bi][rr][i] = v;
+          S[bi][rr][ii] = v;
         }
-    softmax_pv<RPW, BPW>(st, lds, blk, S, lane);
+    softmax_pv_swz<RPW, BPW>(st, stg, blk, S, lane);
   }
   const int nslot = a.n_split * TG;
   const int64_t unit = (int64_t)b * a.Hkv + g;
@@ -133,14 +142,127 @@ __global__ __launch_bounds__(NT) void k_fa_split(FaArgs a) {
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
 }
 
+// ---------------------------------------------------------------------------- ring variant
+// grid (n_split, Hkv, B), 64 * NWV threads (NWV = 1 or 2 waves), dynamic LDS
+// = NS stages of TW rows of K and V.  The workgroup owns a contiguous token
+// split of one (b, g); each wave owns RT / NWV query row tiles.  The split
+// streams through a private ring with NS - 1 stages in flight; with one wave
+// there is no barrier at all, with two waves one barrier per stage.  One
+// partial (m, l, O) per split.
+template <int RT, int NWV, int TW, int NS>
+__global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
+  constexpr int RPW = RT / NWV;
+  constexpr int NB = TW / 16;             // 16-row blocks per stage
+  constexpr int LPM = TW / 4 / NWV;       // 1 KB loads per matrix per stage per wave
+  constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int Lv = clamp_len(a.len, b, a.max_len);
+  const int t_begin = split * a.split_tokens;
+  if (t_begin >= Lv) return;
+  const int t_end = min(Lv, t_begin + a.split_tokens);
+  const int ntiles = (t_end - t_begin + TW - 1) / TW;
+  const int rt0 = wave * RPW;
+
+  uint4 q[RPW][4];
+  int rpos[RPW];
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) {
+    load_q_tile(q[rr], a.q, rt0 + rr, lane, a.Gp, a.G, a.C, a.Hq, g, b);
+    const int c = (16 * (rt0 + rr) + (lane & 15)) / a.Gp;
+    rpos[rr] = c < a.C ? Lv - a.C + c : Lv - 1;  // padding rows see everything
+  }
+  const int min_pos = Lv - a.C;
+  const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
+  const uint16_t* Kbg = a.K + kvoff;
+  const uint16_t* Vbg = a.V + kvoff;
+  const uint32_t ring = lds_addr(smem);
+
+  // per-lane part of each load's element offset: row * stride + swizzled chunk
+  int64_t lane_off[LPM];
+#pragma unroll
+  for (int u = 0; u < LPM; ++u) {
+    const int row = 4 * (wave * LPM + u) + (lane >> 4);
+    lane_off[u] = (int64_t)row * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+  }
+  auto issue = [&](int tile) {
+    const int t0 = t_begin + tile * TW;
+    const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
+    const bool whole = t0 + TW <= t_end;
+    const int64_t tile_off = (int64_t)t0 * a.stride_t;
+#pragma unroll
+    for (int u = 0; u < LPM; ++u) {
+      const int n = wave * LPM + u;
+      int64_t off = tile_off + lane_off[u];
+      if (!whole) {  // rows past the range repeat the last valid row; masked below
+        const int row = 4 * n + (lane >> 4);
+        const int t = min(t0 + row, t_end - 1);
+        off = (int64_t)t * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+      }
+      dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * STAGE_ROW_BYTES + 1024 * n));
+    }
+  };
+
+  WaveState<RPW> st;
+  st.init();
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < ntiles) issue(i);
+  for (int i = 0; i < ntiles; ++i) {
+    wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
+    if (NWV > 1) __syncthreads();
+    if (i + NS - 1 < ntiles) issue(i + NS - 1);
+    const unsigned char* stg = smem + (i % NS) * SB;
+    const int t0 = t_begin + i * TW;
+    f32x4 S[NB][RPW];
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    const bool full = (t0 + TW <= t_end) && (t0 + TW - 1 <= min_pos);
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          float v = S[bi][rr][ii] * a.c2;
+          if (!full) {
+            const int t = t0 + 16 * bi + 4 * (lane >> 4) + ii;
+            if (t >= t_end || t > rpos[rr]) v = -INFINITY;
+          }
+          S[bi][rr][ii] = v;
+        }
+    uint2 pa[NB][RPW];
+    online_softmax<RPW, NB>(st, S, pa, lane);
+    const unsigned char* vbase = stg + TW * STAGE_ROW_BYTES;
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const uint2 vb = v_operand_tr_at(vbase, bi, nb, lane);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+      }
+  }
+  const int64_t unit = (int64_t)b * a.Hkv + g;
+  const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
+  store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
+}
+
 // ============================================================================ combine
-// grid (rows_per_unit, units), 128 threads (one per head-dim element).
+// grid (rows_per_unit, units), 256 threads = 8 slot groups x 32 column quads.
 // FA: unit = (b, g), row r = c * Gp + h; slots valid = ceil(Lv / split) * TG.
 // SA: unit = (b, g, c), row = h; all n_split * TG slots written.
-__global__ __launch_bounds__(HD) void k_combine(CombineArgs a) {
+__global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
+  __shared__ float s_wmax[8];
+  __shared__ float s_z[8];
+  __shared__ float4 s_o[8][32];
   const int r = blockIdx.x;
   const int64_t unit = blockIdx.y;
-  const int d = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sg = tid >> 5, dq = tid & 31;
   int b, g, c, h;
   if (a.sa_mode) {
     c = (int)(unit % a.C);
@@ -159,49 +281,181 @@ __global__ __launch_bounds__(HD) void k_combine(CombineArgs a) {
     const int Lv = clamp_len(a.len, b, a.max_len);
     nvalid = ((Lv + a.split_tokens - 1) / a.split_tokens) * a.tg;
   }
-  const int64_t base = unit * a.nslot * a.rows;
-  float M = -INFINITY;
-  for (int s = 0; s < nvalid; ++s) M = fmaxf(M, a.part_ml[(base + (int64_t)s * a.rows + r) * 2]);
-  float Z = 0.f, acc = 0.f;
+  const int64_t base = unit * a.nslot * a.rows + r;
+  // largest reference maximum and largest true maximum of the partials
+  float M = -INFINITY, Mt = -INFINITY;
+  for (int s = tid; s < nvalid; s += 256) {
+    const float4 ml = *(const float4*)(a.part_ml + (base + (int64_t)s * a.rows) * 4);
+    M = fmaxf(M, ml.x);
+    Mt = fmaxf(Mt, ml.z);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    M = fmaxf(M, __shfl_xor(M, o));
+    Mt = fmaxf(Mt, __shfl_xor(Mt, o));
+  }
+  if (lane == 0) {
+    s_wmax[wave] = M;
+    s_wmax[4 + wave] = Mt;
+  }
+  __syncthreads();
+  M = fmaxf(fmaxf(s_wmax[0], s_wmax[1]), fmaxf(s_wmax[2], s_wmax[3]));
+  Mt = fmaxf(fmaxf(s_wmax[4], s_wmax[5]), fmaxf(s_wmax[6], s_wmax[7]));
+  float z = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (M != -INFINITY) {
-    for (int s = 0; s < nvalid; ++s) {
-      const int64_t pr = base + (int64_t)s * a.rows + r;
-      const float m = a.part_ml[pr * 2];
+    for (int s = sg; s < nvalid; s += 8) {
+      const int64_t pr = base + (int64_t)s * a.rows;
+      const float m = a.part_ml[pr * 4];
       if (m == -INFINITY) continue;
       const float w = fast_exp2(m - M);
-      Z += a.part_ml[pr * 2 + 1] * w;
-      acc += a.part_o[pr * HD + d] * w;
+      z += a.part_ml[pr * 4 + 1] * w;
+      const float4 o = *(const float4*)(a.part_o + pr * HD + 4 * dq);
+      acc.x += o.x * w;
+      acc.y += o.y * w;
+      acc.z += o.z * w;
+      acc.w += o.w * w;
     }
   }
-  const float o = Z > 0.f ? acc / Z : 0.f;
+  s_o[sg][dq] = acc;
+  if (dq == 0) s_z[sg] = z;
+  __syncthreads();
+  if (sg != 0) return;
+  float Z = 0.f;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    Z += s_z[j];
+    o.x += s_o[j][dq].x;
+    o.y += s_o[j][dq].y;
+    o.z += s_o[j][dq].z;
+    o.w += s_o[j][dq].w;
+  }
+  const float inv = Z > 0.f ? 1.f / Z : 0.f;
   const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
-  a.out[orow * HD + d] = (uint16_t)f32_to_bf16_bits(o);
-  if (d == 0) {
+  uint2 packed;
+  packed.x = f32_to_bf16_bits(o.x * inv) | (f32_to_bf16_bits(o.y * inv) << 16);
+  packed.y = f32_to_bf16_bits(o.z * inv) | (f32_to_bf16_bits(o.w * inv) << 16);
+  *(uint2*)(a.out + orow * HD + 4 * dq) = packed;
+  if (dq == 0) {
     if (a.stats_log2) {
       a.stats_log2[orow * 2] = M;
       a.stats_log2[orow * 2 + 1] = Z;
     }
-    if (a.stats_user) {
-      a.stats_user[orow * 2] = M == -INFINITY ? M : M * 0.69314718055994531f;
-      a.stats_user[orow * 2 + 1] = Z;
+    if (a.stats_user) {  // against the true maximum: Z * 2^(M - Mt), M <= Mt
+      a.stats_user[orow * 2] = Mt == -INFINITY ? Mt : Mt * 0.69314718055994531f;
+      a.stats_user[orow * 2 + 1] = Mt == -INFINITY ? 0.f : Z * fast_exp2(M - Mt);
     }
   }
 }
 
 // ============================================================================ pooled scores
-// grid (n_split, Hkv, B), 256 threads; wave w handles 16-row block w of every
-// LDS tile, for all RT query row tiles (queries read from LDS).
-template <int RT>
+// grid (n_split, Hkv, B), 256 threads.  Each wave streams its own 64-token
+// groups (wave w: groups w, w + 4, ...) with K rows loaded straight into MFMA
+// operand registers, double-buffered; queries come from LDS.  Logits are
+// computed as S = Q . K^T (query rows on MFMA rows), so lane l holds rows
+// 4(l/16)+i of token l%16: the GP heads of a query are summed inside the
+// lane and across at most two lane groups, and the 16 scores of a block are
+// written by 16 consecutive lanes.  Per token and row the probability is
+// exp2(s2 - msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless M2 is
+// too large for that, then msub = M2 and fac = 1 / Z).
+struct PoolCtx {
+  float* scores;          // row of query 0 of this (b, g)
+  int64_t score_stride;
+  uint32_t* hist;         // LDS [C][NBINS/2], 16-bit packed counters
+  int nc0;                // candidates of query 0: Lv - C - W + 1 (query c: nc0 + c)
+  int C;
+};
+
+__device__ inline void pool_emit(const PoolCtx& p, float v, int c, int t) {
+  if (c < p.C && t < p.nc0 + c) {
+    p.scores[c * p.score_stride + t] = v;
+    const int dg = score_digit(score_key(v));
+    atomicAdd(&p.hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+  }
+}
+
+template <int RT, int GP>
+__device__ inline void pool_group(const PoolCtx& p, float c2, const uint4 (&kb)[4][4], int tg0, const uint16_t* qs,
+                                  const float (&fac)[RT][4], const float (&msub)[RT][4], int lane) {
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) {
+    const int t = tg0 + 16 * blk + (lane & 15);  // this lane's token
+    float e[RT][4];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const uint16_t* qp = qs + (16 * rt + (lane & 15)) * KPAD + 8 * q4;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(*(const uint4*)(qp + 32 * kk), kb[blk][kk], acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) e[rt][i] = fast_exp2(acc[i] * c2 - msub[rt][i]) * fac[rt][i];
+    }
+    if constexpr (GP == 1) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pool_emit(p, e[rt][i], 16 * rt + 4 * q4 + i, t);
+    } else if constexpr (GP == 2) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        pool_emit(p, e[rt][0] + e[rt][1], 8 * rt + 2 * q4, t);
+        pool_emit(p, e[rt][2] + e[rt][3], 8 * rt + 2 * q4 + 1, t);
+      }
+    } else if constexpr (GP <= 16) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        float v = (e[rt][0] + e[rt][1]) + (e[rt][2] + e[rt][3]);
+        if constexpr (GP >= 8) v += __shfl_xor(v, 16);
+        if constexpr (GP >= 16) v += __shfl_xor(v, 32);
+        // rows 16 rt + 4 q4 .. belong to query (16 rt + 4 q4) / GP; one lane group per query emits
+        if (((4 * q4) & (GP - 1)) == 0) pool_emit(p, v, (16 * rt + 4 * q4) / GP, t);
+      }
+    } else {
+      constexpr int TPQ = GP / 16;  // row tiles per query
+#pragma unroll
+      for (int c = 0; c < RT / TPQ; ++c) {
+        float v = 0.f;
+#pragma unroll
+        for (int j = 0; j < TPQ; ++j) {
+          const int rt = c * TPQ + j;
+          v += (e[rt][0] + e[rt][1]) + (e[rt][2] + e[rt][3]);
+        }
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (q4 == 0) pool_emit(p, v, c, t);
+      }
+    }
+  }
+}
+
+__device__ inline void pool_load_group(uint4 (&kb)[4][4], const uint16_t* __restrict__ Kbg, int64_t stride_t,
+                                       int tg0, int t_end, int lane) {
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) {
+    const int t = tg0 + 16 * blk + (lane & 15);
+    if (t < t_end) {
+      const uint16_t* p = Kbg + (int64_t)t * stride_t + 8 * (lane >> 4);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) kb[blk][kk] = *(const uint4*)(p + 32 * kk);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) kb[blk][kk] = make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
+template <int RT, int GP>
 __global__ __launch_bounds__(NT) void k_pool(PoolArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  TileLds& lds = *(TileLds*)smem;  // only the K part (first member) is allocated and used
-  uint16_t* qs = (uint16_t*)(smem + KTILE_BYTES);                                   // [16 RT][KPAD]
-  uint32_t* hist = (uint32_t*)(smem + KTILE_BYTES + 16 * RT * KPAD * sizeof(uint16_t));  // [C][NBINS/2]
+  uint16_t* qs = (uint16_t*)smem;                                           // [16 RT][KPAD]
+  uint32_t* hist = (uint32_t*)(smem + 16 * RT * KPAD * sizeof(uint16_t));  // [C][NBINS/2]
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Lv = clamp_len(a.len, b, a.max_len);
-  // candidates of query c: [0, Lv - C + c - W + 1); the union over c ends at Lv - W
+  // candidates of query c: [0, Lv - C + c - W + 1); their union ends at Lv - W
   const int n_cand_max = Lv - a.W;
   const int t_begin = split * a.split_tokens;
   if (t_begin >= n_cand_max) return;
@@ -210,130 +464,58 @@ __global__ __launch_bounds__(NT) void k_pool(PoolArgs a) {
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) hist[i] = 0;
   for (int i = tid; i < 16 * RT * 16; i += NT) {
     const int r = i >> 4, cgq = i & 15;
-    const int c = r / a.Gp, h = r % a.Gp;
+    const int c = r / GP, h = r % GP;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (c < a.C && h < a.G) v = *(const uint4*)(a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HD + cgq * 8);
     *(uint4*)&qs[r * KPAD + cgq * 8] = v;
   }
-  // per-lane (M, 1/Z-free) stats of rows 16 rt + (lane & 15)
-  float m2[RT], zr[RT];
-  int ncand[RT];
+  // constants of this lane's rows 16 rt + 4(lane/16) + i
+  float fac[RT][4], msub[RT][4];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = 16 * rt + (lane & 15);
-    const int c = r / a.Gp, h = r % a.Gp;
-    if (c < a.C && h < a.G) {
-      const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
-      m2[rt] = a.stats_log2[orow * 2];
-      zr[rt] = a.stats_log2[orow * 2 + 1];
-      ncand[rt] = Lv - a.C + c - a.W + 1;
-    } else {
-      m2[rt] = 0.f;
-      zr[rt] = 0.f;  // marks a padding row: contributes nothing
-      ncand[rt] = 0;
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rt + 4 * (lane >> 4) + i;
+      const int c = r / GP, h = r % GP;
+      fac[rt][i] = 0.f;  // padding rows contribute nothing
+      msub[rt][i] = 0.f;
+      if (c < a.C && h < a.G) {
+        const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
+        const float m2 = a.stats_log2[orow * 2];
+        const float z = a.stats_log2[orow * 2 + 1];
+        if (z > 0.f) {
+          if (fabsf(m2) < 64.f) {
+            fac[rt][i] = fast_exp2(-m2) / z;  // exact power of two over Z
+          } else {  // large maxima: subtract first to stay in range
+            msub[rt][i] = m2;
+            fac[rt][i] = 1.f / z;
+          }
+        }
+      }
     }
-  }
+  __syncthreads();
+
+  PoolCtx pc;
+  pc.scores = a.scores + ((int64_t)b * a.Hkv + g) * a.C * a.score_stride;
+  pc.score_stride = a.score_stride;
+  pc.hist = hist;
+  pc.nc0 = Lv - a.C - a.W + 1;
+  pc.C = a.C;
   const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
   const uint16_t* Kbg = a.K + kvoff;
-  const int cg = tid & 15;
-  TileRegs regs;
-  {
-    int tok[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int t = t_begin + row_of(tid, u);
-      tok[u] = t < t_end ? t : -1;
-    }
-    load_tile<false>(regs, Kbg, nullptr, a.stride_t, tok, cg);
-  }
-  const int64_t row_c0 = ((int64_t)b * a.Hkv + g) * a.C;  // selection row of query 0
-  for (int t0 = t_begin; t0 < t_end; t0 += TILE) {
-    __syncthreads();
-    store_tile<false>(lds, regs, tid);
-    __syncthreads();
-    if (t0 + TILE < t_end) {
-      int tok[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int t = t0 + TILE + row_of(tid, u);
-        tok[u] = t < t_end ? t : -1;
-      }
-      load_tile<false>(regs, Kbg, nullptr, a.stride_t, tok, cg);
-    }
-    // logits of block `wave` against every row tile
-    const uint16_t* kp = &lds.k[(16 * wave + (lane & 15)) * KPAD + 8 * (lane >> 4)];
-    uint4 ka[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) ka[kk] = *(const uint4*)(kp + 32 * kk);
-    const int tbase = t0 + 16 * wave + 4 * (lane >> 4);
-    float e[RT][4];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const uint16_t* qp = &qs[(16 * rt + (lane & 15)) * KPAD + 8 * (lane >> 4)];
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(ka[kk], *(const uint4*)(qp + 32 * kk), acc);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float s2 = acc[i] * a.c2;
-        e[rt][i] = (zr[rt] > 0.f && tbase + i < ncand[rt]) ? fast_exp2(s2 - m2[rt]) / zr[rt] : 0.f;
-      }
-    }
-    // sum over the heads of each query, then record candidates
-    if (a.Gp <= 16) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = e[rt][i];
-          for (int s = 1; s < a.Gp; s <<= 1) v += __shfl_xor(v, s);
-          e[rt][i] = v;
-        }
-        const int r = 16 * rt + (lane & 15);
-        const int c = r / a.Gp;
-        if ((r % a.Gp) == 0 && c < a.C) {
-          const int nc = Lv - a.C + c - a.W + 1;
-          float* dst = a.scores + (row_c0 + c) * a.score_stride;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int t = tbase + i;
-            if (t < nc) {
-              dst[t] = e[rt][i];
-              const int dg = score_digit(score_key(e[rt][i]));
-              atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
-            }
-          }
-        }
-      }
-    } else {
-      const int tiles_per_q = a.Gp / 16;
-      for (int c = 0; c < a.C; ++c) {
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          if (rt / tiles_per_q == c)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] += e[rt][i];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          for (int s = 1; s < 16; s <<= 1) v[i] += __shfl_xor(v[i], s);
-        if ((lane & 15) == 0) {
-          const int nc = Lv - a.C + c - a.W + 1;
-          float* dst = a.scores + (row_c0 + c) * a.score_stride;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int t = tbase + i;
-            if (t < nc) {
-              dst[t] = v[i];
-              const int dg = score_digit(score_key(v[i]));
-              atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
-            }
-          }
-        }
-      }
-    }
+  uint4 kb0[4][4], kb1[4][4];
+  int g0 = t_begin + 64 * wave;
+  if (g0 < t_end) pool_load_group(kb0, Kbg, a.stride_t, g0, t_end, lane);
+  for (; g0 < t_end; g0 += 512) {
+    const int g1 = g0 + 256;
+    if (g1 < t_end) pool_load_group(kb1, Kbg, a.stride_t, g1, t_end, lane);
+    pool_group<RT, GP>(pc, a.c2, kb0, g0, qs, fac, msub, lane);
+    if (g1 >= t_end) break;
+    if (g1 + 256 < t_end) pool_load_group(kb0, Kbg, a.stride_t, g1 + 256, t_end, lane);
+    pool_group<RT, GP>(pc, a.c2, kb1, g1, qs, fac, msub, lane);
   }
   __syncthreads();
+  const int64_t row_c0 = ((int64_t)b * a.Hkv + g) * a.C;  // selection row of query 0
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
     const uint32_t v = hist[i];
     if (!v) continue;
@@ -374,9 +556,9 @@ __global__ __launch_bounds__(NT) void k_sel_hist(SelArgs a) {
   __shared__ uint32_t h[NBINS];
   const int64_t row = blockIdx.y;
   const RowInfo ri = row_info(a, row);
-  const int t0 = blockIdx.x * a.chunk;
+  const int t0 = blockIdx.x * SEL_CHUNK;
   if (t0 >= ri.N) return;
-  const int t1 = min(ri.N, t0 + a.chunk);
+  const int t1 = min(ri.N, t0 + SEL_CHUNK);
   for (int i = threadIdx.x; i < NBINS; i += NT) h[i] = 0;
   __syncthreads();
   const float* P = a.scores + row * a.score_stride;
@@ -390,6 +572,7 @@ __global__ __launch_bounds__(NT) void k_sel_hist(SelArgs a) {
 // state: [0] mode (0 none, 1 all candidates, 2 threshold), [1] bin b*,
 //        [2] need = k_eff - #(keys in bins above b*), [3] candidate count.
 __global__ __launch_bounds__(NT) void k_sel_threshold(SelArgs a) {
+  constexpr int PER = NBINS / NT;
   __shared__ int part[NT];
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(a, row);
@@ -403,32 +586,32 @@ __global__ __launch_bounds__(NT) void k_sel_threshold(SelArgs a) {
     }
     return;
   }
-  // thread tid owns bins [NBINS - 8 (tid + 1), NBINS - 8 tid), scanned from the top
+  // thread tid owns bins NBINS-1-PER*tid-j, j = 0..PER-1, scanned from the top
   const uint32_t* hr = a.hist + row * NBINS;
-  int cnt[8], s = 0;
+  int cnt[PER], s = 0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    cnt[j] = (int)hr[NBINS - 1 - 8 * tid - j];
+  for (int j = 0; j < PER; ++j) {
+    cnt[j] = (int)hr[NBINS - 1 - PER * tid - j];
     s += cnt[j];
   }
-  part[tid] = s;
-  __syncthreads();
-  if (tid == 0) {
-    int acc = 0;
-    for (int i = 0; i < NT; ++i) {
-      const int v = part[i];
-      part[i] = acc;  // exclusive prefix from the top
-      acc += v;
-    }
+  // exclusive prefix over threads (from the top bin down)
+  const int lane = tid & 63, w = tid >> 6;
+  int x = s;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
   }
+  if (lane == 63) part[w] = x;
   __syncthreads();
-  int above = part[tid];
+  int above = x - s;
+  for (int i = 0; i < w; ++i) above += part[i];
   if (above < ri.keff && above + s >= ri.keff) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < PER; ++j) {
       if (above + cnt[j] >= ri.keff) {
         st[0] = 2;
-        st[1] = NBINS - 1 - 8 * tid - j;
+        st[1] = NBINS - 1 - PER * tid - j;
         st[2] = ri.keff - above;
         break;
       }
@@ -438,28 +621,45 @@ __global__ __launch_bounds__(NT) void k_sel_threshold(SelArgs a) {
 }
 
 // Mark tokens above the threshold bin in the row bitmap and collect the
-// tokens of the threshold bin: grid (chunks, rows), 256 threads.
+// tokens of the threshold bin: grid (chunks of SEL_CHUNK tokens, rows), 256
+// threads.  Scores are loaded up front (16 per lane); candidates gather in
+// LDS and take one global slot reservation per workgroup.
 __global__ __launch_bounds__(NT) void k_sel_filter(SelArgs a) {
+  constexpr int PER = SEL_CHUNK / NT;
+  __shared__ uint32_t s_key[SEL_CHUNK];
+  __shared__ int32_t s_idx[SEL_CHUNK];
+  __shared__ int s_n, s_base;
   const int64_t row = blockIdx.y;
   const RowInfo ri = row_info(a, row);
-  const int t0 = blockIdx.x * a.chunk;
+  const int t0 = blockIdx.x * SEL_CHUNK;
   if (t0 >= ri.N) return;
-  const int t1 = min(ri.N, t0 + a.chunk);
+  const int t1 = min(ri.N, t0 + SEL_CHUNK);
   int* st = a.state + row * 8;
   const int mode = st[0], bstar = st[1];
   const float* P = a.scores + row * a.score_stride;
   uint64_t* bm = a.bitmap + row * a.bitmap_words;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int tb = t0 + 64 * wave; tb < t1; tb += 64 * (NT / 64)) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) s_n = 0;
+  float v[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int t = t0 + NT * j + 64 * wave + lane;
+    v[j] = (t < t1 && mode == 2) ? P[t] : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int tb = t0 + NT * j + 64 * wave;
+    if (tb >= t1) break;  // uniform across the wave
     const int t = tb + lane;
     const bool valid = t < t1;
     bool sel = false, cand = false;
     uint32_t key = 0;
-    if (valid && mode != 0) {
-      key = score_key(P[t]);
+    if (valid) {
       if (mode == 1) {
         sel = true;
-      } else {
+      } else if (mode == 2) {
+        key = score_key(v[j]);
         const int d = score_digit(key);
         sel = d > bstar;
         cand = d == bstar;
@@ -469,68 +669,102 @@ __global__ __launch_bounds__(NT) void k_sel_filter(SelArgs a) {
     if (lane == 0) bm[tb >> 6] = sm;
     const uint64_t cm = __ballot(cand);
     if (cm) {
-      int basev = 0;
-      if (lane == 0) basev = atomicAdd(&st[3], __popcll(cm));
-      basev = __shfl(basev, 0);
+      int off = 0;
+      if (lane == 0) off = atomicAdd(&s_n, __popcll(cm));
+      off = __shfl(off, 0);
       if (cand) {
-        const int slot = basev + __popcll(cm & ((1ull << lane) - 1ull));
-        a.cand_key[row * a.cand_cap + slot] = key;
-        a.cand_idx[row * a.cand_cap + slot] = t;
+        const int slot = off + __popcll(cm & ((1ull << lane) - 1ull));
+        s_key[slot] = key;
+        s_idx[slot] = t;
       }
     }
   }
+  __syncthreads();
+  const int n = s_n;
+  if (n == 0) return;
+  if (tid == 0) s_base = atomicAdd(&st[3], n);
+  __syncthreads();
+  const int64_t dst = row * a.cand_cap + s_base;
+  for (int i = tid; i < n; i += NT) {
+    a.cand_key[dst + i] = s_key[i];
+    a.cand_idx[dst + i] = s_idx[i];
+  }
 }
 
-// Exact selection inside the threshold bin: the `need` largest of the
-// candidates by (key desc, index asc), by radix select on the 64-bit
-// composite key (key << 32) | ~index.  grid (rows), 1024 threads.
+// Exact selection inside the threshold bin: the `need` largest candidates by
+// (key desc, index asc), i.e. by the 64-bit composite (key << 32) | ~index,
+// found by an 8-bit radix select (8 passes).  Candidates are held in LDS
+// when they fit, else read from global memory on every pass.
+// grid (rows), 1024 threads.
+constexpr int RESOLVE_LDS_CAP = 6144;
 __global__ __launch_bounds__(1024) void k_sel_resolve(SelArgs a) {
+  __shared__ uint64_t comp[RESOLVE_LDS_CAP];
   __shared__ uint32_t h[256];
-  __shared__ uint64_t s_prefix;
-  __shared__ int s_rem;
+  __shared__ int wsum[4];
+  __shared__ int s_digit, s_rem;
   const int64_t row = blockIdx.x;
   const int* st = a.state + row * 8;
   if (st[0] != 2) return;
   const int need = st[2];
-  const int m = min(st[3], a.cand_cap);
+  const int m = min(st[3], (int)a.cand_cap);
+  if (need <= 0 || m <= 0) return;
   const uint32_t* ck = a.cand_key + row * a.cand_cap;
   const int32_t* ci = a.cand_idx + row * a.cand_cap;
   uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
-  const int tid = threadIdx.x;
-  if (need <= 0 || m <= 0) return;
-  uint64_t thresh = 0;  // composite of the need-th largest (0: take all)
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const bool in_lds = m <= RESOLVE_LDS_CAP;
+  auto composite = [&](int i) -> uint64_t {
+    return in_lds ? comp[i] : (((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]));
+  };
+  if (in_lds)
+    for (int i = tid; i < m; i += 1024) comp[i] = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
+  uint64_t thresh = 0;  // composite of the need-th largest (0: take every candidate)
   if (need < m) {
-    if (tid == 0) {
-      s_prefix = 0;
-      s_rem = need;
-    }
-    uint64_t pmask = 0;
+    uint64_t prefix = 0, pmask = 0;
+    int rem = need;
     for (int shift = 56; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += 1024) h[i] = 0;
+      if (tid < 256) h[tid] = 0;
       __syncthreads();
-      const uint64_t prefix = s_prefix;
       for (int i = tid; i < m; i += 1024) {
-        const uint64_t comp = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
-        if ((comp & pmask) == prefix) atomicAdd(&h[(comp >> shift) & 255], 1u);
+        const uint64_t cv = composite(i);
+        if ((cv & pmask) == prefix) atomicAdd(&h[(cv >> shift) & 255], 1u);
       }
       __syncthreads();
-      if (tid == 0) {
-        int rem = s_rem, acc = 0, dd = 255;
-        for (; dd > 0; --dd) {
-          if (acc + (int)h[dd] >= rem) break;
-          acc += (int)h[dd];
+      // suffix sums from the top digit: thread t < 256 holds digit 255 - t
+      int x = 0, hv = 0;
+      if (tid < 256) {
+        hv = (int)h[255 - tid];
+        x = hv;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x, o);
+          if (lane >= o) x += y;
         }
-        s_rem = rem - acc;
-        s_prefix = prefix | ((uint64_t)dd << shift);
+        if (lane == 63) wsum[w] = x;
       }
+      __syncthreads();
+      if (tid < 256) {
+        int incl = x;
+        for (int i = 0; i < w; ++i) incl += wsum[i];
+        const int excl = incl - hv;  // keys with a larger digit
+        if (excl < rem && incl >= rem) {
+          s_digit = 255 - tid;
+          s_rem = rem - excl;
+        }
+      }
+      __syncthreads();
+      prefix |= (uint64_t)s_digit << shift;
       pmask |= (uint64_t)255 << shift;
+      rem = s_rem;
       __syncthreads();
     }
-    thresh = s_prefix;
+    thresh = prefix;
+  } else {
+    __syncthreads();
   }
   for (int i = tid; i < m; i += 1024) {
-    const uint64_t comp = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
-    if (comp >= thresh) {
+    const uint64_t cv = composite(i);
+    if (cv >= thresh) {
       const int t = ci[i];
       atomicOr(&bm32[t >> 5], 1u << (t & 31));
     }
@@ -695,48 +929,90 @@ __global__ __launch_bounds__(NT) void k_sa_split(SaArgs a) {
 #define HS2_LAUNCH(kernel, grid, block, shmem, stream, arg) \
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
-hipError_t launch_fa_split(const FaArgs& a, int RT, hipStream_t s) {
-  dim3 grid(a.n_split, a.Hkv, a.B);
+// Full attention kernel variants (planner default 0):
+//   0: ring kernel, 16-row stages x 4, one wave (RT <= 2) or two waves (RT = 4)
+//   1: workgroup kernel (shared stages, 4 or 8 waves)
+//   2: ring kernel, 32-row stages x 3;  3: 16-row stages x 3;  4: 16 x 4, one wave
+// RT = 8 always uses the workgroup kernel.
+#define HS2_RING_VARIANTS(X)                 \
+  X(0, 1, 1, 16, 4) X(0, 2, 1, 16, 4) X(0, 4, 2, 16, 4) \
+  X(2, 1, 1, 32, 3) X(2, 2, 1, 32, 3) X(2, 4, 2, 32, 3) \
+  X(3, 1, 1, 16, 3) X(3, 2, 1, 16, 3) X(3, 4, 2, 16, 3) \
+  X(4, 1, 1, 16, 4) X(4, 2, 1, 16, 4) X(4, 4, 1, 16, 4)
+
+int fa_token_groups(int RT, int variant) {
+  if (RT < 8 && variant != 1) return 1;
   switch (RT) {
-    case 1: HS2_LAUNCH(k_fa_split<1>, grid, dim3(NT), 0, s, a); break;
-    case 2: HS2_LAUNCH(k_fa_split<2>, grid, dim3(NT), 0, s, a); break;
-    case 4: HS2_LAUNCH(k_fa_split<4>, grid, dim3(NT), 0, s, a); break;
-    case 8: HS2_LAUNCH(k_fa_split<8>, grid, dim3(NT), 0, s, a); break;
+    case 1: return FaShape<1>::TGN;
+    case 2: return FaShape<2>::TGN;
+    case 4: return FaShape<4>::TGN;
+    default: return FaShape<8>::TGN;
+  }
+}
+
+hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
+  dim3 grid(a.n_split, a.Hkv, a.B);
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns)                                                           \
+  if (variant == v && RT == rt) {                                                                      \
+    HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns>), grid, dim3(64 * nwv), (size_t)ns * 2 * tw * STAGE_ROW_BYTES, s, a); \
+    return hipGetLastError();                                                                         \
+  }
+  HS2_RING_VARIANTS(HS2_RING_LAUNCH)
+#undef HS2_RING_LAUNCH
+  const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
+  switch (RT) {
+    case 1: HS2_LAUNCH(k_fa_split<1>, grid, dim3(64 * FaShape<1>::NW), sm, s, a); break;
+    case 2: HS2_LAUNCH(k_fa_split<2>, grid, dim3(64 * FaShape<2>::NW), sm, s, a); break;
+    case 4: HS2_LAUNCH(k_fa_split<4>, grid, dim3(64 * FaShape<4>::NW), sm, s, a); break;
+    case 8: HS2_LAUNCH(k_fa_split<8>, grid, dim3(64 * FaShape<8>::NW), sm, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 size_t pool_smem_bytes(int RT, int C) {
-  return KTILE_BYTES + (size_t)16 * RT * KPAD * sizeof(uint16_t) + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
+  return (size_t)16 * RT * KPAD * sizeof(uint16_t) + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
 }
+
+// pool kernels for every (row tiles, padded group) pair the planner can produce:
+// RT = pow2(ceil(C * GP / 16)) with C <= 16 and C * GP <= 128
+#define HS2_POOL_CASES(X) \
+  X(1, 1) X(1, 2) X(1, 4) X(1, 8) X(1, 16)                    \
+  X(2, 1) X(2, 2) X(2, 4) X(2, 8) X(2, 16) X(2, 32)           \
+  X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)                  \
+  X(8, 8) X(8, 16) X(8, 32) X(8, 64)
 
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
   const size_t sm = pool_smem_bytes(RT, a.C);
-  switch (RT) {
-    case 1: HS2_LAUNCH(k_pool<1>, grid, dim3(NT), sm, s, a); break;
-    case 2: HS2_LAUNCH(k_pool<2>, grid, dim3(NT), sm, s, a); break;
-    case 4: HS2_LAUNCH(k_pool<4>, grid, dim3(NT), sm, s, a); break;
-    case 8: HS2_LAUNCH(k_pool<8>, grid, dim3(NT), sm, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+#define HS2_POOL_LAUNCH(rt, gp) \
+  if (RT == rt && a.Gp == gp) { HS2_LAUNCH((k_pool<rt, gp>), grid, dim3(NT), sm, s, a); return hipGetLastError(); }
+  HS2_POOL_CASES(HS2_POOL_LAUNCH)
+#undef HS2_POOL_LAUNCH
+  return hipErrorInvalidValue;
 }
 
 hipError_t set_pool_smem_limits() {
   // dynamic LDS above 64 KB must be allowed explicitly
   const int big = 160 * 1024;
   hipError_t e = hipSuccess;
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<1>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<2>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<4>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<8>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_POOL_ATTR(rt, gp) \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  HS2_POOL_CASES(HS2_POOL_ATTR)
+#undef HS2_POOL_ATTR
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<1>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<2>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<4>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<8>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_RING_ATTR(v, rt, nwv, tw, ns) \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  HS2_RING_VARIANTS(HS2_RING_ATTR)
+#undef HS2_RING_ATTR
   return e;
 }
 
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s) {
-  HS2_LAUNCH(k_combine, dim3(rows_per_unit, (unsigned)units), dim3(HD), 0, s, a);
+  HS2_LAUNCH(k_combine, dim3(rows_per_unit, (unsigned)units), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -12,7 +12,7 @@ struct FaArgs {
   const uint16_t* V;
   const int32_t* len;
   float* part_o;   // [B*Hkv][n_split*TG][16 RT][HD]
-  float* part_ml;  // [B*Hkv][n_split*TG][16 RT][2]
+  float* part_ml;  // [B*Hkv][n_split*TG][16 RT][4]: (m ref, l, m true, 0)
   int64_t stride_b, stride_h, stride_t;
   float c2;        // softmax scale * log2(e)
   int B, C, Hq, Hkv, G, Gp, max_len;
@@ -24,7 +24,7 @@ struct CombineArgs {
   const float* part_ml;
   const int32_t* len;
   uint16_t* out;        // [B, C, Hq, HD] bf16
-  float* stats_log2;    // [B, C, Hq, 2] (M in log2 units, Z) or null
+  float* stats_log2;    // [B, C, Hq, 2] (reference max M in log2 units, Z against it) or null
   float* stats_user;    // [B, C, Hq, 2] (M in natural units, Z) or null
   int B, C, Hq, Hkv, G, Gp, max_len;
   int rows;             // partial rows per slot
@@ -76,7 +76,8 @@ struct SaArgs {
   int n_slots, split_slots, n_split;
 };
 
-hipError_t launch_fa_split(const FaArgs& a, int RT, hipStream_t s);
+int fa_token_groups(int RT, int variant);  // partial slots per token split
+hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
 size_t pool_smem_bytes(int RT, int C);
