@@ -170,10 +170,11 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
 void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
   s.n_slots = n_slots;
   s.RT = next_pow2((int)cdiv(p.Gp, 16));
-  s.TG = s.RT >= 4 ? 1 : 4 / s.RT;
+  s.TG = 1;  // one partial per split
+  // about 1024 workgroups, at most 4096 slots each (their indices are staged in LDS)
   int split = (int)std::max<int64_t>(64, round_up(cdiv(p.rows * (int64_t)n_slots, 1024), 64));
   split = env_int("HS2_SA_SPLIT", split);
-  split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, n_slots), 64));
+  split = (int)std::min<int64_t>(4096, std::max<int64_t>(64, round_up(std::min<int64_t>(split, n_slots), 64)));
   s.split = split;
   s.nsplit = (int)cdiv(n_slots, split);
   const int64_t prow = 16 * s.RT;

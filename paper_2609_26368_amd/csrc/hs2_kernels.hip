@@ -830,29 +830,39 @@ __global__ __launch_bounds__(1024) void k_sel_emit(SelArgs a) {
 }
 
 // ============================================================================ sparse attention
-// grid (n_split, units = B * Hkv * C), 256 threads.  Rows: the Gp heads of
-// KV head g for query c (RT_SA = Gp / 16 row tiles, at least 1).
-template <int RT>
-__global__ __launch_bounds__(NT) void k_sa_split(SaArgs a) {
-  constexpr int TG = RT >= 4 ? 1 : 4 / RT;
-  constexpr int RPW = RT >= 4 ? RT / 4 : 1;
-  constexpr int BPW = 4 / TG;
-  constexpr int WPT = 4 / TG;
-  __shared__ TileLds lds;
+// grid (n_split, units = B * Hkv * C), 64 * NWV threads, dynamic LDS = NS
+// stages of TW gathered rows of K and V + the split's index slice.  Rows are
+// the G heads of KV head g for query c (RT row tiles).  The split's index
+// entries are staged in LDS first; each stage then gathers its rows straight
+// into the ring (per-lane addresses), invalid entries (< 0 or >= len) read
+// row 0 and are masked out of the softmax.
+template <int RT, int NWV, int TW, int NS>
+__global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
+  constexpr int RPW = RT / NWV;
+  constexpr int NB = TW / 16;
+  constexpr int LPM = TW / 4 / NWV;
+  constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
+  extern __shared__ __align__(16) unsigned char smem[];
+  int32_t* sidx = (int32_t*)(smem + NS * SB);  // [split_slots]
 
   const int split = blockIdx.x;
   const int64_t unit = blockIdx.y;
   const int c = (int)(unit % a.C);
   const int g = (int)((unit / a.C) % a.Hkv);
   const int b = (int)(unit / ((int64_t)a.C * a.Hkv));
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int Lv = clamp_len(a.len, b, a.max_len);
   const int s_begin = split * a.split_slots;
   const int s_end = min(a.n_slots, s_begin + a.split_slots);
-  const int tg = wave / WPT;
-  const int rt0 = (wave % WPT) * RPW;
+  const int nslots = s_end - s_begin;
+  const int ntiles = (nslots + TW - 1) / TW;
+  const int rt0 = wave * RPW;
 
-  // queries: heads h = 16 rt + (lane & 15) of query c
+  const int32_t* irow = a.idx + unit * a.idx_stride + s_begin;
+  for (int i = threadIdx.x; i < ntiles * TW; i += 64 * NWV) {
+    int t = i < nslots ? irow[i] : -1;
+    sidx[i] = (t >= 0 && t < Lv) ? t : -1;
+  }
   uint4 q[RPW][4];
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
@@ -866,62 +876,83 @@ __global__ __launch_bounds__(NT) void k_sa_split(SaArgs a) {
       for (int kk = 0; kk < 4; ++kk) q[rr][kk] = make_uint4(0, 0, 0, 0);
     }
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));
+  __syncthreads();
+
   const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
   const uint16_t* Kbg = a.K + kvoff;
   const uint16_t* Vbg = a.V + kvoff;
-  const int32_t* irow = a.idx + unit * a.idx_stride;
-  const int cg = tid & 15;
+  const uint32_t ring = lds_addr(smem);
+  uint32_t vmask[NS];  // row-validity bits of each ring stage (wave-uniform)
+
+  auto issue = [&](int tile) {
+    const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
+    uint32_t mask = 0;
+#pragma unroll
+    for (int u = 0; u < LPM; ++u) {
+      const int n = wave * LPM + u;
+      const int row = 4 * n + (lane >> 4);
+      const int t = sidx[tile * TW + row];
+      const int64_t off = (int64_t)(t < 0 ? 0 : t) * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+      dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * STAGE_ROW_BYTES + 1024 * n));
+      const uint64_t bal = __ballot(t >= 0);  // lanes 16j .. 16j+15 hold row 4n + j
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mask |= (uint32_t)((bal >> (16 * j)) & 1ull) << (4 * n + j);
+    }
+    return mask;
+  };
 
   WaveState<RPW> st;
   st.init();
-  int blk[BPW];
 #pragma unroll
-  for (int bi = 0; bi < BPW; ++bi) blk[bi] = tg * BPW + bi;
-
-  auto gather = [&](int s0, int (&tok)[4]) {
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < ntiles) vmask[i] = issue(i);
+  for (int i = 0; i < ntiles; ++i) {
+    wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
+    if (NWV > 1) __syncthreads();
+    uint32_t m_i = 0;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int s = s0 + row_of(tid, u);
-      int t = s < s_end ? irow[s] : -1;
-      if (t >= Lv) t = -1;
-      tok[u] = t;
+    for (int k = 0; k < NS; ++k)
+      if (k == i % NS) m_i = vmask[k];
+    if (i + NS - 1 < ntiles) {
+      const uint32_t mnew = issue(i + NS - 1);
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        if (k == (i + NS - 1) % NS) vmask[k] = mnew;
     }
-  };
-  TileRegs regs;
-  int tok[4];
-  if (s_begin < s_end) {
-    gather(s_begin, tok);
-    load_tile<true>(regs, Kbg, Vbg, a.stride_t, tok, cg);
-  }
-  for (int s0 = s_begin; s0 < s_end; s0 += TILE) {
-    __syncthreads();
-    store_tile<true>(lds, regs, tid);
-    if (cg == 0) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) lds.tok[row_of(tid, u)] = tok[u];
+    if (NWV > 1) {  // both waves' row bits
+      __shared__ uint32_t s_mask[2];
+      if (lane == 0) s_mask[wave] = m_i;
+      __syncthreads();
+      m_i = s_mask[0] | s_mask[1];
     }
-    __syncthreads();
-    if (s0 + TILE < s_end) {
-      gather(s0 + TILE, tok);
-      load_tile<true>(regs, Kbg, Vbg, a.stride_t, tok, cg);
-    }
-    f32x4 S[BPW][RPW];
+    const unsigned char* stg = smem + (i % NS) * SB;
+    f32x4 S[NB][RPW];
 #pragma unroll
-    for (int bi = 0; bi < BPW; ++bi) qk_block<RPW>(lds, blk[bi], q, S[bi], lane);
+    for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
 #pragma unroll
-    for (int bi = 0; bi < BPW; ++bi) {
-      int valid[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) valid[i] = lds.tok[16 * blk[bi] + 4 * (lane >> 4) + i] >= 0;
+    for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
       for (int rr = 0; rr < RPW; ++rr)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) S[bi][rr][i] = valid[i] ? S[bi][rr][i] * a.c2 : -INFINITY;
-    }
-    softmax_pv<RPW, BPW>(st, lds, blk, S, lane);
+        for (int ii = 0; ii < 4; ++ii) {
+          const int row = 16 * bi + 4 * (lane >> 4) + ii;
+          S[bi][rr][ii] = ((m_i >> row) & 1u) ? S[bi][rr][ii] * a.c2 : -INFINITY;
+        }
+    uint2 pa[NB][RPW];
+    online_softmax<RPW, NB>(st, S, pa, lane);
+    const unsigned char* vbase = stg + TW * STAGE_ROW_BYTES;
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const uint2 vb = v_operand_tr_at(vbase, bi, nb, lane);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+      }
   }
-  const int nslot = a.n_split * TG;
-  const int64_t slot_base_row = (unit * nslot + (int64_t)split * TG + tg) * (16 * RT);
+  const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
 }
 
@@ -992,9 +1023,11 @@ hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+constexpr int SAR_TW = 16, SAR_NS = 4;
+
 hipError_t set_pool_smem_limits() {
   // dynamic LDS above 64 KB must be allowed explicitly
-  const int big = 160 * 1024;
+  const int big = 150 * 1024;  // leaves room for static LDS; no kernel asks for more
   hipError_t e = hipSuccess;
 #define HS2_POOL_ATTR(rt, gp) \
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
@@ -1008,6 +1041,9 @@ hipError_t set_pool_smem_limits() {
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   HS2_RING_VARIANTS(HS2_RING_ATTR)
 #undef HS2_RING_ATTR
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<1, 1, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<2, 1, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<4, 2, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   return e;
 }
 
@@ -1043,12 +1079,17 @@ hipError_t launch_sel_emit(const SelArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+size_t sa_smem_bytes(int split_slots) {
+  return (size_t)SAR_NS * 2 * SAR_TW * STAGE_ROW_BYTES + sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
+}
+
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, (unsigned)((int64_t)a.B * a.Hkv * a.C));
+  const size_t sm = sa_smem_bytes(a.split_slots);
   switch (RT) {
-    case 1: HS2_LAUNCH(k_sa_split<1>, grid, dim3(NT), 0, s, a); break;
-    case 2: HS2_LAUNCH(k_sa_split<2>, grid, dim3(NT), 0, s, a); break;
-    case 4: HS2_LAUNCH(k_sa_split<4>, grid, dim3(NT), 0, s, a); break;
+    case 1: HS2_LAUNCH((k_sa_ring<1, 1, SAR_TW, SAR_NS>), grid, dim3(64), sm, s, a); break;
+    case 2: HS2_LAUNCH((k_sa_ring<2, 1, SAR_TW, SAR_NS>), grid, dim3(64), sm, s, a); break;
+    case 4: HS2_LAUNCH((k_sa_ring<4, 2, SAR_TW, SAR_NS>), grid, dim3(128), sm, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
