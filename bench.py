@@ -31,7 +31,8 @@ sys.path.insert(0, ROOT)
 METRIC = "hybrid-block decode tokens/sec and achieved HBM GB/s at 128K ctx, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 DEFAULT_WORKLOAD = "chunk8_128k_b4"
-KERNEL_SOURCES = ["paper_2609_26368_amd/csrc/hs2_kernels.hip", "paper_2609_26368_amd/csrc/hs2_device.h"]
+KERNEL_SOURCES = ["paper_2609_26368_amd/csrc/hs2_kernels.hip", "paper_2609_26368_amd/csrc/hs2_device.h",
+                  "paper_2609_26368_amd/csrc/hs2_api.hip"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fa_split_traffic_{workload}.json")
 
 
@@ -55,11 +56,75 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of COPY_BYTES (counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs into the traffic record of fa_split")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain copy of COPY_BYTES, 5 times: its FETCH_SIZE / WRITE_SIZE per dispatch
+    give the factor from counter units to bytes."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}))
+
+
+def _pmc_per_kernel(d, counter):
+    import csv
+    import glob
+    import re
+    vals = {}
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        per = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            key = (r["Dispatch_Id"], re.sub(r"\(.*", "", r["Kernel_Name"]))
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+        for (_, name), v in per.items():
+            vals.setdefault(name, []).append(v)
+    return {k: sum(v) / len(v) for k, v in vals.items()}
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload):
+    fetch = _pmc_per_kernel(fetch_dir, "FETCH_SIZE")
+    write = _pmc_per_kernel(write_dir, "WRITE_SIZE")
+    cf = _pmc_per_kernel(copy_fetch_dir, "FETCH_SIZE")
+    cw = _pmc_per_kernel(copy_write_dir, "WRITE_SIZE")
+    copy_name = max(cf, key=lambda k: cf[k])  # the copy kernel dominates its run
+    f_fac = COPY_BYTES / (cf[copy_name] * 1024.0)
+    w_fac = COPY_BYTES / (cw[copy_name] * 1024.0)
+    fa = [k for k in fetch if "k_fa_" in k]
+    rec = {"workload": workload, "source_hash": kernel_source_hash(), "kernel": fa[0] if fa else None,
+           "copy_kernel": copy_name, "fetch_factor": f_fac, "write_factor": w_fac,
+           "fetch_bytes_per_launch": fetch[fa[0]] * 1024 * f_fac if fa else None,
+           "write_bytes_per_launch": write[fa[0]] * 1024 * w_fac if fa else None}
+    rec["bytes_per_launch"] = (rec["fetch_bytes_per_launch"] or 0) + (rec["write_bytes_per_launch"] or 0)
+    rec["per_kernel_bytes"] = {k: {"fetch": fetch.get(k, 0) * 1024 * f_fac, "write": write.get(k, 0) * 1024 * w_fac}
+                               for k in sorted(set(fetch) | set(write))}
+    out = TRAFFIC_FILE.format(workload=workload)
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
 
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.workload)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
               file=sys.stderr)
@@ -137,13 +202,13 @@ def main():
     step_bytes = (fa_bytes + q_bytes + idx_h.nbytes) + w.n_sparse * (uniq * kv_row + 2 * q_bytes + idx_h.nbytes)
     fa_avg_s = kernels["fa_split"]["avg_us"] * 1e-6
     achieved = fa_bytes / fa_avg_s / 1e9
-    traffic = None
+    traffic = None  # HBM bytes per launch from calibrated counters, if taken on these kernels
     tf = TRAFFIC_FILE.format(workload=w.name)
     if os.path.exists(tf):
         with open(tf) as f:
-            rec = json.load(f)
-        if rec.get("source_hash") == kernel_source_hash():
-            traffic = rec.get("bytes_per_launch")
+            trec = json.load(f)
+        if trec.get("source_hash") == kernel_source_hash():
+            traffic = int(trec["bytes_per_launch"])
     roofline = {"kernel": "fa_split", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": fa_bytes}
