@@ -187,10 +187,10 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // ---------------------------------------------------------------- timing
-enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_THRESH, KK_SEL_FILTER,
-                  KK_SEL_RESOLVE, KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
-const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "sel_init", "sel_hist", "sel_threshold",
-                                    "sel_filter", "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
+enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_FILTER, KK_SEL_RESOLVE,
+                  KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
+const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "sel_init", "sel_hist", "sel_filter",
+                                    "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
 constexpr int kMaxTimed = 16384;
 struct Timing {
   bool on = false;
@@ -267,7 +267,6 @@ SelArgs sel_args(const Plan& p, char* ws, const float* scores, int64_t score_str
 }
 
 hs2_status run_selection_tail(const Plan& p, const SelArgs& sa, hipStream_t s) {
-  HS2_TRY_LAUNCH(KK_SEL_THRESH, s, launch_sel_threshold(sa, s));
   HS2_TRY_LAUNCH(KK_SEL_FILTER, s, launch_sel_filter(sa, p.sel_nchunks, s));
   HS2_TRY_LAUNCH(KK_SEL_RESOLVE, s, launch_sel_resolve(sa, s));
   HS2_TRY_LAUNCH(KK_SEL_EMIT, s, launch_sel_emit(sa, s));
@@ -326,7 +325,6 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   const int64_t sc_stride = scores ? (int64_t)p.Lmax : p.score_stride;
 
   SelArgs sa = sel_args(p, ws, sc, sc_stride, len, idx);
-  HS2_TRY_LAUNCH(KK_SEL_INIT, s, launch_sel_init(sa, s));
 
   FaArgs fa{};
   fa.q = q;
@@ -369,6 +367,9 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   ca.tg = p.TG;
   ca.split_tokens = p.fa_split;
   ca.sa_mode = 0;
+  // the histogram and the per-row counters (contiguous) start at zero
+  ca.clear = (uint4*)(ws + p.off_hist);
+  ca.n_clear = (int64_t)(p.off_state - p.off_hist + sizeof(int32_t) * p.rows * 8) / 16;
   HS2_TRY_LAUNCH(KK_COMBINE, s, launch_combine(ca, std::min(16 * p.RT, p.C * p.Gp), p.units, s));
 
   PoolArgs pa{};
@@ -394,7 +395,6 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   pa.split_tokens = p.pool_split;
   pa.n_split = p.pool_nsplit;
   HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
-
   return run_selection_tail(p, sa, s);
 }
 

@@ -263,6 +263,10 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   const int64_t unit = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sg = tid >> 5, dq = tid & 31;
+  if (a.clear) {  // zero the selection histogram and counters for the kernels that follow
+    const int64_t nb = (int64_t)gridDim.x * gridDim.y, bid = unit * gridDim.x + r;
+    for (int64_t i = bid * 256 + tid; i < a.n_clear; i += nb * 256) a.clear[i] = make_uint4(0, 0, 0, 0);
+  }
   int b, g, c, h;
   if (a.sa_mode) {
     c = (int)(unit % a.C);
@@ -350,37 +354,60 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
 }
 
 // ============================================================================ pooled scores
-// grid (n_split, Hkv, B), 256 threads.  Each wave streams its own 64-token
-// groups (wave w: groups w, w + 4, ...) with K rows loaded straight into MFMA
-// operand registers, double-buffered; queries come from LDS.  Logits are
-// computed as S = Q . K^T (query rows on MFMA rows), so lane l holds rows
-// 4(l/16)+i of token l%16: the GP heads of a query are summed inside the
-// lane and across at most two lane groups, and the 16 scores of a block are
-// written by 16 consecutive lanes.  Per token and row the probability is
-// exp2(s2 - msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless M2 is
-// too large for that, then msub = M2 and fac = 1 / Z).
-struct PoolCtx {
-  float* scores;          // row of query 0 of this (b, g)
-  int64_t score_stride;
-  uint32_t* hist;         // LDS [C][NBINS/2], 16-bit packed counters
-  int nc0;                // candidates of query 0: Lv - C - W + 1 (query c: nc0 + c)
-  int C;
-};
+// Token scores of the full-attention layer: for query c and candidate token t,
+// P = sum over the heads h of query c of exp2(s2_h(t) - M2_h) / Z_h, with the
+// same logits s2 the full-attention kernel used and its merged (M2, Z).
+//
+// k_pool writes every candidate's score and the rows' first-level histogram
+// of score keys.  grid (token splits, Hkv, B), 256 threads.  Each wave
+// handles 16 PB tokens at a time with K rows loaded straight into MFMA
+// operand registers; queries come from LDS.  Logits are computed as S = Q . K^T
+// (query rows on MFMA rows), so lane l holds rows 4(l/16)+i of token l%16:
+// the GP heads of a query are summed inside the lane and across at most two
+// lane groups, and the 16 scores of a block sit in 16 consecutive lanes.
+// p = exp2(s2 - msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless
+// M2 is too large for that, then msub = M2 and fac = 1 / Z).
 
-__device__ inline void pool_emit(const PoolCtx& p, float v, int c, int t) {
-  if (c < p.C && t < p.nc0 + c) {
-    p.scores[c * p.score_stride + t] = v;
-    const int dg = score_digit(score_key(v));
-    atomicAdd(&p.hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+// Fill the query rows (LDS) and this lane's row constants.
+template <int RT, int GP>
+__device__ __forceinline__ void pool_setup(const PoolArgs& a, int b, int g, uint16_t* qs, float (&fac)[RT][4],
+                                  float (&msub)[RT][4], int tid, int lane) {
+  for (int i = tid; i < 16 * RT * 16; i += NT) {
+    const int r = i >> 4, cgq = i & 15;
+    const int c = r / GP, h = r % GP;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (c < a.C && h < a.G) v = *(const uint4*)(a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HD + cgq * 8);
+    *(uint4*)&qs[r * KPAD + cgq * 8] = v;
   }
+  // Branch-free on purpose: conditional stores into fac / msub make the
+  // compiler carry both arrays whole through every merge.
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rt + 4 * (lane >> 4) + i;
+      const int c = r / GP, h = r % GP;
+      const bool valid = c < a.C && h < a.G;  // padding rows contribute nothing
+      const int64_t orow = valid ? ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h : 0;
+      const float2 mz = *(const float2*)(a.stats_log2 + orow * 2);
+      const float z = valid ? mz.y : 0.f;
+      const bool big = !(fabsf(mz.x) < 64.f);  // large maxima: subtract first to stay in range
+      const float inv_z = 1.f / z;
+      fac[rt][i] = z > 0.f ? (big ? inv_z : fast_exp2(-mz.x) * inv_z) : 0.f;  // exact power of two over Z
+      msub[rt][i] = (z > 0.f && big) ? mz.x : 0.f;
+    }
 }
 
-template <int RT, int GP>
-__device__ inline void pool_group(const PoolCtx& p, float c2, const uint4 (&kb)[4][4], int tg0, const uint16_t* qs,
-                                  const float (&fac)[RT][4], const float (&msub)[RT][4], int lane) {
+// Scores of PB blocks of 16 tokens whose K rows are in kb (block blk holds
+// tokens tg0 + 16 blk + 0..15); emit(v, c, t) is called by the lanes holding
+// query c's score of token t = tg0 + 16 blk + lane % 16.
+constexpr int PB = 2;  // 16-token blocks per register buffer
+template <int RT, int GP, class Emit>
+__device__ __forceinline__ void pool_group(float c2, const uint4 (&kb)[PB][4], int tg0, const uint16_t* qs,
+                                  const float (&fac)[RT][4], const float (&msub)[RT][4], int lane, Emit& emit) {
   const int q4 = lane >> 4;
 #pragma unroll
-  for (int blk = 0; blk < 4; ++blk) {
+  for (int blk = 0; blk < PB; ++blk) {
     const int t = tg0 + 16 * blk + (lane & 15);  // this lane's token
     float e[RT][4];
 #pragma unroll
@@ -396,12 +423,12 @@ __device__ inline void pool_group(const PoolCtx& p, float c2, const uint4 (&kb)[
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pool_emit(p, e[rt][i], 16 * rt + 4 * q4 + i, t);
+        for (int i = 0; i < 4; ++i) emit(e[rt][i], 16 * rt + 4 * q4 + i, t);
     } else if constexpr (GP == 2) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        pool_emit(p, e[rt][0] + e[rt][1], 8 * rt + 2 * q4, t);
-        pool_emit(p, e[rt][2] + e[rt][3], 8 * rt + 2 * q4 + 1, t);
+        emit(e[rt][0] + e[rt][1], 8 * rt + 2 * q4, t);
+        emit(e[rt][2] + e[rt][3], 8 * rt + 2 * q4 + 1, t);
       }
     } else if constexpr (GP <= 16) {
 #pragma unroll
@@ -410,7 +437,7 @@ __device__ inline void pool_group(const PoolCtx& p, float c2, const uint4 (&kb)[
         if constexpr (GP >= 8) v += __shfl_xor(v, 16);
         if constexpr (GP >= 16) v += __shfl_xor(v, 32);
         // rows 16 rt + 4 q4 .. belong to query (16 rt + 4 q4) / GP; one lane group per query emits
-        if (((4 * q4) & (GP - 1)) == 0) pool_emit(p, v, (16 * rt + 4 * q4) / GP, t);
+        if (((4 * q4) & (GP - 1)) == 0) emit(v, (16 * rt + 4 * q4) / GP, t);
       }
     } else {
       constexpr int TPQ = GP / 16;  // row tiles per query
@@ -424,18 +451,20 @@ __device__ inline void pool_group(const PoolCtx& p, float c2, const uint4 (&kb)[
         }
         v += __shfl_xor(v, 16);
         v += __shfl_xor(v, 32);
-        if (q4 == 0) pool_emit(p, v, c, t);
+        if (q4 == 0) emit(v, c, t);
       }
     }
   }
 }
 
-__device__ inline void pool_load_group(uint4 (&kb)[4][4], const uint16_t* __restrict__ Kbg, int64_t stride_t,
-                                       int tg0, int t_end, int lane) {
+// K rows of tokens tok(blk) (one per lane, tok < 0: zeros) in MFMA B layout.
+template <class TokOf>
+__device__ __forceinline__ void pool_load_rows(uint4 (&kb)[PB][4], const uint16_t* __restrict__ Kbg, int64_t stride_t,
+                                      TokOf tok_of, int lane) {
 #pragma unroll
-  for (int blk = 0; blk < 4; ++blk) {
-    const int t = tg0 + 16 * blk + (lane & 15);
-    if (t < t_end) {
+  for (int blk = 0; blk < PB; ++blk) {
+    const int t = tok_of(blk);
+    if (t >= 0) {
       const uint16_t* p = Kbg + (int64_t)t * stride_t + 8 * (lane >> 4);
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) kb[blk][kk] = *(const uint4*)(p + 32 * kk);
@@ -446,8 +475,34 @@ __device__ inline void pool_load_group(uint4 (&kb)[4][4], const uint16_t* __rest
   }
 }
 
+// Stream the contiguous token range [t_begin, t_end): wave w handles groups
+// of 16 PB tokens w, w + 4, ..., double-buffered.
+template <int RT, int GP, class Emit>
+__device__ __forceinline__ void pool_stream(const PoolArgs& a, const uint16_t* Kbg, int t_begin, int t_end, const uint16_t* qs,
+                                   const float (&fac)[RT][4], const float (&msub)[RT][4], int wave, int lane,
+                                   Emit& emit) {
+  constexpr int GT = 16 * PB;  // tokens per group
+  uint4 kb0[PB][4], kb1[PB][4];
+  auto contiguous = [&](int tg0) {
+    return [=](int blk) {
+      const int t = tg0 + 16 * blk + (lane & 15);
+      return t < t_end ? t : -1;
+    };
+  };
+  int g0 = t_begin + GT * wave;
+  if (g0 < t_end) pool_load_rows(kb0, Kbg, a.stride_t, contiguous(g0), lane);
+  for (; g0 < t_end; g0 += 8 * GT) {
+    const int g1 = g0 + 4 * GT;
+    if (g1 < t_end) pool_load_rows(kb1, Kbg, a.stride_t, contiguous(g1), lane);
+    pool_group<RT, GP>(a.c2, kb0, g0, qs, fac, msub, lane, emit);
+    if (g1 >= t_end) break;
+    if (g1 + 4 * GT < t_end) pool_load_rows(kb0, Kbg, a.stride_t, contiguous(g1 + 4 * GT), lane);
+    pool_group<RT, GP>(a.c2, kb1, g1, qs, fac, msub, lane, emit);
+  }
+}
+
 template <int RT, int GP>
-__global__ __launch_bounds__(NT) void k_pool(PoolArgs a) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_pool(PoolArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint16_t* qs = (uint16_t*)smem;                                           // [16 RT][KPAD]
   uint32_t* hist = (uint32_t*)(smem + 16 * RT * KPAD * sizeof(uint16_t));  // [C][NBINS/2]
@@ -462,58 +517,21 @@ __global__ __launch_bounds__(NT) void k_pool(PoolArgs a) {
   const int t_end = min(n_cand_max, t_begin + a.split_tokens);
 
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) hist[i] = 0;
-  for (int i = tid; i < 16 * RT * 16; i += NT) {
-    const int r = i >> 4, cgq = i & 15;
-    const int c = r / GP, h = r % GP;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (c < a.C && h < a.G) v = *(const uint4*)(a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HD + cgq * 8);
-    *(uint4*)&qs[r * KPAD + cgq * 8] = v;
-  }
-  // constants of this lane's rows 16 rt + 4(lane/16) + i
   float fac[RT][4], msub[RT][4];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 16 * rt + 4 * (lane >> 4) + i;
-      const int c = r / GP, h = r % GP;
-      fac[rt][i] = 0.f;  // padding rows contribute nothing
-      msub[rt][i] = 0.f;
-      if (c < a.C && h < a.G) {
-        const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
-        const float m2 = a.stats_log2[orow * 2];
-        const float z = a.stats_log2[orow * 2 + 1];
-        if (z > 0.f) {
-          if (fabsf(m2) < 64.f) {
-            fac[rt][i] = fast_exp2(-m2) / z;  // exact power of two over Z
-          } else {  // large maxima: subtract first to stay in range
-            msub[rt][i] = m2;
-            fac[rt][i] = 1.f / z;
-          }
-        }
-      }
-    }
+  pool_setup<RT, GP>(a, b, g, qs, fac, msub, tid, lane);
   __syncthreads();
 
-  PoolCtx pc;
-  pc.scores = a.scores + ((int64_t)b * a.Hkv + g) * a.C * a.score_stride;
-  pc.score_stride = a.score_stride;
-  pc.hist = hist;
-  pc.nc0 = Lv - a.C - a.W + 1;
-  pc.C = a.C;
-  const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
-  const uint16_t* Kbg = a.K + kvoff;
-  uint4 kb0[4][4], kb1[4][4];
-  int g0 = t_begin + 64 * wave;
-  if (g0 < t_end) pool_load_group(kb0, Kbg, a.stride_t, g0, t_end, lane);
-  for (; g0 < t_end; g0 += 512) {
-    const int g1 = g0 + 256;
-    if (g1 < t_end) pool_load_group(kb1, Kbg, a.stride_t, g1, t_end, lane);
-    pool_group<RT, GP>(pc, a.c2, kb0, g0, qs, fac, msub, lane);
-    if (g1 >= t_end) break;
-    if (g1 + 256 < t_end) pool_load_group(kb0, Kbg, a.stride_t, g1 + 256, t_end, lane);
-    pool_group<RT, GP>(pc, a.c2, kb1, g1, qs, fac, msub, lane);
-  }
+  float* scores = a.scores + ((int64_t)b * a.Hkv + g) * a.C * a.score_stride;
+  const int nc0 = Lv - a.C - a.W + 1;  // candidates of query 0 (query c: nc0 + c)
+  auto emit = [&](float v, int c, int t) {
+    if (c < a.C && t < nc0 + c) {
+      scores[c * a.score_stride + t] = v;
+      const int dg = score_digit(score_key(v));
+      atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+    }
+  };
+  const uint16_t* Kbg = a.K + (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
+  pool_stream<RT, GP>(a, Kbg, t_begin, t_end, qs, fac, msub, wave, lane, emit);
   __syncthreads();
   const int64_t row_c0 = ((int64_t)b * a.Hkv + g) * a.C;  // selection row of query 0
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
@@ -568,35 +586,32 @@ __global__ __launch_bounds__(NT) void k_sel_hist(SelArgs a) {
     if (h[i]) atomicAdd(&a.hist[row * NBINS + i], h[i]);
 }
 
-// Find the bin holding the k_eff-th largest key: grid (rows), 256 threads.
-// state: [0] mode (0 none, 1 all candidates, 2 threshold), [1] bin b*,
-//        [2] need = k_eff - #(keys in bins above b*), [3] candidate count.
-__global__ __launch_bounds__(NT) void k_sel_threshold(SelArgs a) {
-  constexpr int PER = NBINS / NT;
-  __shared__ int part[NT];
-  const int64_t row = blockIdx.x;
-  const RowInfo ri = row_info(a, row);
-  int* st = a.state + row * 8;
-  const int tid = threadIdx.x;
-  if (ri.keff == 0 || ri.keff == ri.N) {
-    if (tid == 0) {
-      st[0] = ri.keff == 0 ? 0 : 1;
-      st[1] = -1;
-      st[2] = 0;
-    }
-    return;
+// Threshold bin of a row from its histogram, computed by all 256 threads of a
+// block (every filter block of the row derives the same values): the bin b*
+// holding the k_eff-th largest key and need = k_eff - #(keys in bins above
+// b*).  mode 0: nothing to select, 1: every candidate, 2: threshold bin.
+struct Threshold {
+  int mode, bstar, need;
+};
+__device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const RowInfo& ri, int* part, int* s_out) {
+  constexpr int PER = NBINS / NT;  // 4 bins per thread
+  static_assert(PER == 4, "one uint4 of bins per thread");
+  Threshold th{0, -1, 0};
+  if (ri.keff == 0) return th;
+  if (ri.keff == ri.N) {
+    th.mode = 1;
+    return th;
   }
-  // thread tid owns bins NBINS-1-PER*tid-j, j = 0..PER-1, scanned from the top
-  const uint32_t* hr = a.hist + row * NBINS;
-  int cnt[PER], s = 0;
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    cnt[j] = (int)hr[NBINS - 1 - PER * tid - j];
-    s += cnt[j];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (tid == 0) {  // defaults if the histogram held fewer than k_eff keys (it cannot)
+    s_out[0] = 0;
+    s_out[1] = 0;
   }
-  // exclusive prefix over threads (from the top bin down)
-  const int lane = tid & 63, w = tid >> 6;
-  int x = s;
+  // thread tid owns bins NBINS-1-4 tid-j, j = 0..3, scanned from the top
+  const uint4 hv = *(const uint4*)(a.hist + row * NBINS + NBINS - 4 - 4 * tid);
+  const int cnt[PER] = {(int)hv.w, (int)hv.z, (int)hv.y, (int)hv.x};
+  const int sum = cnt[0] + cnt[1] + cnt[2] + cnt[3];
+  int x = sum;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int y = __shfl_up(x, o);
@@ -604,83 +619,105 @@ __global__ __launch_bounds__(NT) void k_sel_threshold(SelArgs a) {
   }
   if (lane == 63) part[w] = x;
   __syncthreads();
-  int above = x - s;
+  int above = x - sum;
   for (int i = 0; i < w; ++i) above += part[i];
-  if (above < ri.keff && above + s >= ri.keff) {
+  if (above < ri.keff && above + sum >= ri.keff) {
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       if (above + cnt[j] >= ri.keff) {
-        st[0] = 2;
-        st[1] = NBINS - 1 - PER * tid - j;
-        st[2] = ri.keff - above;
+        s_out[0] = NBINS - 1 - 4 * tid - j;
+        s_out[1] = ri.keff - above;
         break;
       }
       above += cnt[j];
     }
   }
+  __syncthreads();
+  th.mode = 2;
+  th.bstar = s_out[0];
+  th.need = s_out[1];
+  return th;
 }
 
 // Mark tokens above the threshold bin in the row bitmap and collect the
 // tokens of the threshold bin: grid (chunks of SEL_CHUNK tokens, rows), 256
-// threads.  Scores are loaded up front (16 per lane); candidates gather in
-// LDS and take one global slot reservation per workgroup.
+// threads.  The scores are requested first (16 per lane) and the threshold
+// is derived from the histogram while they arrive.  Candidates gather in LDS
+// (up to FILTER_LDS_CAND; beyond that a wave reserves global slots itself)
+// and take one global slot reservation per workgroup.  The first chunk's
+// block records the row's threshold for k_sel_resolve.
+// state: [0] mode, [1] b*, [2] need, [3] candidates collected.
+constexpr int FILTER_LDS_CAND = 1024;
 __global__ __launch_bounds__(NT) void k_sel_filter(SelArgs a) {
   constexpr int PER = SEL_CHUNK / NT;
-  __shared__ uint32_t s_key[SEL_CHUNK];
-  __shared__ int32_t s_idx[SEL_CHUNK];
-  __shared__ int s_n, s_base;
+  __shared__ uint32_t s_key[FILTER_LDS_CAND];
+  __shared__ int32_t s_idx[FILTER_LDS_CAND];
+  __shared__ int s_n, s_base, part[4], s_th[2];
   const int64_t row = blockIdx.y;
   const RowInfo ri = row_info(a, row);
   const int t0 = blockIdx.x * SEL_CHUNK;
   if (t0 >= ri.N) return;
   const int t1 = min(ri.N, t0 + SEL_CHUNK);
-  int* st = a.state + row * 8;
-  const int mode = st[0], bstar = st[1];
   const float* P = a.scores + row * a.score_stride;
   uint64_t* bm = a.bitmap + row * a.bitmap_words;
+  int* st = a.state + row * 8;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) s_n = 0;
   float v[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int t = t0 + NT * j + 64 * wave + lane;
-    v[j] = (t < t1 && mode == 2) ? P[t] : 0.f;
+    v[j] = t < t1 ? P[t] : 0.f;
   }
-  __syncthreads();
+  if (tid == 0) s_n = 0;
+  const Threshold th = find_threshold(a, row, ri, part, s_th);
+  if (blockIdx.x == 0 && tid == 0) {
+    st[0] = th.mode;
+    st[1] = th.bstar;
+    st[2] = th.need;
+  }
+  __syncthreads();  // s_n initialised (find_threshold may return before its barriers)
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int tb = t0 + NT * j + 64 * wave;
     if (tb >= t1) break;  // uniform across the wave
     const int t = tb + lane;
     const bool valid = t < t1;
-    bool sel = false, cand = false;
-    uint32_t key = 0;
-    if (valid) {
-      if (mode == 1) {
-        sel = true;
-      } else if (mode == 2) {
-        key = score_key(v[j]);
-        const int d = score_digit(key);
-        sel = d > bstar;
-        cand = d == bstar;
-      }
-    }
+    const uint32_t key = score_key(v[j]);
+    const int d = score_digit(key);
+    const bool sel = valid && (th.mode == 1 || (th.mode == 2 && d > th.bstar));
+    const bool cand = valid && th.mode == 2 && d == th.bstar;
     const uint64_t sm = __ballot(sel);
     if (lane == 0) bm[tb >> 6] = sm;
     const uint64_t cm = __ballot(cand);
     if (cm) {
-      int off = 0;
-      if (lane == 0) off = atomicAdd(&s_n, __popcll(cm));
-      off = __shfl(off, 0);
+      // LDS slots [off, off + cnt) are claimed; those at or past the LDS
+      // capacity go to global slots reserved here (LDS slots below the
+      // capacity are then all written exactly once)
+      const int leader = __builtin_ctzll(cm);
+      const int cnt = __popcll(cm);
+      int off = 0, gbase = 0;
+      if (lane == leader) {
+        off = atomicAdd(&s_n, cnt);
+        const int excess = off + cnt - max(off, FILTER_LDS_CAND);
+        if (excess > 0) gbase = atomicAdd(&st[3], excess);
+      }
+      off = __shfl(off, leader);
+      gbase = __shfl(gbase, leader);
       if (cand) {
         const int slot = off + __popcll(cm & ((1ull << lane) - 1ull));
-        s_key[slot] = key;
-        s_idx[slot] = t;
+        if (slot < FILTER_LDS_CAND) {
+          s_key[slot] = key;
+          s_idx[slot] = t;
+        } else {
+          const int64_t gs = row * a.cand_cap + gbase + (slot - max(off, FILTER_LDS_CAND));
+          a.cand_key[gs] = key;
+          a.cand_idx[gs] = t;
+        }
       }
     }
   }
   __syncthreads();
-  const int n = s_n;
+  const int n = min(s_n, FILTER_LDS_CAND);
   if (n == 0) return;
   if (tid == 0) s_base = atomicAdd(&st[3], n);
   __syncthreads();
@@ -693,7 +730,8 @@ __global__ __launch_bounds__(NT) void k_sel_filter(SelArgs a) {
 
 // Exact selection inside the threshold bin: the `need` largest candidates by
 // (key desc, index asc), i.e. by the 64-bit composite (key << 32) | ~index,
-// found by an 8-bit radix select (8 passes).  Candidates are held in LDS
+// found by an 8-bit radix select (at most 8 passes; it stops at the first
+// digit whose keys are all taken, usually right after the score bits).  Candidates are held in LDS
 // when they fit, else read from global memory on every pass.
 // grid (rows), 1024 threads.
 constexpr int RESOLVE_LDS_CAP = 6144;
@@ -701,17 +739,17 @@ __global__ __launch_bounds__(1024) void k_sel_resolve(SelArgs a) {
   __shared__ uint64_t comp[RESOLVE_LDS_CAP];
   __shared__ uint32_t h[256];
   __shared__ int wsum[4];
-  __shared__ int s_digit, s_rem;
+  __shared__ int s_digit, s_rem, s_all;
   const int64_t row = blockIdx.x;
   const int* st = a.state + row * 8;
   if (st[0] != 2) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  uint32_t* ck = a.cand_key + row * a.cand_cap;
+  int32_t* ci = a.cand_idx + row * a.cand_cap;
+  uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
   const int need = st[2];
   const int m = min(st[3], (int)a.cand_cap);
   if (need <= 0 || m <= 0) return;
-  const uint32_t* ck = a.cand_key + row * a.cand_cap;
-  const int32_t* ci = a.cand_idx + row * a.cand_cap;
-  uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const bool in_lds = m <= RESOLVE_LDS_CAP;
   auto composite = [&](int i) -> uint64_t {
     return in_lds ? comp[i] : (((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]));
@@ -750,13 +788,18 @@ __global__ __launch_bounds__(1024) void k_sel_resolve(SelArgs a) {
         if (excl < rem && incl >= rem) {
           s_digit = 255 - tid;
           s_rem = rem - excl;
+          s_all = hv == rem - excl;  // the whole digit is taken
         }
       }
       __syncthreads();
       prefix |= (uint64_t)s_digit << shift;
       pmask |= (uint64_t)255 << shift;
       rem = s_rem;
+      const bool done = s_all;
       __syncthreads();
+      // every candidate under the prefix is taken: prefix with zero low bits
+      // is the threshold (all larger composites are taken too)
+      if (done) break;
     }
     thresh = prefix;
   } else {
@@ -812,6 +855,7 @@ __global__ __launch_bounds__(1024) void k_sel_emit(SelArgs a) {
   for (int w0 = 0; w0 < nwords; w0 += 1024) {
     const int w = w0 + tid;
     uint64_t bits = w < nwords ? bm[w] : 0ull;
+    if (w == nwords - 1 && (ri.N & 63)) bits &= (1ull << (ri.N & 63)) - 1ull;  // tail bits are not maintained
     int total;
     int off = block_scan_1024(__popcll(bits), lds16, total);
     while (bits) {
@@ -1060,10 +1104,6 @@ hipError_t launch_sel_init(const SelArgs& a, hipStream_t s) {
 }
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s) {
   HS2_LAUNCH(k_sel_hist, dim3(nchunks, (unsigned)a.rows), dim3(NT), 0, s, a);
-  return hipGetLastError();
-}
-hipError_t launch_sel_threshold(const SelArgs& a, hipStream_t s) {
-  HS2_LAUNCH(k_sel_threshold, dim3((unsigned)a.rows), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_sel_filter(const SelArgs& a, int nchunks, hipStream_t s) {

@@ -32,6 +32,8 @@ struct CombineArgs {
   int tg;               // slots per split (FA)
   int split_tokens;     // FA split size (FA only)
   int sa_mode;
+  uint4* clear;         // 16-byte words zeroed by the kernel as a side job, or null
+  int64_t n_clear;
 };
 
 struct PoolArgs {
@@ -84,7 +86,6 @@ size_t pool_smem_bytes(int RT, int C);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
-hipError_t launch_sel_threshold(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_filter(const SelArgs& a, int nchunks, hipStream_t s);
 hipError_t launch_sel_resolve(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_emit(const SelArgs& a, hipStream_t s);

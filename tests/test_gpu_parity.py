@@ -51,7 +51,10 @@ def run_gpu(inp, oracle_idx=None):
     lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
     stats = torch.empty((B, C, Hq, 2), dtype=torch.float32, device="cuda")
     scores = torch.zeros((B, Hkv, C, Lmax), dtype=torch.float32, device="cuda")
-    out, idx = blk.full(dev_bf16(inp.q_fa), K, V, lens, stats=stats, scores=scores)
+    q_fa = dev_bf16(inp.q_fa)
+    # with the scores and statistics requested, then the plain call (scores in the workspace)
+    out_s, idx_s = blk.full(q_fa, K, V, lens, stats=stats, scores=scores)
+    out, idx = blk.full(q_fa, K, V, lens)
     sa = [blk.sparse(dev_bf16(qs), K, V, lens, idx) for qs in inp.q_sa]
     sa_ref_idx = None
     if oracle_idx is not None:
@@ -59,7 +62,8 @@ def run_gpu(inp, oracle_idx=None):
         sa_ref_idx = [blk.sparse(dev_bf16(qs), K, V, lens, ridx) for qs in inp.q_sa]
     torch.cuda.synchronize()
     res = {"out": CK.bf16_bits_to_f64(host_bits(out)), "idx": idx.cpu().numpy(), "stats": stats.cpu().numpy(),
-           "scores": scores.cpu().numpy(), "sa": [CK.bf16_bits_to_f64(host_bits(t)) for t in sa]}
+           "scores": scores.cpu().numpy(), "sa": [CK.bf16_bits_to_f64(host_bits(t)) for t in sa],
+           "out_with_scores": CK.bf16_bits_to_f64(host_bits(out_s)), "idx_with_scores": idx_s.cpu().numpy()}
     if sa_ref_idx is not None:
         res["sa_ref_idx"] = [CK.bf16_bits_to_f64(host_bits(t)) for t in sa_ref_idx]
     return res
@@ -81,6 +85,8 @@ def compare(inp, ref, gpu, groups=None):
     assert np.allclose(Z[sel], ref["Z"][sel], rtol=1e-4), "stats Z"
     r_sc = CK.check_scores(gpu["scores"], ref["P"], inp.lens, w.n_queries, w.window, groups)
     r_idx = CK.check_idx(gpu["idx"], ref["idx"], ref["P"], inp.lens, w.n_queries, w.window, groups)
+    assert np.array_equal(gpu["idx_with_scores"], gpu["idx"]), "selection depends on where the scores are kept"
+    assert np.array_equal(gpu["out_with_scores"], gpu["out"]), "full-attention output depends on the score request"
     for li, qs in enumerate(inp.q_sa):
         ref_sa = O.sparse_attention(qs, inp.K, inp.V, ref["idx"], groups=groups)
         CK.check_out(gpu["sa_ref_idx"][li], ref_sa, f"sparse layer {li} (oracle selection)", rows)
@@ -198,6 +204,9 @@ SEL = [
     ("random", 2, 3, 2, 5000, 300, 40, "uniform"),
     ("heavy_ties", 2, 2, 1, 7000, 500, 16, "ties"),
     ("all_equal", 1, 2, 1, 3000, 700, 8, "const"),
+    # every chunk overflows the filter's LDS candidate buffer; the row's
+    # candidates exceed the resolver's LDS capacity
+    ("all_equal_long", 1, 1, 2, 20000, 5000, 64, "const"),
     ("denormals_and_zeros", 1, 1, 3, 2000, 100, 10, "tiny"),
     ("lognormal_long", 1, 2, 1, 200000, 4096, 256, "lognormal"),
     ("k_equals_N", 1, 1, 1, 1000, 990, 10, "uniform"),
