@@ -68,8 +68,10 @@ struct Plan {
   int64_t rows;               // selection rows B * Hkv * C
   int64_t score_stride, bitmap_words, cand_cap;
   int sel_nchunks;
+  bool pool_logits;           // scores from logits stored by the full-attention kernel
+  int64_t logit_stride;
   // workspace layout of hs2_full_attn_score_select / hs2_select_from_scores
-  size_t off_part_o, off_part_ml, off_stats, off_scores, off_hist, off_state, off_bitmap, off_ckey, off_cidx;
+  size_t off_part_o, off_part_ml, off_stats, off_scores, off_hist, off_state, off_bitmap, off_ckey, off_cidx, off_logits;
   size_t fa_bytes;
 };
 
@@ -151,6 +153,11 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
   p.bitmap_words = cdiv(p.Lmax, 64);
   p.cand_cap = p.Lmax;
   p.sel_nchunks = (int)cdiv(p.Lmax, kSelChunk);
+  // with at most 16 query rows per KV head (C * G <= 16) the ring kernel
+  // stores its logits (4 C G bytes per token) and the scores are computed
+  // from them instead of re-reading K (256 bytes per token)
+  p.pool_logits = p.RT == 1 && p.fa_variant != 1 && env_int("HS2_POOL_FROM_K", 0) == 0;
+  p.logit_stride = round_up(p.Lmax, 64);
 
   const int64_t prow = 16 * p.RT;
   const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
@@ -164,6 +171,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
   p.off_bitmap = carve(cur, sizeof(uint64_t) * p.rows * p.bitmap_words);
   p.off_ckey = carve(cur, sizeof(uint32_t) * p.rows * p.cand_cap);
   p.off_cidx = carve(cur, sizeof(int32_t) * p.rows * p.cand_cap);
+  p.off_logits = carve(cur, p.pool_logits ? sizeof(float) * p.rows * p.G * p.logit_stride : 0);
   p.fa_bytes = (size_t)round_up((int64_t)cur, kAlign);
 }
 
@@ -187,10 +195,10 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // ---------------------------------------------------------------- timing
-enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_FILTER, KK_SEL_RESOLVE,
-                  KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
-const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "sel_init", "sel_hist", "sel_filter",
-                                    "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
+enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_POOL_LOGITS, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_FILTER,
+                  KK_SEL_RESOLVE, KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
+const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "pool_logits", "sel_init", "sel_hist",
+                                    "sel_filter", "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
 constexpr int kMaxTimed = 16384;
 struct Timing {
   bool on = false;
@@ -346,6 +354,8 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   fa.max_len = p.Lmax;
   fa.split_tokens = p.fa_split;
   fa.n_split = p.fa_nsplit;
+  fa.logits = p.pool_logits ? (float*)(ws + p.off_logits) : nullptr;
+  fa.logit_stride = p.logit_stride;
   HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, p.fa_variant, s));
 
   CombineArgs ca{};
@@ -394,7 +404,12 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   pa.W = p.W;
   pa.split_tokens = p.pool_split;
   pa.n_split = p.pool_nsplit;
-  HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
+  pa.logits = fa.logits;
+  pa.logit_stride = p.logit_stride;
+  if (p.pool_logits)
+    HS2_TRY_LAUNCH(KK_POOL_LOGITS, s, launch_pool_logits(pa, s));
+  else
+    HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
   return run_selection_tail(p, sa, s);
 }
 

@@ -179,6 +179,15 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
   const uint16_t* Kbg = a.K + kvoff;
   const uint16_t* Vbg = a.V + kvoff;
   const uint32_t ring = lds_addr(smem);
+  // logits output of a single row tile (C G <= 16 query rows): this lane's
+  // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
+  float* lrow = nullptr;
+  if constexpr (RT == 1) {
+    const int r = lane & 15;
+    const int c = r / a.Gp, h = r % a.Gp;
+    if (a.logits && c < a.C && h < a.G)
+      lrow = a.logits + (((int64_t)b * a.Hkv + g) * a.C * a.G + c * a.G + h) * a.logit_stride;
+  }
 
   // per-lane part of each load's element offset: row * stride + swizzled chunk
   int64_t lane_off[LPM];
@@ -212,6 +221,7 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
   for (int i = 0; i < NS - 1; ++i)
     if (i < ntiles) issue(i);
   for (int i = 0; i < ntiles; ++i) {
+    // logits stores also count in vmcnt; they only make this wait longer
     wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
     if (NWV > 1) __syncthreads();
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
@@ -220,6 +230,11 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
     f32x4 S[NB][RPW];
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    if constexpr (RT == 1) {  // the lane's 4 consecutive tokens; the row stride covers whole tiles
+      if (lrow)
+#pragma unroll
+        for (int bi = 0; bi < NB; ++bi) *(f32x4*)(lrow + t0 + 16 * bi + 4 * (lane >> 4)) = S[bi][0] * a.c2;
+    }
     const bool full = (t0 + TW <= t_end) && (t0 + TW - 1 <= min_pos);
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
@@ -539,6 +554,73 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     if (!v) continue;
     const int c = i / (NBINS / 2), w = i % (NBINS / 2);
     uint32_t* gh = a.hist + (row_c0 + c) * NBINS + 2 * w;
+    if (v & 0xFFFFu) atomicAdd(gh, v & 0xFFFFu);
+    if (v >> 16) atomicAdd(gh + 1, v >> 16);
+  }
+}
+
+// Scores from the logits the full-attention ring kernel stored (small row
+// counts: C * G logits per token cost less traffic than re-reading K):
+// P = sum over h of exp2(s2_h - msub) * fac, the same constants as k_pool.
+// grid (chunks of LOGIT_CHUNK tokens, B * Hkv), 256 threads, 4 consecutive
+// tokens per thread; dynamic LDS: C packed histograms.
+constexpr int LOGIT_CHUNK = 4096;
+__global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  uint32_t* hist = (uint32_t*)smem;  // [C][NBINS/2], 16-bit packed counters
+  __shared__ float s_fac[16], s_msub[16];
+  const int64_t unit = blockIdx.y;
+  const int b = (int)(unit / a.Hkv), g = (int)(unit % a.Hkv);
+  const int tid = threadIdx.x;
+  const int Lv = clamp_len(a.len, b, a.max_len);
+  const int n_cand_max = Lv - a.W;  // union of the queries' candidates
+  const int t_begin = blockIdx.x * LOGIT_CHUNK;
+  if (t_begin >= n_cand_max) return;
+  const int t_end = min(n_cand_max, t_begin + LOGIT_CHUNK);
+  const int CG = a.C * a.G;
+  for (int i = tid; i < a.C * (NBINS / 2); i += NT) hist[i] = 0;
+  if (tid < CG) {
+    const int c = tid / a.G, h = tid % a.G;
+    const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
+    const float m2 = a.stats_log2[orow * 2], z = a.stats_log2[orow * 2 + 1];
+    const bool big = !(fabsf(m2) < 64.f);
+    s_fac[tid] = z > 0.f ? (big ? 1.f / z : fast_exp2(-m2) / z) : 0.f;
+    s_msub[tid] = (z > 0.f && big) ? m2 : 0.f;
+  }
+  __syncthreads();
+  const int nc0 = Lv - a.C - a.W + 1;  // candidates of query 0 (query c: nc0 + c)
+  const float* lg = a.logits + unit * CG * a.logit_stride;
+  for (int t = t_begin + 4 * tid; t < t_end; t += 4 * NT) {
+    for (int c = 0; c < a.C; ++c) {
+      const int nc = nc0 + c;
+      if (t >= nc) continue;  // not a candidate of query c (later queries have more)
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int h = 0; h < a.G; ++h) {
+        const int r = c * a.G + h;
+        const float4 l = *(const float4*)(lg + r * a.logit_stride + t);
+        const float f = s_fac[r], m = s_msub[r];
+        acc.x += fast_exp2(l.x - m) * f;
+        acc.y += fast_exp2(l.y - m) * f;
+        acc.z += fast_exp2(l.z - m) * f;
+        acc.w += fast_exp2(l.w - m) * f;
+      }
+      float* sr = a.scores + (unit * a.C + c) * a.score_stride + t;
+      const float v[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (t + j < nc) {
+          sr[j] = v[j];
+          const int dg = score_digit(score_key(v[j]));
+          atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+        }
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
+    const uint32_t v = hist[i];
+    if (!v) continue;
+    const int c = i / (NBINS / 2), w = i % (NBINS / 2);
+    uint32_t* gh = a.hist + (unit * a.C + c) * NBINS + 2 * w;
     if (v & 0xFFFFu) atomicAdd(gh, v & 0xFFFFu);
     if (v >> 16) atomicAdd(gh + 1, v >> 16);
   }
@@ -1027,10 +1109,10 @@ int fa_token_groups(int RT, int variant) {
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns)                                                           \
-  if (variant == v && RT == rt) {                                                                      \
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns)                                                            \
+  if (variant == v && RT == rt) {                                                                       \
     HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns>), grid, dim3(64 * nwv), (size_t)ns * 2 * tw * STAGE_ROW_BYTES, s, a); \
-    return hipGetLastError();                                                                         \
+    return hipGetLastError();                                                                          \
   }
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
 #undef HS2_RING_LAUNCH
@@ -1056,6 +1138,13 @@ size_t pool_smem_bytes(int RT, int C) {
   X(2, 1) X(2, 2) X(2, 4) X(2, 8) X(2, 16) X(2, 32)           \
   X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)                  \
   X(8, 8) X(8, 16) X(8, 32) X(8, 64)
+
+hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
+  const int64_t chunks = ((int64_t)a.max_len + LOGIT_CHUNK - 1) / LOGIT_CHUNK;
+  HS2_LAUNCH(k_pool_logits, dim3((unsigned)chunks, (unsigned)(a.B * a.Hkv)), dim3(NT),
+             (size_t)a.C * (NBINS / 2) * sizeof(uint32_t), s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);

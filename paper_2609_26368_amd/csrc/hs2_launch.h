@@ -17,6 +17,8 @@ struct FaArgs {
   float c2;        // softmax scale * log2(e)
   int B, C, Hq, Hkv, G, Gp, max_len;
   int split_tokens, n_split;
+  float* logits;   // [B*Hkv][C*G][logit_stride] logits in log2 units (ring kernels), or null
+  int64_t logit_stride;
 };
 
 struct CombineArgs {
@@ -43,6 +45,8 @@ struct PoolArgs {
   const float* stats_log2;
   float* scores;        // [rows][score_stride]
   uint32_t* hist;       // [rows][NBINS]
+  const float* logits;  // [B*Hkv][C*G][logit_stride] (k_pool_logits)
+  int64_t logit_stride;
   int64_t stride_b, stride_h, stride_t;
   int64_t score_stride;
   float c2;
@@ -82,6 +86,7 @@ int fa_token_groups(int RT, int variant);  // partial slots per token split
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
+hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s);
 size_t pool_smem_bytes(int RT, int C);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);

@@ -182,6 +182,13 @@ def test_strided_cache_layout():
         CK.check_out(CK.bf16_bits_to_f64(host_bits(sa)), O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"]))
 
 
+@pytest.mark.parametrize("w", [SMALL[0], SMALL[2]], ids=[SMALL[0].name, SMALL[2].name])
+def test_parity_scores_from_k(w, monkeypatch):
+    """Single row tile with the scores recomputed from K instead of the stored logits."""
+    monkeypatch.setenv("HS2_POOL_FROM_K", "1")
+    parity_case(w, seed=7)
+
+
 # ---------------------------------------------------------------- selection alone: bit-exact
 def _select_case(B, Hkv, C, Lmax, lens, k, win, scores):
     hs2 = _hs2()
