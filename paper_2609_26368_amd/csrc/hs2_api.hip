@@ -61,7 +61,7 @@ struct Plan {
   int B, C, Hq, Hkv, G, Gp, D, Lmax, k, W, S;
   float c2;
   int RT, TG;                 // full-attention / pooling row tiles
-  int fa_variant;             // 0: one-wave ring kernel (RT <= 4), 1: workgroup kernel
+  int fa_variant;             // ring kernel shape (0, 2, 3, 4) for RT <= 4; 1: workgroup kernel
   int fa_split, fa_nsplit;
   int pool_split, pool_nsplit;
   int64_t units;              // B * Hkv
@@ -116,7 +116,20 @@ size_t carve(size_t& cur, size_t bytes) {
   return at;
 }
 
-void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
+// What the planner needs to know about the current device: compute units
+// and, per full-attention kernel shape, how many workgroups stay resident
+// on one compute unit (runtime occupancy query).
+struct DeviceInfo {
+  int cus = 256;
+  int fa_wgs[4][kFaVariants] = {};  // [log2 RT][variant]; 0 = unknown
+};
+
+// Measured on MI355X with one-round splits: 32-token tiles in 3 stages for
+// one row tile, 16-token tiles in 3 stages for two and four, the workgroup
+// kernel for eight.
+int default_fa_variant(int RT) { return RT >= 8 ? 1 : RT == 1 ? 2 : 3; }
+
+void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const DeviceInfo* di) {
   p.B = d->batch;
   p.C = d->n_queries;
   p.Hq = d->n_q_heads;
@@ -132,15 +145,19 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p) {
   p.c2 = (float)(scale * 1.4426950408889634);
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
-  p.fa_variant = env_int("HS2_FA_VARIANT", 0);
+  p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT));
+  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || p.RT >= 8) p.fa_variant = p.RT >= 8 ? 1 : 0;
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
   p.rows = p.units * p.C;
-  // token splits over the whole cache: about 4096 / RT one-wave workgroups
-  // (partials cost 16 RT rows per split), whole 64-token tiles
-  const int64_t total = p.units * (int64_t)p.Lmax;
-  const int target_wgs = p.fa_variant == 1 || p.RT >= 8 ? 1024 : 4096 / p.RT;
-  int split = (int)std::max<int64_t>(256, round_up(cdiv(total, target_wgs), 64));
+  // token splits: as many workgroups as stay resident at once on the device
+  // (one round, no tail), each a whole number of 64-token tiles and at least
+  // 256 tokens (a split's partial costs 16 RT rows of D + 4 floats)
+  const int lrt = p.RT >= 8 ? 3 : p.RT >= 4 ? 2 : p.RT >= 2 ? 1 : 0;
+  const int wgs_cu = di && di->fa_wgs[lrt][p.fa_variant] > 0 ? di->fa_wgs[lrt][p.fa_variant] : 4;
+  const int64_t slots = (int64_t)(di ? di->cus : 256) * wgs_cu * std::max(1, env_int("HS2_FA_ROUNDS", 1));
+  const int64_t per_unit = std::max<int64_t>(1, slots / p.units);
+  int split = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, per_unit), 64));
   split = env_int("HS2_FA_SPLIT", split);
   split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, p.Lmax), 64));
   p.fa_split = split;
@@ -223,19 +240,40 @@ struct TimedLaunch {
 };
 
 std::mutex g_init_mu;
-bool g_pool_attr_done[64] = {};
+bool g_dev_done[64] = {};
+DeviceInfo g_dev[64];
 
-hs2_status ensure_device_init() {
+// Per-device set-up (once): LDS limits of the kernels that need more than
+// 64 KB, and the occupancy figures the planner uses.
+hs2_status ensure_device_init(const DeviceInfo** info) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(HS2_ERR_HIP, "hipGetDevice failed");
   if (dev < 0 || dev >= 64) return fail(HS2_ERR_HIP, "device index out of range");
   std::lock_guard<std::mutex> lk(g_init_mu);
-  if (!g_pool_attr_done[dev]) {
+  if (!g_dev_done[dev]) {
     hipError_t e = set_pool_smem_limits();
     if (e != hipSuccess) return fail(HS2_ERR_HIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
-    g_pool_attr_done[dev] = true;
+    DeviceInfo di;
+    if ((e = hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+      return fail(HS2_ERR_HIP, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
+    for (int l = 0; l < 4; ++l)
+      for (int v = 0; v < kFaVariants; ++v)
+        if ((e = fa_wgs_per_cu(1 << l, v, &di.fa_wgs[l][v])) != hipSuccess)
+          return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+    g_dev[dev] = di;
+    g_dev_done[dev] = true;
   }
+  if (info) *info = &g_dev[dev];
   return HS2_OK;
+}
+
+// Device information for planning if a device is present (null on a host
+// without one; the plan then falls back to fixed figures).
+const DeviceInfo* try_device_info() {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) return nullptr;
+  const DeviceInfo* di = nullptr;
+  return ensure_device_init(&di) == HS2_OK ? di : nullptr;
 }
 
 #define HS2_TRY_LAUNCH(kind, stream, call)                                                        \
@@ -303,7 +341,7 @@ const char* hs2_last_error(void) { return g_last_error.c_str(); }
 size_t hs2_workspace_bytes(const hs2_dims* dims, int32_t k, int32_t window) {
   if (check_dims(dims) != HS2_OK || check_budget(k, window) != HS2_OK) return 0;
   Plan p;
-  make_plan(dims, k, window, p);
+  make_plan(dims, k, window, p, try_device_info());
   SaPlan sp;
   make_sa_plan(p, k + window, sp);
   return std::max(p.fa_bytes, sp.bytes);
@@ -321,11 +359,12 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
       !aligned(len, 4) || !aligned(workspace, kAlign) || (stats && !aligned(stats, 8)) || (scores && !aligned(scores, 4)))
     return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len/scores 4-byte alignment");
+  const DeviceInfo* di = try_device_info();
   Plan p;
-  make_plan(dims, k, window, p);
+  make_plan(dims, k, window, p, di);
   if (workspace_bytes < p.fa_bytes)
     return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
-  if ((st = ensure_device_init()) != HS2_OK) return st;
+  if ((st = ensure_device_init(&di)) != HS2_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   float* stats_log2 = (float*)(ws + p.off_stats);
@@ -421,11 +460,12 @@ hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, con
   if (!scores || !len || !idx || !workspace) return fail(HS2_ERR_NULL, "scores, len, idx and workspace are required");
   if (!aligned(scores, 4) || !aligned(len, 4) || !aligned(idx, 4) || !aligned(workspace, kAlign))
     return fail(HS2_ERR_ALIGN, "scores/len/idx need 4-byte, workspace 256-byte alignment");
+  const DeviceInfo* di = try_device_info();
   Plan p;
-  make_plan(dims, k, window, p);
+  make_plan(dims, k, window, p, di);
   if (workspace_bytes < p.fa_bytes)
     return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
-  if ((st = ensure_device_init()) != HS2_OK) return st;
+  if ((st = ensure_device_init(&di)) != HS2_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   SelArgs sa = sel_args(p, (char*)workspace, scores, p.Lmax, len, idx);
   HS2_TRY_LAUNCH(KK_SEL_INIT, s, launch_sel_init(sa, s));
@@ -444,13 +484,14 @@ hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
       !aligned(len, 4) || !aligned(workspace, kAlign))
     return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len 4-byte alignment");
+  const DeviceInfo* di = try_device_info();
   Plan p;
-  make_plan(dims, 0, n_slots, p);
+  make_plan(dims, 0, n_slots, p, di);
   SaPlan sp;
   make_sa_plan(p, n_slots, sp);
   if (workspace_bytes < sp.bytes)
     return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, sp.bytes);
-  if ((st = ensure_device_init()) != HS2_OK) return st;
+  if ((st = ensure_device_init(&di)) != HS2_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   SaArgs a{};

@@ -1107,6 +1107,33 @@ int fa_token_groups(int RT, int variant) {
   }
 }
 
+// The runtime's figure, capped so that each resident workgroup's LDS plus
+// 1 KB fits in the 160 KB of a compute unit: kernels whose LDS divides
+// 160 KB exactly time as if one workgroup fewer were resident.
+static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t lds) {
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs, fn, threads, lds);
+  if (e == hipSuccess && lds > 0) *wgs = std::min(*wgs, (int)((160 * 1024) / (lds + 1024)));
+  return e;
+}
+
+hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs) {
+  *wgs = 0;
+#define HS2_RING_OCC(v, rt, nwv, tw, ns)                                                               \
+  if (variant == v && RT == rt)                                                                         \
+    return occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns>, 64 * nwv,                    \
+                            (size_t)ns * 2 * tw * STAGE_ROW_BYTES);
+  HS2_RING_VARIANTS(HS2_RING_OCC)
+#undef HS2_RING_OCC
+  const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
+  switch (RT) {
+    case 1: return occupancy_capped(wgs, (const void*)k_fa_split<1>, 64 * FaShape<1>::NW, sm);
+    case 2: return occupancy_capped(wgs, (const void*)k_fa_split<2>, 64 * FaShape<2>::NW, sm);
+    case 4: return occupancy_capped(wgs, (const void*)k_fa_split<4>, 64 * FaShape<4>::NW, sm);
+    case 8: return occupancy_capped(wgs, (const void*)k_fa_split<8>, 64 * FaShape<8>::NW, sm);
+    default: return hipSuccess;
+  }
+}
+
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
 #define HS2_RING_LAUNCH(v, rt, nwv, tw, ns)                                                            \

@@ -82,7 +82,11 @@ struct SaArgs {
   int n_slots, split_slots, n_split;
 };
 
+constexpr int kFaVariants = 5;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
+// workgroups of the full-attention kernel (RT, variant) resident per compute
+// unit on the current device (0 if that kernel does not exist)
+hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs);
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
