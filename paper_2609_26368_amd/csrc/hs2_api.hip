@@ -212,10 +212,10 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // ---------------------------------------------------------------- timing
-enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_POOL_LOGITS, KK_SEL_INIT, KK_SEL_HIST, KK_SEL_FILTER,
-                  KK_SEL_RESOLVE, KK_SEL_EMIT, KK_SA, KK_SA_COMBINE, KK_COUNT };
+enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_POOL_LOGITS, KK_SEL_INIT, KK_SEL_HIST, KK_SELECT, KK_SA,
+                  KK_SA_COMBINE, KK_COUNT };
 const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "pool_logits", "sel_init", "sel_hist",
-                                    "sel_filter", "sel_resolve", "sel_emit", "sa_split", "sa_combine"};
+                                    "select", "sa_split", "sa_combine"};
 constexpr int kMaxTimed = 16384;
 struct Timing {
   bool on = false;
@@ -313,9 +313,7 @@ SelArgs sel_args(const Plan& p, char* ws, const float* scores, int64_t score_str
 }
 
 hs2_status run_selection_tail(const Plan& p, const SelArgs& sa, hipStream_t s) {
-  HS2_TRY_LAUNCH(KK_SEL_FILTER, s, launch_sel_filter(sa, p.sel_nchunks, s));
-  HS2_TRY_LAUNCH(KK_SEL_RESOLVE, s, launch_sel_resolve(sa, s));
-  HS2_TRY_LAUNCH(KK_SEL_EMIT, s, launch_sel_emit(sa, s));
+  HS2_TRY_LAUNCH(KK_SELECT, s, launch_select(sa, s));
   return HS2_OK;
 }
 
@@ -445,10 +443,15 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   pa.n_split = p.pool_nsplit;
   pa.logits = fa.logits;
   pa.logit_stride = p.logit_stride;
-  if (p.pool_logits)
+  if (p.pool_logits) {
     HS2_TRY_LAUNCH(KK_POOL_LOGITS, s, launch_pool_logits(pa, s));
-  else
+  } else if (env_int("HS2_POOL_HIST_SEPARATE", 0)) {
+    pa.hist = nullptr;
     HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
+    HS2_TRY_LAUNCH(KK_SEL_HIST, s, launch_sel_hist(sa, p.sel_nchunks, s));
+  } else {
+    HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
+  }
   return run_selection_tail(p, sa, s);
 }
 

@@ -541,13 +541,16 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   auto emit = [&](float v, int c, int t) {
     if (c < a.C && t < nc0 + c) {
       scores[c * a.score_stride + t] = v;
-      const int dg = score_digit(score_key(v));
-      atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+      if (a.hist) {
+        const int dg = score_digit(score_key(v));
+        atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+      }
     }
   };
   const uint16_t* Kbg = a.K + (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
   pool_stream<RT, GP>(a, Kbg, t_begin, t_end, qs, fac, msub, wave, lane, emit);
   __syncthreads();
+  if (!a.hist) return;
   const int64_t row_c0 = ((int64_t)b * a.Hkv + g) * a.C;  // selection row of query 0
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
     const uint32_t v = hist[i];
@@ -668,234 +671,6 @@ __global__ __launch_bounds__(NT) void k_sel_hist(SelArgs a) {
     if (h[i]) atomicAdd(&a.hist[row * NBINS + i], h[i]);
 }
 
-// Threshold bin of a row from its histogram, computed by all 256 threads of a
-// block (every filter block of the row derives the same values): the bin b*
-// holding the k_eff-th largest key and need = k_eff - #(keys in bins above
-// b*).  mode 0: nothing to select, 1: every candidate, 2: threshold bin.
-struct Threshold {
-  int mode, bstar, need;
-};
-__device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const RowInfo& ri, int* part, int* s_out) {
-  constexpr int PER = NBINS / NT;  // 4 bins per thread
-  static_assert(PER == 4, "one uint4 of bins per thread");
-  Threshold th{0, -1, 0};
-  if (ri.keff == 0) return th;
-  if (ri.keff == ri.N) {
-    th.mode = 1;
-    return th;
-  }
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (tid == 0) {  // defaults if the histogram held fewer than k_eff keys (it cannot)
-    s_out[0] = 0;
-    s_out[1] = 0;
-  }
-  // thread tid owns bins NBINS-1-4 tid-j, j = 0..3, scanned from the top
-  const uint4 hv = *(const uint4*)(a.hist + row * NBINS + NBINS - 4 - 4 * tid);
-  const int cnt[PER] = {(int)hv.w, (int)hv.z, (int)hv.y, (int)hv.x};
-  const int sum = cnt[0] + cnt[1] + cnt[2] + cnt[3];
-  int x = sum;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) part[w] = x;
-  __syncthreads();
-  int above = x - sum;
-  for (int i = 0; i < w; ++i) above += part[i];
-  if (above < ri.keff && above + sum >= ri.keff) {
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      if (above + cnt[j] >= ri.keff) {
-        s_out[0] = NBINS - 1 - 4 * tid - j;
-        s_out[1] = ri.keff - above;
-        break;
-      }
-      above += cnt[j];
-    }
-  }
-  __syncthreads();
-  th.mode = 2;
-  th.bstar = s_out[0];
-  th.need = s_out[1];
-  return th;
-}
-
-// Mark tokens above the threshold bin in the row bitmap and collect the
-// tokens of the threshold bin: grid (chunks of SEL_CHUNK tokens, rows), 256
-// threads.  The scores are requested first (16 per lane) and the threshold
-// is derived from the histogram while they arrive.  Candidates gather in LDS
-// (up to FILTER_LDS_CAND; beyond that a wave reserves global slots itself)
-// and take one global slot reservation per workgroup.  The first chunk's
-// block records the row's threshold for k_sel_resolve.
-// state: [0] mode, [1] b*, [2] need, [3] candidates collected.
-constexpr int FILTER_LDS_CAND = 1024;
-__global__ __launch_bounds__(NT) void k_sel_filter(SelArgs a) {
-  constexpr int PER = SEL_CHUNK / NT;
-  __shared__ uint32_t s_key[FILTER_LDS_CAND];
-  __shared__ int32_t s_idx[FILTER_LDS_CAND];
-  __shared__ int s_n, s_base, part[4], s_th[2];
-  const int64_t row = blockIdx.y;
-  const RowInfo ri = row_info(a, row);
-  const int t0 = blockIdx.x * SEL_CHUNK;
-  if (t0 >= ri.N) return;
-  const int t1 = min(ri.N, t0 + SEL_CHUNK);
-  const float* P = a.scores + row * a.score_stride;
-  uint64_t* bm = a.bitmap + row * a.bitmap_words;
-  int* st = a.state + row * 8;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float v[PER];
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int t = t0 + NT * j + 64 * wave + lane;
-    v[j] = t < t1 ? P[t] : 0.f;
-  }
-  if (tid == 0) s_n = 0;
-  const Threshold th = find_threshold(a, row, ri, part, s_th);
-  if (blockIdx.x == 0 && tid == 0) {
-    st[0] = th.mode;
-    st[1] = th.bstar;
-    st[2] = th.need;
-  }
-  __syncthreads();  // s_n initialised (find_threshold may return before its barriers)
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int tb = t0 + NT * j + 64 * wave;
-    if (tb >= t1) break;  // uniform across the wave
-    const int t = tb + lane;
-    const bool valid = t < t1;
-    const uint32_t key = score_key(v[j]);
-    const int d = score_digit(key);
-    const bool sel = valid && (th.mode == 1 || (th.mode == 2 && d > th.bstar));
-    const bool cand = valid && th.mode == 2 && d == th.bstar;
-    const uint64_t sm = __ballot(sel);
-    if (lane == 0) bm[tb >> 6] = sm;
-    const uint64_t cm = __ballot(cand);
-    if (cm) {
-      // LDS slots [off, off + cnt) are claimed; those at or past the LDS
-      // capacity go to global slots reserved here (LDS slots below the
-      // capacity are then all written exactly once)
-      const int leader = __builtin_ctzll(cm);
-      const int cnt = __popcll(cm);
-      int off = 0, gbase = 0;
-      if (lane == leader) {
-        off = atomicAdd(&s_n, cnt);
-        const int excess = off + cnt - max(off, FILTER_LDS_CAND);
-        if (excess > 0) gbase = atomicAdd(&st[3], excess);
-      }
-      off = __shfl(off, leader);
-      gbase = __shfl(gbase, leader);
-      if (cand) {
-        const int slot = off + __popcll(cm & ((1ull << lane) - 1ull));
-        if (slot < FILTER_LDS_CAND) {
-          s_key[slot] = key;
-          s_idx[slot] = t;
-        } else {
-          const int64_t gs = row * a.cand_cap + gbase + (slot - max(off, FILTER_LDS_CAND));
-          a.cand_key[gs] = key;
-          a.cand_idx[gs] = t;
-        }
-      }
-    }
-  }
-  __syncthreads();
-  const int n = min(s_n, FILTER_LDS_CAND);
-  if (n == 0) return;
-  if (tid == 0) s_base = atomicAdd(&st[3], n);
-  __syncthreads();
-  const int64_t dst = row * a.cand_cap + s_base;
-  for (int i = tid; i < n; i += NT) {
-    a.cand_key[dst + i] = s_key[i];
-    a.cand_idx[dst + i] = s_idx[i];
-  }
-}
-
-// Exact selection inside the threshold bin: the `need` largest candidates by
-// (key desc, index asc), i.e. by the 64-bit composite (key << 32) | ~index,
-// found by an 8-bit radix select (at most 8 passes; it stops at the first
-// digit whose keys are all taken, usually right after the score bits).  Candidates are held in LDS
-// when they fit, else read from global memory on every pass.
-// grid (rows), 1024 threads.
-constexpr int RESOLVE_LDS_CAP = 6144;
-__global__ __launch_bounds__(1024) void k_sel_resolve(SelArgs a) {
-  __shared__ uint64_t comp[RESOLVE_LDS_CAP];
-  __shared__ uint32_t h[256];
-  __shared__ int wsum[4];
-  __shared__ int s_digit, s_rem, s_all;
-  const int64_t row = blockIdx.x;
-  const int* st = a.state + row * 8;
-  if (st[0] != 2) return;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  uint32_t* ck = a.cand_key + row * a.cand_cap;
-  int32_t* ci = a.cand_idx + row * a.cand_cap;
-  uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
-  const int need = st[2];
-  const int m = min(st[3], (int)a.cand_cap);
-  if (need <= 0 || m <= 0) return;
-  const bool in_lds = m <= RESOLVE_LDS_CAP;
-  auto composite = [&](int i) -> uint64_t {
-    return in_lds ? comp[i] : (((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]));
-  };
-  if (in_lds)
-    for (int i = tid; i < m; i += 1024) comp[i] = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
-  uint64_t thresh = 0;  // composite of the need-th largest (0: take every candidate)
-  if (need < m) {
-    uint64_t prefix = 0, pmask = 0;
-    int rem = need;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      if (tid < 256) h[tid] = 0;
-      __syncthreads();
-      for (int i = tid; i < m; i += 1024) {
-        const uint64_t cv = composite(i);
-        if ((cv & pmask) == prefix) atomicAdd(&h[(cv >> shift) & 255], 1u);
-      }
-      __syncthreads();
-      // suffix sums from the top digit: thread t < 256 holds digit 255 - t
-      int x = 0, hv = 0;
-      if (tid < 256) {
-        hv = (int)h[255 - tid];
-        x = hv;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(x, o);
-          if (lane >= o) x += y;
-        }
-        if (lane == 63) wsum[w] = x;
-      }
-      __syncthreads();
-      if (tid < 256) {
-        int incl = x;
-        for (int i = 0; i < w; ++i) incl += wsum[i];
-        const int excl = incl - hv;  // keys with a larger digit
-        if (excl < rem && incl >= rem) {
-          s_digit = 255 - tid;
-          s_rem = rem - excl;
-          s_all = hv == rem - excl;  // the whole digit is taken
-        }
-      }
-      __syncthreads();
-      prefix |= (uint64_t)s_digit << shift;
-      pmask |= (uint64_t)255 << shift;
-      rem = s_rem;
-      const bool done = s_all;
-      __syncthreads();
-      // every candidate under the prefix is taken: prefix with zero low bits
-      // is the threshold (all larger composites are taken too)
-      if (done) break;
-    }
-    thresh = prefix;
-  } else {
-    __syncthreads();
-  }
-  for (int i = tid; i < m; i += 1024) {
-    const uint64_t cv = composite(i);
-    if (cv >= thresh) {
-      const int t = ci[i];
-      atomicOr(&bm32[t >> 5], 1u << (t & 31));
-    }
-  }
-}
-
 // Exclusive scan over a 1024-thread block; returns the prefix, sets total.
 __device__ inline int block_scan_1024(int v, int* lds16, int& total) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -923,23 +698,157 @@ __device__ inline int block_scan_1024(int v, int* lds16, int& total) {
   return off + x - v;
 }
 
-// Ascending emission: bitmap tokens, then the window, then -1 padding.
-// grid (rows), 1024 threads.
-__global__ __launch_bounds__(1024) void k_sel_emit(SelArgs a) {
-  __shared__ int lds16[16];
-  const int64_t row = blockIdx.x;
-  const RowInfo ri = row_info(a, row);
+// Selection from the pooled scores and their histogram, in two launches
+// (1024 threads per workgroup; every workgroup of a row derives the same
+// threshold bin b* and need = k_eff - #(keys in bins above b*)):
+//   k_sel_filter  grid (chunks of SEL_TOKENS tokens, rows): marks the tokens
+//                 above b* in the row bitmap and collects the tokens of b*
+//                 (gathered in LDS, one global slot reservation per
+//                 workgroup);
+//   k_sel_finish  grid (rows): selects the `need` largest candidates by
+//                 (key desc, index asc), i.e. by the 64-bit composite
+//                 (key << 32) | ~index, with an 8-bit radix select that stops
+//                 at the first digit whose keys are all taken, sets their
+//                 bits, then emits the bitmap's tokens in ascending order,
+//                 the window, and -1 padding.
+// state: [3] candidates collected (starts at zero).
+constexpr int SELB = 1024;              // threads per selection workgroup
+constexpr int SEL_PER = 16;             // tokens per thread
+constexpr int SEL_TOKENS = SELB * SEL_PER;
+constexpr int SEL_LDS_CAND = 2048;      // candidates a workgroup gathers in LDS
+constexpr int RESOLVE_LDS_CAP = 6144;   // candidates the resolver keeps in LDS
+static_assert(NBINS == SELB, "one histogram bin per thread");
+
+struct SelShared {
+  union {
+    struct {
+      uint32_t key[SEL_LDS_CAND];
+      int32_t idx[SEL_LDS_CAND];
+    } cand;
+    uint64_t comp[RESOLVE_LDS_CAP];
+  } u;
+  uint32_t h[256];
+  int lds16[16];
+  int wsum[4];
+  int n, base, digit, rem, all, th[2];
+};
+
+struct Threshold {
+  int mode, bstar, need;  // mode 0: nothing to select, 1: every candidate, 2: threshold bin
+};
+
+__device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh) {
+  Threshold th{0, -1, 0};
+  if (ri.keff == 0) return th;
+  if (ri.keff == ri.N) {
+    th.mode = 1;
+    return th;
+  }
+  const int tid = threadIdx.x;
+  if (tid == 0) {  // defaults if the histogram held fewer than k_eff keys (it cannot)
+    sh.th[0] = 0;
+    sh.th[1] = 0;
+  }
+  const int cnt = (int)a.hist[row * NBINS + NBINS - 1 - tid];  // bins from the top
+  int total;
+  const int above = block_scan_1024(cnt, sh.lds16, total);
+  if (above < ri.keff && above + cnt >= ri.keff) {
+    sh.th[0] = NBINS - 1 - tid;
+    sh.th[1] = ri.keff - above;
+  }
+  __syncthreads();
+  th.mode = 2;
+  th.bstar = sh.th[0];
+  th.need = sh.th[1];
+  return th;
+}
+
+// The need largest of the m candidates get their bitmap bits.
+__device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, SelShared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t* ck = a.cand_key + row * a.cand_cap;
+  const int32_t* ci = a.cand_idx + row * a.cand_cap;
+  uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
+  if (need <= 0 || m <= 0) return;
+  const bool in_lds = m <= RESOLVE_LDS_CAP;
+  auto composite = [&](int i) -> uint64_t {
+    return in_lds ? sh.u.comp[i] : (((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]));
+  };
+  if (in_lds)
+    for (int i = tid; i < m; i += SELB) sh.u.comp[i] = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
+  uint64_t thresh = 0;  // composite of the need-th largest (0: take every candidate)
+  if (need < m) {
+    uint64_t prefix = 0, pmask = 0;
+    int rem = need;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+      if (tid < 256) sh.h[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < m; i += SELB) {
+        const uint64_t cv = composite(i);
+        if ((cv & pmask) == prefix) atomicAdd(&sh.h[(cv >> shift) & 255], 1u);
+      }
+      __syncthreads();
+      // suffix sums from the top digit: thread t < 256 holds digit 255 - t
+      int x = 0, hv = 0;
+      if (tid < 256) {
+        hv = (int)sh.h[255 - tid];
+        x = hv;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(x, o);
+          if (lane >= o) x += y;
+        }
+        if (lane == 63) sh.wsum[w] = x;
+      }
+      __syncthreads();
+      if (tid < 256) {
+        int incl = x;
+        for (int i = 0; i < w; ++i) incl += sh.wsum[i];
+        const int excl = incl - hv;  // keys with a larger digit
+        if (excl < rem && incl >= rem) {
+          sh.digit = 255 - tid;
+          sh.rem = rem - excl;
+          sh.all = hv == rem - excl;  // the whole digit is taken
+        }
+      }
+      __syncthreads();
+      prefix |= (uint64_t)sh.digit << shift;
+      pmask |= (uint64_t)255 << shift;
+      rem = sh.rem;
+      const bool done = sh.all;
+      __syncthreads();
+      // every candidate under the prefix is taken: prefix with zero low bits
+      // is the threshold (all larger composites are taken too)
+      if (done) break;
+    }
+    thresh = prefix;
+  } else {
+    __syncthreads();
+  }
+  for (int i = tid; i < m; i += SELB) {
+    const uint64_t cv = composite(i);
+    if (cv >= thresh) {
+      const int t = ci[i];
+      atomicOr(&bm32[t >> 5], 1u << (t & 31));
+    }
+  }
+}
+
+// Ascending emission into the row's index slots.  The bitmap words are read
+// with agent-scope atomic loads: this workgroup has just set bits in them
+// with device atomics (ordered before these loads by the block barrier).
+__device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh) {
   int32_t* out = a.idx + row * a.S;
-  const uint64_t* bm = a.bitmap + row * a.bitmap_words;
+  uint64_t* bm = a.bitmap + row * a.bitmap_words;
   const int tid = threadIdx.x;
   const int nwords = (ri.N + 63) >> 6;
   int base = 0;
-  for (int w0 = 0; w0 < nwords; w0 += 1024) {
+  for (int w0 = 0; w0 < nwords; w0 += SELB) {
     const int w = w0 + tid;
-    uint64_t bits = w < nwords ? bm[w] : 0ull;
+    uint64_t bits = w < nwords ? __hip_atomic_load(&bm[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
     if (w == nwords - 1 && (ri.N & 63)) bits &= (1ull << (ri.N & 63)) - 1ull;  // tail bits are not maintained
     int total;
-    int off = block_scan_1024(__popcll(bits), lds16, total);
+    int off = block_scan_1024(__popcll(bits), sh.lds16, total);
     while (bits) {
       const int bit = __ffsll((long long)bits) - 1;
       bits &= bits - 1;
@@ -950,9 +859,92 @@ __global__ __launch_bounds__(1024) void k_sel_emit(SelArgs a) {
   }
   const int wlo = ri.pos - a.W + 1 < 0 ? 0 : ri.pos - a.W + 1;
   const int nw = ri.pos >= 0 ? ri.pos - wlo + 1 : 0;
-  for (int j = tid; j < nw; j += 1024)
+  for (int j = tid; j < nw; j += SELB)
     if (base + j < a.S) out[base + j] = wlo + j;
-  for (int j = base + nw + tid; j < a.S; j += 1024) out[j] = -1;
+  for (int j = base + nw + tid; j < a.S; j += SELB) out[j] = -1;
+}
+
+__global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
+  __shared__ SelShared sh;
+  const int64_t row = blockIdx.y;
+  const RowInfo ri = row_info(a, row);
+  const int t0 = blockIdx.x * SEL_TOKENS;
+  if (t0 >= ri.N) return;
+  const int t1 = min(ri.N, t0 + SEL_TOKENS);
+  const float* P = a.scores + row * a.score_stride;
+  uint64_t* bm = a.bitmap + row * a.bitmap_words;
+  int* st = a.state + row * 8;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float v[SEL_PER];
+#pragma unroll
+  for (int j = 0; j < SEL_PER; ++j) {
+    const int t = t0 + SELB * j + tid;
+    v[j] = t < t1 ? P[t] : 0.f;
+  }
+  if (tid == 0) sh.n = 0;
+  const Threshold th = find_threshold(a, row, ri, sh);
+  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
+#pragma unroll
+  for (int j = 0; j < SEL_PER; ++j) {
+    const int tb = t0 + SELB * j + 64 * wave;  // this wave's 64 tokens: one bitmap word
+    if (tb >= t1) break;  // uniform across the wave
+    const int t = tb + lane;
+    const bool valid = t < t1;
+    const uint32_t key = score_key(v[j]);
+    const int d = score_digit(key);
+    const bool sel = valid && (th.mode == 1 || (th.mode == 2 && d > th.bstar));
+    const bool cand = valid && th.mode == 2 && d == th.bstar;
+    const uint64_t sm = __ballot(sel);
+    if (lane == 0) bm[tb >> 6] = sm;
+    const uint64_t cm = __ballot(cand);
+    if (cm) {
+      // LDS slots [off, off + cnt) are claimed; those at or past the LDS
+      // capacity go to global slots reserved here (LDS slots below the
+      // capacity are then all written exactly once)
+      const int leader = __builtin_ctzll(cm);
+      const int cnt = __popcll(cm);
+      int off = 0, gbase = 0;
+      if (lane == leader) {
+        off = atomicAdd(&sh.n, cnt);
+        const int excess = off + cnt - max(off, SEL_LDS_CAND);
+        if (excess > 0) gbase = atomicAdd(&st[3], excess);
+      }
+      off = __shfl(off, leader);
+      gbase = __shfl(gbase, leader);
+      if (cand) {
+        const int slot = off + __popcll(cm & ((1ull << lane) - 1ull));
+        if (slot < SEL_LDS_CAND) {
+          sh.u.cand.key[slot] = key;
+          sh.u.cand.idx[slot] = t;
+        } else {
+          const int64_t gs = row * a.cand_cap + gbase + (slot - max(off, SEL_LDS_CAND));
+          a.cand_key[gs] = key;
+          a.cand_idx[gs] = t;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int n = min(sh.n, SEL_LDS_CAND);
+  if (n > 0) {
+    if (tid == 0) sh.base = atomicAdd(&st[3], n);
+    __syncthreads();
+    const int64_t dst = row * a.cand_cap + sh.base;
+    for (int i = tid; i < n; i += SELB) {
+      a.cand_key[dst + i] = sh.u.cand.key[i];
+      a.cand_idx[dst + i] = sh.u.cand.idx[i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
+  __shared__ SelShared sh;
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(a, row);
+  const Threshold th = find_threshold(a, row, ri, sh);
+  if (th.mode == 2) resolve_row(a, row, th.need, min(a.state[row * 8 + 3], (int)a.cand_cap), sh);
+  __syncthreads();
+  emit_row(a, row, ri, sh);
 }
 
 // ============================================================================ sparse attention
@@ -1222,16 +1214,12 @@ hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s) {
   HS2_LAUNCH(k_sel_hist, dim3(nchunks, (unsigned)a.rows), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_sel_filter(const SelArgs& a, int nchunks, hipStream_t s) {
-  HS2_LAUNCH(k_sel_filter, dim3(nchunks, (unsigned)a.rows), dim3(NT), 0, s, a);
-  return hipGetLastError();
-}
-hipError_t launch_sel_resolve(const SelArgs& a, hipStream_t s) {
-  HS2_LAUNCH(k_sel_resolve, dim3((unsigned)a.rows), dim3(1024), 0, s, a);
-  return hipGetLastError();
-}
-hipError_t launch_sel_emit(const SelArgs& a, hipStream_t s) {
-  HS2_LAUNCH(k_sel_emit, dim3((unsigned)a.rows), dim3(1024), 0, s, a);
+hipError_t launch_select(const SelArgs& a, hipStream_t s) {
+  const int64_t chunks = ((int64_t)a.max_len + SEL_TOKENS - 1) / SEL_TOKENS;
+  HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELB), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  HS2_LAUNCH(k_sel_finish, dim3((unsigned)a.rows), dim3(SELB), 0, s, a);
   return hipGetLastError();
 }
 

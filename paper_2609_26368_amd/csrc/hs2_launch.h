@@ -95,9 +95,7 @@ size_t pool_smem_bytes(int RT, int C);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
-hipError_t launch_sel_filter(const SelArgs& a, int nchunks, hipStream_t s);
-hipError_t launch_sel_resolve(const SelArgs& a, hipStream_t s);
-hipError_t launch_sel_emit(const SelArgs& a, hipStream_t s);
+hipError_t launch_select(const SelArgs& a, hipStream_t s);
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s);
 
 }  // namespace hs2
