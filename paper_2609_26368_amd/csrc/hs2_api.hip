@@ -122,12 +122,20 @@ size_t carve(size_t& cur, size_t bytes) {
 struct DeviceInfo {
   int cus = 256;
   int fa_wgs[4][kFaVariants] = {};  // [log2 RT][variant]; 0 = unknown
+  int pool_wgs[4][7][17] = {};      // k_pool: [log2 RT][log2 Gp][C]; 0 = unknown
 };
 
+int ilog2(int v) {
+  int l = 0;
+  while ((1 << (l + 1)) <= v) ++l;
+  return l;
+}
+
 // Measured on MI355X with one-round splits: 32-token tiles in 3 stages for
-// one row tile, 16-token tiles in 3 stages for two and four, the workgroup
-// kernel for eight.
-int default_fa_variant(int RT) { return RT >= 8 ? 1 : RT == 1 ? 2 : 3; }
+// one row tile; 16-token tiles in 3 stages and two token groups merged in
+// LDS (half the split partials) for two and four; the workgroup kernel for
+// eight.
+int default_fa_variant(int RT) { return RT >= 8 ? 1 : RT == 1 ? 2 : 5; }
 
 void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const DeviceInfo* di) {
   p.B = d->batch;
@@ -157,12 +165,18 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int wgs_cu = di && di->fa_wgs[lrt][p.fa_variant] > 0 ? di->fa_wgs[lrt][p.fa_variant] : 4;
   const int64_t slots = (int64_t)(di ? di->cus : 256) * wgs_cu * std::max(1, env_int("HS2_FA_ROUNDS", 1));
   const int64_t per_unit = std::max<int64_t>(1, slots / p.units);
-  int split = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, per_unit), 64));
+  const int align = fa_split_align(p.RT, p.fa_variant);
+  int split = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, per_unit), align));
   split = env_int("HS2_FA_SPLIT", split);
-  split = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(split, p.Lmax), 64));
+  split = (int)std::max<int64_t>(align, round_up(std::min<int64_t>(split, p.Lmax), align));
   p.fa_split = split;
   p.fa_nsplit = (int)cdiv(p.Lmax, split);
-  int psplit = env_int("HS2_POOL_SPLIT", split);
+  // score pass over K: the same one-round rule for its own kernel; at most
+  // 32768 tokens per split (16-bit histogram counters in LDS)
+  const int pool_cu = di && p.C <= 16 ? di->pool_wgs[lrt][ilog2(p.Gp)][p.C] : 0;
+  const int64_t pslots = (int64_t)(di ? di->cus : 256) * (pool_cu > 0 ? pool_cu : 4);
+  int psplit = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, std::max<int64_t>(1, pslots / p.units)), 64));
+  psplit = env_int("HS2_POOL_SPLIT", psplit);
   psplit = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(std::min(psplit, 32768), p.Lmax), 64));
   p.pool_split = psplit;
   p.pool_nsplit = (int)cdiv(p.Lmax, psplit);
@@ -256,10 +270,15 @@ hs2_status ensure_device_init(const DeviceInfo** info) {
     DeviceInfo di;
     if ((e = hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
       return fail(HS2_ERR_HIP, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
-    for (int l = 0; l < 4; ++l)
+    for (int l = 0; l < 4; ++l) {
       for (int v = 0; v < kFaVariants; ++v)
         if ((e = fa_wgs_per_cu(1 << l, v, &di.fa_wgs[l][v])) != hipSuccess)
           return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+      for (int lg = 0; lg < 7; ++lg)
+        for (int c = 1; c <= 16; ++c)
+          if ((e = pool_wgs_per_cu(1 << l, 1 << lg, c, &di.pool_wgs[l][lg][c])) != hipSuccess)
+            return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+    }
     g_dev[dev] = di;
     g_dev_done[dev] = true;
   }

@@ -135,6 +135,23 @@ __device__ inline void store_tile(TileLds& s, const TileRegs& r, int tid) {
 // taken against, mt the true running maximum of the log2-domain logits; l is
 // this lane's share of the running sum; o holds the unnormalised output rows
 // 4(lane/16)+i, columns 16*nb + (lane & 15).
+// x combined with its value in lane ^ 16 (^ 32) through gfx950's VALU lane
+// swaps instead of an LDS permute: swapping a register with itself leaves
+// each lane's pair {x[lane], x[lane ^ 16]} in the two result registers, so
+// max and sum are identical in both lanes of a pair.
+__device__ inline float2 lane_pair16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float2 lane_pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float max_xor16(float x) { const float2 p = lane_pair16(x); return fmaxf(p.x, p.y); }
+__device__ inline float max_xor32(float x) { const float2 p = lane_pair32(x); return fmaxf(p.x, p.y); }
+__device__ inline float sum_xor16(float x) { const float2 p = lane_pair16(x); return p.x + p.y; }
+__device__ inline float sum_xor32(float x) { const float2 p = lane_pair32(x); return p.x + p.y; }
+
 template <int RPW>
 struct WaveState {
   float m[RPW];   // reference maximum the probabilities are taken against
@@ -185,8 +202,7 @@ __device__ inline void online_softmax(WaveState<RPW>& st, f32x4 (&S)[BPW][RPW], 
 #pragma unroll
     for (int bi = 0; bi < BPW; ++bi)
       mx = fmaxf(mx, fmaxf(fmaxf(S[bi][rr][0], S[bi][rr][1]), fmaxf(S[bi][rr][2], S[bi][rr][3])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_xor32(max_xor16(mx));
     st.mt[rr] = fmaxf(st.mt[rr], mx);
     if (__ballot(mx > st.m[rr] + LAZY_MARGIN)) {
       const float mnew = fmaxf(st.m[rr], mx);
@@ -243,8 +259,7 @@ __device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     float l = st.l[rr];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    l = sum_xor32(sum_xor16(l));
     const int64_t row0 = slot_base_row + 16 * (rt0 + rr);
     if (lane < 16) *(float4*)(part_ml + (row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
 #pragma unroll
@@ -378,14 +393,19 @@ __device__ inline void softmax_pv_swz(WaveState<RPW>& st, const unsigned char* s
 // No workgroup barrier: the wave only waits for its own direct LDS loads.
 constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
-// s_waitcnt vmcnt(per_stage * stages) for stages in [0, 3]
+// s_waitcnt vmcnt(per_stage * stages) for stages in [0, 5] (larger values
+// wait as for 5; counts above the 6-bit field wait for 63: both only wait
+// longer than needed)
+constexpr int vmcnt_enc_sat(int n) { return vmcnt_enc(n > 63 ? 63 : n); }
 template <int PER_STAGE>
 __device__ inline void wait_ring(int stages) {
   switch (stages) {
     case 0: __builtin_amdgcn_s_waitcnt(vmcnt_enc(0)); break;
-    case 1: __builtin_amdgcn_s_waitcnt(vmcnt_enc(PER_STAGE)); break;
-    case 2: __builtin_amdgcn_s_waitcnt(vmcnt_enc(2 * PER_STAGE)); break;
-    default: __builtin_amdgcn_s_waitcnt(vmcnt_enc(3 * PER_STAGE)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(vmcnt_enc_sat(PER_STAGE)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(vmcnt_enc_sat(2 * PER_STAGE)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(vmcnt_enc_sat(3 * PER_STAGE)); break;
+    case 4: __builtin_amdgcn_s_waitcnt(vmcnt_enc_sat(4 * PER_STAGE)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_enc_sat(5 * PER_STAGE)); break;
   }
 }
 

@@ -149,21 +149,27 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // streams through a private ring with NS - 1 stages in flight; with one wave
 // there is no barrier at all, with two waves one barrier per stage.  One
 // partial (m, l, O) per split.
-template <int RT, int NWV, int TW, int NS>
-__global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
+template <int RT, int NWV, int TW, int NS, int TGW>
+__global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
   constexpr int NB = TW / 16;             // 16-row blocks per stage
   constexpr int LPM = TW / 4 / NWV;       // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
+  static_assert(TGW == 1 || (TGW == 2 && RT > 1), "two token groups, not with the logits output");
+  static_assert(TGW == 1 || 2 * 16 * RT * 16 + 16 * RT * HD * 4 <= TGW * NS * SB, "merge fits in the rings");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int tg = (threadIdx.x >> 6) / NWV, wave = (threadIdx.x >> 6) % NWV;  // token group, wave in it
   const int Lv = clamp_len(a.len, b, a.max_len);
-  const int t_begin = split * a.split_tokens;
-  if (t_begin >= Lv) return;
-  const int t_end = min(Lv, t_begin + a.split_tokens);
-  const int ntiles = (t_end - t_begin + TW - 1) / TW;
+  if (split * a.split_tokens >= Lv) return;
+  // token group tg streams the tg-th contiguous part of the split through its own ring
+  const int part = a.split_tokens / TGW;
+  const int t_begin = split * a.split_tokens + tg * part;
+  const int t_end = min(Lv, t_begin + part);
+  const int ntiles = t_end > t_begin ? (t_end - t_begin + TW - 1) / TW : 0;
+  const int nloop = (min(Lv, split * a.split_tokens + part) - split * a.split_tokens + TW - 1) / TW;  // group 0's
   const int rt0 = wave * RPW;
 
   uint4 q[RPW][4];
@@ -178,7 +184,8 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
   const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
   const uint16_t* Kbg = a.K + kvoff;
   const uint16_t* Vbg = a.V + kvoff;
-  const uint32_t ring = lds_addr(smem);
+  const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * NS * SB);
+  unsigned char* ring_p = smem + tg * NS * SB;
   // logits output of a single row tile (C G <= 16 query rows): this lane's
   // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
   float* lrow = nullptr;
@@ -220,12 +227,15 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
     if (i < ntiles) issue(i);
-  for (int i = 0; i < ntiles; ++i) {
+  // every wave runs group 0's tile count (the barrier count must match); a
+  // group past its own tiles only takes part in the barrier
+  for (int i = 0; i < nloop; ++i) {
     // logits stores also count in vmcnt; they only make this wait longer
-    wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
-    if (NWV > 1) __syncthreads();
+    if (i < ntiles) wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
+    if (NWV * TGW > 1) __syncthreads();
+    if (i >= ntiles) continue;
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
-    const unsigned char* stg = smem + (i % NS) * SB;
+    const unsigned char* stg = ring_p + (i % NS) * SB;
     const int t0 = t_begin + i * TW;
     f32x4 S[NB][RPW];
 #pragma unroll
@@ -263,7 +273,50 @@ __global__ __launch_bounds__(64 * NWV) void k_fa_ring(FaArgs a) {
   }
   const int64_t unit = (int64_t)b * a.Hkv + g;
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
-  store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
+  if constexpr (TGW == 1) {
+    store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
+  } else {
+    // merge the two token groups in LDS (the rings are free), one partial per split
+    __syncthreads();
+    float* mlL = (float*)smem;            // [2][16 RT][4]: (m ref, l, m true, -)
+    float* oL = mlL + 2 * 16 * RT * 4;    // [16 RT][HD]: group 1's O
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+      float l = st.l[rr];
+      l = sum_xor32(sum_xor16(l));
+      const int row0 = 16 * (rt0 + rr);
+      if (lane < 16) *(float4*)(mlL + ((tg * 16 * RT) + row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
+      if (tg == 1)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) oL[(row0 + 4 * (lane >> 4) + i) * HD + 16 * nb + (lane & 15)] = st.o[rr][nb][i];
+    }
+    __syncthreads();
+    if (tg == 1) return;
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+      const int row0 = 16 * (rt0 + rr);
+      if (lane < 16) {
+        const float4 x = *(const float4*)(mlL + (row0 + lane) * 4);
+        const float4 y = *(const float4*)(mlL + (16 * RT + row0 + lane) * 4);
+        const float M = fmaxf(x.x, y.x);
+        const float fx = x.x == -INFINITY ? 0.f : fast_exp2(x.x - M), fy = y.x == -INFINITY ? 0.f : fast_exp2(y.x - M);
+        *(float4*)(a.part_ml + (slot_base_row + row0 + lane) * 4) =
+            make_float4(M, x.y * fx + y.y * fy, fmaxf(x.z, y.z), 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int R = row0 + 4 * (lane >> 4) + i;
+        const float m0 = mlL[R * 4], m1 = mlL[(16 * RT + R) * 4];
+        const float M = fmaxf(m0, m1);
+        const float f0 = m0 == -INFINITY ? 0.f : fast_exp2(m0 - M), f1 = m1 == -INFINITY ? 0.f : fast_exp2(m1 - M);
+        float* dst = a.part_o + (slot_base_row + R) * HD + (lane & 15);
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) dst[16 * nb] = st.o[rr][nb][i] * f0 + oL[R * HD + 16 * nb + (lane & 15)] * f1;
+      }
+    }
+  }
 }
 
 // ============================================================================ combine
@@ -373,154 +426,112 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
 // P = sum over the heads h of query c of exp2(s2_h(t) - M2_h) / Z_h, with the
 // same logits s2 the full-attention kernel used and its merged (M2, Z).
 //
-// k_pool writes every candidate's score and the rows' first-level histogram
-// of score keys.  grid (token splits, Hkv, B), 256 threads.  Each wave
-// handles 16 PB tokens at a time with K rows loaded straight into MFMA
-// operand registers; queries come from LDS.  Logits are computed as S = Q . K^T
-// (query rows on MFMA rows), so lane l holds rows 4(l/16)+i of token l%16:
-// the GP heads of a query are summed inside the lane and across at most two
-// lane groups, and the 16 scores of a block sit in 16 consecutive lanes.
-// p = exp2(s2 - msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless
-// M2 is too large for that, then msub = M2 and fac = 1 / Z).
+// Both score kernels write every candidate's score and the rows' first-level
+// histogram of score keys: k_pool recomputes the logits from K, k_pool_logits
+// reads the ones the full-attention kernel stored.  Logits are computed as
+// S = Q . K^T (query rows on MFMA rows), so lane l holds rows 4(l/16)+i of
+// token l%16: the GP heads of a query are summed inside the lane and across
+// at most two lane groups, and the 16 scores of a block sit in 16
+// consecutive lanes.
 
-// Fill the query rows (LDS) and this lane's row constants.
-template <int RT, int GP>
-__device__ __forceinline__ void pool_setup(const PoolArgs& a, int b, int g, uint16_t* qs, float (&fac)[RT][4],
-                                  float (&msub)[RT][4], int tid, int lane) {
-  for (int i = tid; i < 16 * RT * 16; i += NT) {
-    const int r = i >> 4, cgq = i & 15;
-    const int c = r / GP, h = r % GP;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (c < a.C && h < a.G) v = *(const uint4*)(a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HD + cgq * 8);
-    *(uint4*)&qs[r * KPAD + cgq * 8] = v;
-  }
-  // Branch-free on purpose: conditional stores into fac / msub make the
-  // compiler carry both arrays whole through every merge.
+// Scores of one 16-token block from the logits in acc (S = Q.K^T: lane l
+// holds rows 16 (rt0 + rr) + 4 (l / 16) + i of token l % 16): p = exp2(s2 -
+// msub) * fac per head, summed over the GP heads of each query (in-lane, then
+// across lane groups / row tiles); emit(v, c, t) is called by the lanes
+// holding query c's score of token t.
+template <int RPW, int GP, class Emit>
+__device__ __forceinline__ void pool_emit_block(const f32x4 (&acc)[RPW], float c2, const float (&fac)[RPW][4],
+                                                const float (&msub)[RPW][4], int rt0, int t, int lane, Emit& emit) {
+  const int q4 = lane >> 4;
+  float e[RPW][4];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
+  for (int rr = 0; rr < RPW; ++rr)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) e[rr][i] = fast_exp2(acc[rr][i] * c2 - msub[rr][i]) * fac[rr][i];
+  if constexpr (GP == 1) {
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) emit(e[rr][i], 16 * (rt0 + rr) + 4 * q4 + i, t);
+  } else if constexpr (GP == 2) {
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+      emit(e[rr][0] + e[rr][1], 8 * (rt0 + rr) + 2 * q4, t);
+      emit(e[rr][2] + e[rr][3], 8 * (rt0 + rr) + 2 * q4 + 1, t);
+    }
+  } else if constexpr (GP <= 16) {
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+      float v = (e[rr][0] + e[rr][1]) + (e[rr][2] + e[rr][3]);
+      if constexpr (GP >= 8) v = sum_xor16(v);
+      if constexpr (GP >= 16) v = sum_xor32(v);
+      // rows 16 rt + 4 q4 .. belong to query (16 rt + 4 q4) / GP; one lane group per query emits
+      if (((4 * q4) & (GP - 1)) == 0) emit(v, (16 * (rt0 + rr) + 4 * q4) / GP, t);
+    }
+  } else {
+    constexpr int TPQ = GP / 16;  // row tiles per query, all in this wave
+    static_assert(RPW % TPQ == 0, "a query's row tiles must belong to one wave");
+#pragma unroll
+    for (int cq = 0; cq < RPW / TPQ; ++cq) {
+      float v = 0.f;
+#pragma unroll
+      for (int j = 0; j < TPQ; ++j) {
+        const int rr = cq * TPQ + j;
+        v += (e[rr][0] + e[rr][1]) + (e[rr][2] + e[rr][3]);
+      }
+      v = sum_xor32(sum_xor16(v));
+      if (q4 == 0) emit(v, (16 * rt0) / GP + cq, t);
+    }
+  }
+}
+
+// Row constants of rows 16 (rt0 + rr) + 4 (lane / 16) + i: p = exp2(s2 -
+// msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless M2 is too large
+// for that, then msub = M2 and fac = 1 / Z).  Branch-free on purpose:
+// conditional stores into the arrays make the compiler carry them whole.
+template <int RPW, int GP>
+__device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g, int rt0, int lane,
+                                                float (&fac)[RPW][4], float (&msub)[RPW][4]) {
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = 16 * rt + 4 * (lane >> 4) + i;
+      const int r = 16 * (rt0 + rr) + 4 * (lane >> 4) + i;
       const int c = r / GP, h = r % GP;
       const bool valid = c < a.C && h < a.G;  // padding rows contribute nothing
       const int64_t orow = valid ? ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h : 0;
       const float2 mz = *(const float2*)(a.stats_log2 + orow * 2);
       const float z = valid ? mz.y : 0.f;
-      const bool big = !(fabsf(mz.x) < 64.f);  // large maxima: subtract first to stay in range
+      const bool big = !(fabsf(mz.x) < 64.f);
       const float inv_z = 1.f / z;
-      fac[rt][i] = z > 0.f ? (big ? inv_z : fast_exp2(-mz.x) * inv_z) : 0.f;  // exact power of two over Z
-      msub[rt][i] = (z > 0.f && big) ? mz.x : 0.f;
+      fac[rr][i] = z > 0.f ? (big ? inv_z : fast_exp2(-mz.x) * inv_z) : 0.f;
+      msub[rr][i] = (z > 0.f && big) ? mz.x : 0.f;
     }
 }
 
-// Scores of PB blocks of 16 tokens whose K rows are in kb (block blk holds
-// tokens tg0 + 16 blk + 0..15); emit(v, c, t) is called by the lanes holding
-// query c's score of token t = tg0 + 16 blk + lane % 16.
-constexpr int PB = 2;  // 16-token blocks per register buffer
-template <int RT, int GP, class Emit>
-__device__ __forceinline__ void pool_group(float c2, const uint4 (&kb)[PB][4], int tg0, const uint16_t* qs,
-                                  const float (&fac)[RT][4], const float (&msub)[RT][4], int lane, Emit& emit) {
-  const int q4 = lane >> 4;
-#pragma unroll
-  for (int blk = 0; blk < PB; ++blk) {
-    const int t = tg0 + 16 * blk + (lane & 15);  // this lane's token
-    float e[RT][4];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const uint16_t* qp = qs + (16 * rt + (lane & 15)) * KPAD + 8 * q4;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(*(const uint4*)(qp + 32 * kk), kb[blk][kk], acc);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) e[rt][i] = fast_exp2(acc[i] * c2 - msub[rt][i]) * fac[rt][i];
-    }
-    if constexpr (GP == 1) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) emit(e[rt][i], 16 * rt + 4 * q4 + i, t);
-    } else if constexpr (GP == 2) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        emit(e[rt][0] + e[rt][1], 8 * rt + 2 * q4, t);
-        emit(e[rt][2] + e[rt][3], 8 * rt + 2 * q4 + 1, t);
-      }
-    } else if constexpr (GP <= 16) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        float v = (e[rt][0] + e[rt][1]) + (e[rt][2] + e[rt][3]);
-        if constexpr (GP >= 8) v += __shfl_xor(v, 16);
-        if constexpr (GP >= 16) v += __shfl_xor(v, 32);
-        // rows 16 rt + 4 q4 .. belong to query (16 rt + 4 q4) / GP; one lane group per query emits
-        if (((4 * q4) & (GP - 1)) == 0) emit(v, (16 * rt + 4 * q4) / GP, t);
-      }
-    } else {
-      constexpr int TPQ = GP / 16;  // row tiles per query
-#pragma unroll
-      for (int c = 0; c < RT / TPQ; ++c) {
-        float v = 0.f;
-#pragma unroll
-        for (int j = 0; j < TPQ; ++j) {
-          const int rt = c * TPQ + j;
-          v += (e[rt][0] + e[rt][1]) + (e[rt][2] + e[rt][3]);
-        }
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        if (q4 == 0) emit(v, c, t);
-      }
-    }
-  }
-}
-
-// K rows of tokens tok(blk) (one per lane, tok < 0: zeros) in MFMA B layout.
-template <class TokOf>
-__device__ __forceinline__ void pool_load_rows(uint4 (&kb)[PB][4], const uint16_t* __restrict__ Kbg, int64_t stride_t,
-                                      TokOf tok_of, int lane) {
-#pragma unroll
-  for (int blk = 0; blk < PB; ++blk) {
-    const int t = tok_of(blk);
-    if (t >= 0) {
-      const uint16_t* p = Kbg + (int64_t)t * stride_t + 8 * (lane >> 4);
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) kb[blk][kk] = *(const uint4*)(p + 32 * kk);
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) kb[blk][kk] = make_uint4(0, 0, 0, 0);
-    }
-  }
-}
-
-// Stream the contiguous token range [t_begin, t_end): wave w handles groups
-// of 16 PB tokens w, w + 4, ..., double-buffered.
-template <int RT, int GP, class Emit>
-__device__ __forceinline__ void pool_stream(const PoolArgs& a, const uint16_t* Kbg, int t_begin, int t_end, const uint16_t* qs,
-                                   const float (&fac)[RT][4], const float (&msub)[RT][4], int wave, int lane,
-                                   Emit& emit) {
-  constexpr int GT = 16 * PB;  // tokens per group
-  uint4 kb0[PB][4], kb1[PB][4];
-  auto contiguous = [&](int tg0) {
-    return [=](int blk) {
-      const int t = tg0 + 16 * blk + (lane & 15);
-      return t < t_end ? t : -1;
-    };
-  };
-  int g0 = t_begin + GT * wave;
-  if (g0 < t_end) pool_load_rows(kb0, Kbg, a.stride_t, contiguous(g0), lane);
-  for (; g0 < t_end; g0 += 8 * GT) {
-    const int g1 = g0 + 4 * GT;
-    if (g1 < t_end) pool_load_rows(kb1, Kbg, a.stride_t, contiguous(g1), lane);
-    pool_group<RT, GP>(a.c2, kb0, g0, qs, fac, msub, lane, emit);
-    if (g1 >= t_end) break;
-    if (g1 + 4 * GT < t_end) pool_load_rows(kb0, Kbg, a.stride_t, contiguous(g1 + 4 * GT), lane);
-    pool_group<RT, GP>(a.c2, kb1, g1, qs, fac, msub, lane, emit);
-  }
-}
-
+// Scores by a second pass over K, streamed like the full-attention kernel:
+// grid (token splits, Hkv, B), 64 * NWV threads; K tiles of TW tokens go
+// global -> LDS through an NS-stage ring (16-byte direct loads, swizzled
+// rows), every wave reads the whole tile as the MFMA B operand against its
+// own query row tiles held in registers.  Dynamic LDS: ring + C packed
+// first-level histograms (16-bit counters; a split has < 65536 tokens).
 template <int RT, int GP>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_pool(PoolArgs a) {
+struct PoolShape {
+  static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
+  static constexpr int RPW = RT == 1 ? 1 : (TPQ > 2 ? TPQ : 2);  // row tiles per wave
+  static constexpr int NWV = RT / RPW;
+  static constexpr int TW = 16, NS = 4;
+  static constexpr int SB = TW * STAGE_ROW_BYTES;
+};
+template <int RT, int GP>
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
+  using PS = PoolShape<RT, GP>;
+  constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB;
+  constexpr int NB = TW / 16;
+  constexpr int LPM = TW / 4 / NWV;  // 1 KB loads per stage per wave
+  static_assert(LPM >= 1, "each wave loads at least one 1 KB piece per stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  uint16_t* qs = (uint16_t*)smem;                                           // [16 RT][KPAD]
-  uint32_t* hist = (uint32_t*)(smem + 16 * RT * KPAD * sizeof(uint16_t));  // [C][NBINS/2]
+  uint32_t* hist = (uint32_t*)(smem + NS * SB);  // [C][NBINS/2]
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -530,11 +541,42 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int t_begin = split * a.split_tokens;
   if (t_begin >= n_cand_max) return;
   const int t_end = min(n_cand_max, t_begin + a.split_tokens);
+  const int ntiles = (t_end - t_begin + TW - 1) / TW;
+  const int rt0 = wave * RPW;
 
-  for (int i = tid; i < a.C * (NBINS / 2); i += NT) hist[i] = 0;
-  float fac[RT][4], msub[RT][4];
-  pool_setup<RT, GP>(a, b, g, qs, fac, msub, tid, lane);
-  __syncthreads();
+  for (int i = tid; i < a.C * (NBINS / 2); i += 64 * NWV) hist[i] = 0;
+  uint4 q[RPW][4];
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) load_q_tile(q[rr], a.q, rt0 + rr, lane, GP, a.G, a.C, a.Hq, g, b);
+  float fac[RPW][4], msub[RPW][4];
+  pool_row_consts<RPW, GP>(a, b, g, rt0, lane, fac, msub);
+
+  const uint16_t* Kbg = a.K + (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
+  const uint32_t ring = lds_addr(smem);
+  int64_t lane_off[LPM];
+#pragma unroll
+  for (int u = 0; u < LPM; ++u) {
+    const int row = 4 * (wave * LPM + u) + (lane >> 4);
+    lane_off[u] = (int64_t)row * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+  }
+  auto issue = [&](int tile) {
+    const int t0 = t_begin + tile * TW;
+    const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
+    const bool whole = t0 + TW <= t_end;
+    const int64_t tile_off = (int64_t)t0 * a.stride_t;
+#pragma unroll
+    for (int u = 0; u < LPM; ++u) {
+      const int n = wave * LPM + u;
+      int64_t off = tile_off + lane_off[u];
+      if (!whole) {  // rows past the range repeat the last valid row; never emitted
+        const int row = 4 * n + (lane >> 4);
+        const int t = min(t0 + row, t_end - 1);
+        off = (int64_t)t * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+      }
+      dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+    }
+  };
+  __syncthreads();  // histogram cleared before any wave adds to it
 
   float* scores = a.scores + ((int64_t)b * a.Hkv + g) * a.C * a.score_stride;
   const int nc0 = Lv - a.C - a.W + 1;  // candidates of query 0 (query c: nc0 + c)
@@ -547,12 +589,36 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2))) void k_
       }
     }
   };
-  const uint16_t* Kbg = a.K + (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
-  pool_stream<RT, GP>(a, Kbg, t_begin, t_end, qs, fac, msub, wave, lane, emit);
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < ntiles) issue(i);
+  for (int i = 0; i < ntiles; ++i) {
+    wait_ring<LPM>(min(NS - 2, ntiles - 1 - i));
+    if (NWV > 1) __syncthreads();
+    if (i + NS - 1 < ntiles) issue(i + NS - 1);
+    const unsigned char* stg = smem + (i % NS) * SB;
+    const int t0 = t_begin + i * TW;
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi) {
+      const int row = 16 * bi + (lane & 15);
+      const unsigned char* rp = stg + row * STAGE_ROW_BYTES;
+      uint4 k4[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+      f32x4 acc[RPW];
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr) {
+        acc[rr] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
+      }
+      pool_emit_block<RPW, GP>(acc, a.c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
+    }
+  }
   __syncthreads();
   if (!a.hist) return;
   const int64_t row_c0 = ((int64_t)b * a.Hkv + g) * a.C;  // selection row of query 0
-  for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
+  for (int i = tid; i < a.C * (NBINS / 2); i += 64 * NWV) {
     const uint32_t v = hist[i];
     if (!v) continue;
     const int c = i / (NBINS / 2), w = i % (NBINS / 2);
@@ -1084,10 +1150,19 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 //   2: ring kernel, 32-row stages x 3;  3: 16-row stages x 3;  4: 16 x 4, one wave
 // RT = 8 always uses the workgroup kernel.
 #define HS2_RING_VARIANTS(X)                 \
-  X(0, 1, 1, 16, 4) X(0, 2, 1, 16, 4) X(0, 4, 2, 16, 4) \
-  X(2, 1, 1, 32, 3) X(2, 2, 1, 32, 3) X(2, 4, 2, 32, 3) \
-  X(3, 1, 1, 16, 3) X(3, 2, 1, 16, 3) X(3, 4, 2, 16, 3) \
-  X(4, 1, 1, 16, 4) X(4, 2, 1, 16, 4) X(4, 4, 1, 16, 4)
+  X(0, 1, 1, 16, 4, 1) X(0, 2, 1, 16, 4, 1) X(0, 4, 2, 16, 4, 1) \
+  X(2, 1, 1, 32, 3, 1) X(2, 2, 1, 32, 3, 1) X(2, 4, 2, 32, 3, 1) \
+  X(3, 1, 1, 16, 3, 1) X(3, 2, 1, 16, 3, 1) X(3, 4, 2, 16, 3, 1) \
+  X(4, 1, 1, 16, 4, 1) X(4, 2, 1, 16, 4, 1) X(4, 4, 1, 16, 4, 1) \
+  X(5, 1, 1, 32, 3, 1) X(5, 2, 1, 16, 3, 2) X(5, 4, 2, 16, 3, 2)
+
+int fa_split_align(int RT, int variant) {
+#define HS2_RING_ALIGN(v, rt, nwv, tw, ns, tgw) \
+  if (variant == v && RT == rt) return 64 * tgw;
+  HS2_RING_VARIANTS(HS2_RING_ALIGN)
+#undef HS2_RING_ALIGN
+  return 64;
+}
 
 int fa_token_groups(int RT, int variant) {
   if (RT < 8 && variant != 1) return 1;
@@ -1110,10 +1185,10 @@ static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t
 
 hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs) {
   *wgs = 0;
-#define HS2_RING_OCC(v, rt, nwv, tw, ns)                                                               \
+#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw)                                                          \
   if (variant == v && RT == rt)                                                                         \
-    return occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns>, 64 * nwv,                    \
-                            (size_t)ns * 2 * tw * STAGE_ROW_BYTES);
+    return occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw>, 64 * nwv * tgw,         \
+                            (size_t)tgw * ns * 2 * tw * STAGE_ROW_BYTES);
   HS2_RING_VARIANTS(HS2_RING_OCC)
 #undef HS2_RING_OCC
   const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
@@ -1128,9 +1203,10 @@ hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs) {
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns)                                                            \
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw)                                                       \
   if (variant == v && RT == rt) {                                                                       \
-    HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns>), grid, dim3(64 * nwv), (size_t)ns * 2 * tw * STAGE_ROW_BYTES, s, a); \
+    HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw>), grid, dim3(64 * nwv * tgw),                         \
+               (size_t)tgw * ns * 2 * tw * STAGE_ROW_BYTES, s, a);                                     \
     return hipGetLastError();                                                                          \
   }
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
@@ -1146,8 +1222,8 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) 
   return hipGetLastError();
 }
 
-size_t pool_smem_bytes(int RT, int C) {
-  return (size_t)16 * RT * KPAD * sizeof(uint16_t) + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
+size_t pool_smem_bytes(int C) {
+  return (size_t)PoolShape<1, 1>::NS * PoolShape<1, 1>::SB + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
 }
 
 // pool kernels for every (row tiles, padded group) pair the planner can produce:
@@ -1165,11 +1241,24 @@ hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, int* wgs) {
+  *wgs = 0;
+#define HS2_POOL_OCC(rt, gp)                                                                                   \
+  if (RT == rt && Gp == gp)                                                                                    \
+    return occupancy_capped(wgs, (const void*)k_pool<rt, gp>, 64 * PoolShape<rt, gp>::NWV, pool_smem_bytes(C));
+  HS2_POOL_CASES(HS2_POOL_OCC)
+#undef HS2_POOL_OCC
+  return hipSuccess;
+}
+
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-  const size_t sm = pool_smem_bytes(RT, a.C);
-#define HS2_POOL_LAUNCH(rt, gp) \
-  if (RT == rt && a.Gp == gp) { HS2_LAUNCH((k_pool<rt, gp>), grid, dim3(NT), sm, s, a); return hipGetLastError(); }
+  const size_t sm = pool_smem_bytes(a.hist ? a.C : 0);
+#define HS2_POOL_LAUNCH(rt, gp)                                                                   \
+  if (RT == rt && a.Gp == gp) {                                                                   \
+    HS2_LAUNCH((k_pool<rt, gp>), grid, dim3(64 * PoolShape<rt, gp>::NWV), sm, s, a);              \
+    return hipGetLastError();                                                                     \
+  }
   HS2_POOL_CASES(HS2_POOL_LAUNCH)
 #undef HS2_POOL_LAUNCH
   return hipErrorInvalidValue;
@@ -1189,8 +1278,8 @@ hipError_t set_pool_smem_limits() {
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<2>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<4>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<8>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-#define HS2_RING_ATTR(v, rt, nwv, tw, ns) \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw) \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   HS2_RING_VARIANTS(HS2_RING_ATTR)
 #undef HS2_RING_ATTR
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<1, 1, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);

@@ -82,8 +82,9 @@ struct SaArgs {
   int n_slots, split_slots, n_split;
 };
 
-constexpr int kFaVariants = 5;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
+constexpr int kFaVariants = 6;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
+int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
 // workgroups of the full-attention kernel (RT, variant) resident per compute
 // unit on the current device (0 if that kernel does not exist)
 hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs);
@@ -91,7 +92,9 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s);
-size_t pool_smem_bytes(int RT, int C);
+size_t pool_smem_bytes(int C);
+// workgroups of k_pool (RT, Gp) with C queries resident per compute unit
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, int* wgs);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
