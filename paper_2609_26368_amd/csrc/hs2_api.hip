@@ -154,7 +154,8 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
   p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT));
-  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || p.RT >= 8) p.fa_variant = p.RT >= 8 ? 1 : 0;
+  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || !fa_variant_exists(p.RT, p.fa_variant))
+    p.fa_variant = default_fa_variant(p.RT);
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
   p.rows = p.units * p.C;

@@ -155,8 +155,9 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int NB = TW / 16;             // 16-row blocks per stage
   constexpr int LPM = TW / 4 / NWV;       // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
-  static_assert(TGW == 1 || (TGW == 2 && RT > 1), "two token groups, not with the logits output");
-  static_assert(TGW == 1 || 2 * 16 * RT * 16 + 16 * RT * HD * 4 <= TGW * NS * SB, "merge fits in the rings");
+  static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
+  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HD * 4 <= TGW * NS * SB,
+                "the merge fits in the rings");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -276,44 +277,64 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   if constexpr (TGW == 1) {
     store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
   } else {
-    // merge the two token groups in LDS (the rings are free), one partial per split
+    // merge the token groups in LDS (the rings are free), one partial per split
+    constexpr int ROWS = 16 * RT;
     __syncthreads();
-    float* mlL = (float*)smem;            // [2][16 RT][4]: (m ref, l, m true, -)
-    float* oL = mlL + 2 * 16 * RT * 4;    // [16 RT][HD]: group 1's O
+    float* mlL = (float*)smem;              // [TGW][ROWS][4]: (m ref, l, m true, -)
+    float* oL = mlL + TGW * ROWS * 4;       // [TGW - 1][ROWS][HD]: the other groups' O
 #pragma unroll
     for (int rr = 0; rr < RPW; ++rr) {
-      float l = st.l[rr];
-      l = sum_xor32(sum_xor16(l));
+      const float l = sum_xor32(sum_xor16(st.l[rr]));
       const int row0 = 16 * (rt0 + rr);
-      if (lane < 16) *(float4*)(mlL + ((tg * 16 * RT) + row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
-      if (tg == 1)
+      if (lane < 16) *(float4*)(mlL + (tg * ROWS + row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
+      if (tg > 0)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int nb = 0; nb < 8; ++nb) oL[(row0 + 4 * (lane >> 4) + i) * HD + 16 * nb + (lane & 15)] = st.o[rr][nb][i];
+          for (int nb = 0; nb < 8; ++nb)
+            oL[((tg - 1) * ROWS + row0 + 4 * (lane >> 4) + i) * HD + 16 * nb + (lane & 15)] = st.o[rr][nb][i];
     }
     __syncthreads();
-    if (tg == 1) return;
+    if (tg > 0) return;
+    // weight of group j's row R against the rows' common maximum (a group
+    // without tokens has m = -inf and weight 0)
+    auto weights = [&](int R, float (&f)[TGW], float& M) {
+      M = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < TGW; ++j) M = fmaxf(M, mlL[(j * ROWS + R) * 4]);
+#pragma unroll
+      for (int j = 0; j < TGW; ++j) {
+        const float m = mlL[(j * ROWS + R) * 4];
+        f[j] = m == -INFINITY ? 0.f : fast_exp2(m - M);
+      }
+    };
 #pragma unroll
     for (int rr = 0; rr < RPW; ++rr) {
       const int row0 = 16 * (rt0 + rr);
       if (lane < 16) {
-        const float4 x = *(const float4*)(mlL + (row0 + lane) * 4);
-        const float4 y = *(const float4*)(mlL + (16 * RT + row0 + lane) * 4);
-        const float M = fmaxf(x.x, y.x);
-        const float fx = x.x == -INFINITY ? 0.f : fast_exp2(x.x - M), fy = y.x == -INFINITY ? 0.f : fast_exp2(y.x - M);
-        *(float4*)(a.part_ml + (slot_base_row + row0 + lane) * 4) =
-            make_float4(M, x.y * fx + y.y * fy, fmaxf(x.z, y.z), 0.f);
+        float f[TGW], M;
+        weights(row0 + lane, f, M);
+        float l = 0.f, mt = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < TGW; ++j) {
+          l += mlL[(j * ROWS + row0 + lane) * 4 + 1] * f[j];
+          mt = fmaxf(mt, mlL[(j * ROWS + row0 + lane) * 4 + 2]);
+        }
+        *(float4*)(a.part_ml + (slot_base_row + row0 + lane) * 4) = make_float4(M, l, mt, 0.f);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int R = row0 + 4 * (lane >> 4) + i;
-        const float m0 = mlL[R * 4], m1 = mlL[(16 * RT + R) * 4];
-        const float M = fmaxf(m0, m1);
-        const float f0 = m0 == -INFINITY ? 0.f : fast_exp2(m0 - M), f1 = m1 == -INFINITY ? 0.f : fast_exp2(m1 - M);
+        float f[TGW], M;
+        weights(R, f, M);
         float* dst = a.part_o + (slot_base_row + R) * HD + (lane & 15);
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) dst[16 * nb] = st.o[rr][nb][i] * f0 + oL[R * HD + 16 * nb + (lane & 15)] * f1;
+        for (int nb = 0; nb < 8; ++nb) {
+          float o = st.o[rr][nb][i] * f[0];
+#pragma unroll
+          for (int j = 1; j < TGW; ++j) o += oL[((j - 1) * ROWS + R) * HD + 16 * nb + (lane & 15)] * f[j];
+          dst[16 * nb] = o;
+        }
       }
     }
   }
@@ -1153,8 +1174,16 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   X(0, 1, 1, 16, 4, 1) X(0, 2, 1, 16, 4, 1) X(0, 4, 2, 16, 4, 1) \
   X(2, 1, 1, 32, 3, 1) X(2, 2, 1, 32, 3, 1) X(2, 4, 2, 32, 3, 1) \
   X(3, 1, 1, 16, 3, 1) X(3, 2, 1, 16, 3, 1) X(3, 4, 2, 16, 3, 1) \
-  X(4, 1, 1, 16, 4, 1) X(4, 2, 1, 16, 4, 1) X(4, 4, 1, 16, 4, 1) \
   X(5, 1, 1, 32, 3, 1) X(5, 2, 1, 16, 3, 2) X(5, 4, 2, 16, 3, 2)
+
+bool fa_variant_exists(int RT, int variant) {
+  if (variant == 1) return RT == 1 || RT == 2 || RT == 4 || RT == 8;  // workgroup kernel
+#define HS2_RING_HAS(v, rt, nwv, tw, ns, tgw) \
+  if (variant == v && RT == rt) return true;
+  HS2_RING_VARIANTS(HS2_RING_HAS)
+#undef HS2_RING_HAS
+  return false;
+}
 
 int fa_split_align(int RT, int variant) {
 #define HS2_RING_ALIGN(v, rt, nwv, tw, ns, tgw) \

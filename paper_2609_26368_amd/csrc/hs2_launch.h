@@ -85,6 +85,7 @@ struct SaArgs {
 constexpr int kFaVariants = 6;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
 int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
+bool fa_variant_exists(int RT, int variant);
 // workgroups of the full-attention kernel (RT, variant) resident per compute
 // unit on the current device (0 if that kernel does not exist)
 hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs);
