@@ -227,13 +227,46 @@ def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None):
     return {"out": out, "M": M, "Z": Z, "P": P, "idx": idx}
 
 
-def sparse_attention(q, K, V, idx, scale=None, groups=None):
+def attend_with_sink(q: np.ndarray, Krows: np.ndarray, Vrows: np.ndarray, scale: float, sink: float):
+    """Softmax attention whose normaliser also holds a per-head sink logit.
+
+    Sec. "Experimental Setup": the sparse layers carry learnable per-head sink
+    biases (the cited gpt-oss design): one extra logit `sink`, in the units of
+    the scaled logits s_t = scale * <q, k_t>, joins the softmax normaliser and
+    contributes no value row:
+        out = sum_t exp(s_t - M) v_t / (exp(sink - M) + sum_t exp(s_t - M)),
+    M = max(sink, max_t s_t).  With no rows the output is 0.
+    """
+    n = Krows.shape[0]
+    if n == 0:
+        return np.zeros(Vrows.shape[1])
+    s = scale * (Krows @ q)
+    M = max(float(s.max()), float(sink))
+    e = np.exp(s - M)
+    return (e @ Vrows) / (np.exp(sink - M) + e.sum())
+
+
+def sigmoid(x):
+    """Logistic function 1 / (1 + exp(-x)), evaluated without overflow."""
+    x = np.asarray(x, dtype=np.float64)
+    ex = np.exp(-np.abs(x))
+    return np.where(x >= 0, 1.0 / (1.0 + ex), ex / (1.0 + ex))
+
+
+def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None):
     """Sparse-attention layer reusing the full-attention layer's cache and indices.
 
     Sec. "Cross-Layer KV Reuse": the sparse layer reads the KV entries of the
     selected tokens from the full-attention layer's cache, and every query head
     of KV head g uses the selection of (b, g, c).  Slots holding -1 are unused.
     The selected tokens are visited in the order the index row lists them.
+
+    Optional parts of the paper's sparse layers (Sec. "Experimental Setup"):
+    sink: float [Hq], per-head sink logits (see attend_with_sink);
+    gate: uint16 bf16 bits [B, C, Hq, D], output gate logits: the layer
+    output is multiplied elementwise by sigmoid(gate) (the cited
+    gated-attention design; the gate logits come from a trained projection
+    of the layer input, so they are an input here).
 
     q: uint16 [B, C, Hq, D]; idx: int32 [B, Hkv, C, S].  Returns float64 out.
     """
@@ -251,7 +284,13 @@ def sparse_attention(q, K, V, idx, scale=None, groups=None):
             Ks = bf16_to_f64(K[b, g, sel])
             Vs = bf16_to_f64(V[b, g, sel])
             for h in range(G):
-                out[b, c, g * G + h] = attend(qg[c, h], Ks, Vs, scale)[0]
+                hq = g * G + h
+                if sink is None:
+                    out[b, c, hq] = attend(qg[c, h], Ks, Vs, scale)[0]
+                else:
+                    out[b, c, hq] = attend_with_sink(qg[c, h], Ks, Vs, scale, float(sink[hq]))
+                if gate is not None:
+                    out[b, c, hq] *= sigmoid(bf16_to_f64(gate[b, c, hq]))
     return out
 
 

@@ -274,6 +274,69 @@ def pin_sparse(O):
         assert np.array_equal(so[0, :, h], np.repeat(_f64(V[0, h // G, 7])[None], C, axis=0))
 
 
+def pin_sparse_sink_gate(O):
+    """Sinks and output gates of the sparse layers against torch and closed forms."""
+    rng = np.random.default_rng(12)
+    B, C, Hq, Hkv, D, L = 1, 2, 4, 2, 16, 23
+    G = Hq // Hkv
+    q = _bits(rng, (B, C, Hq, D))
+    K = _bits(rng, (B, Hkv, L, D))
+    V = _bits(rng, (B, Hkv, L, D))
+    lens = np.array([L])
+    scale = 1 / math.sqrt(D)
+    sink = np.array([-1.5, 0.25, 2.0, 0.7])  # a different logit per head
+    part = O.full_attn_score_select(q, K, V, lens, k=5, window=3)
+    sa = O.sparse_attention(q, K, V, part["idx"], sink=sink)
+    for g in range(Hkv):
+        for c in range(C):
+            sel = part["idx"][0, g, c]
+            sel = sel[sel >= 0]
+            for h in range(G):
+                hq = g * G + h
+                # library route: one extra key with zero key and value rows whose
+                # additive mask is the sink makes softmax's extra logit the sink
+                Ka = np.concatenate([_f64(K[0, g, sel]), np.zeros((1, D))])[None]
+                Va = np.concatenate([_f64(V[0, g, sel]), np.zeros((1, D))])[None]
+                mask = np.zeros((1, 1, sel.size + 1))
+                mask[0, 0, -1] = sink[hq]
+                ref = _sdpa(_f64(q[0, c, hq])[None, None], Ka, Va, scale, mask)[0, 0]
+                assert np.allclose(sa[0, c, hq], ref, rtol=1e-12, atol=1e-14), (g, c, h)
+    # closed form, one selected token t: out = v_t * sigmoid(s_t - sink)
+    one = np.full_like(part["idx"], -1)
+    one[..., 0] = 5
+    so = O.sparse_attention(q, K, V, one, sink=sink)
+    for c in range(C):
+        for hq in range(Hq):
+            s_t = scale * float(_f64(q[0, c, hq]) @ _f64(K[0, hq // G, 5]))
+            want = _f64(V[0, hq // G, 5]) / (1.0 + math.exp(sink[hq] - s_t))
+            assert np.allclose(so[0, c, hq], want, rtol=1e-13, atol=1e-15)
+    # a sink at -inf is no sink; a huge sink takes all the mass
+    assert np.allclose(O.sparse_attention(q, K, V, part["idx"], sink=np.full(Hq, -np.inf)),
+                       O.sparse_attention(q, K, V, part["idx"]), rtol=1e-14, atol=1e-16)
+    assert np.abs(O.sparse_attention(q, K, V, part["idx"], sink=np.full(Hq, 800.0))).max() < 1e-300
+    # gates: the ungated output times torch's sigmoid of the gate logits
+    gate = _bits(rng, (B, C, Hq, D), 3.0)
+    plain = O.sparse_attention(q, K, V, part["idx"], sink=sink)
+    gated = O.sparse_attention(q, K, V, part["idx"], sink=sink, gate=gate)
+    assert np.allclose(gated, plain * torch.sigmoid(torch.from_numpy(_f64(gate))).numpy(), rtol=1e-14, atol=1e-16)
+    zero = np.zeros_like(gate)  # bf16 +0: sigmoid(0) = 1/2
+    assert np.array_equal(O.sparse_attention(q, K, V, part["idx"], gate=zero), O.sparse_attention(q, K, V, part["idx"]) / 2)
+    # a budget covering every token: sparse attention with a sink equals full
+    # attention over the whole causal range with the same sink
+    full = O.full_attn_score_select(q, K, V, lens, k=L, window=4)
+    sf = O.sparse_attention(q, K, V, full["idx"], sink=sink)
+    for c in range(C):
+        pos = L - C + c
+        for hq in range(Hq):
+            g = hq // G
+            Ka = np.concatenate([_f64(K[0, g, :pos + 1]), np.zeros((1, D))])[None]
+            Va = np.concatenate([_f64(V[0, g, :pos + 1]), np.zeros((1, D))])[None]
+            mask = np.zeros((1, 1, pos + 2))
+            mask[0, 0, -1] = sink[hq]
+            ref = _sdpa(_f64(q[0, c, hq])[None, None], Ka, Va, scale, mask)[0, 0]
+            assert np.allclose(sf[0, c, hq], ref, rtol=1e-12, atol=1e-14)
+
+
 def pin_needles(O):
     """Planted keys aligned with a group's queries must all be selected."""
     w = Workload("needle_pin", 2, 700, 1, 8, 2, 32, 24, 16, 1, ctx_min=500, needles=6)
@@ -287,4 +350,4 @@ def pin_needles(O):
 
 ALL_PINS = [pin_bf16_decode, pin_attend_vs_library, pin_attend_special_cases, pin_full_group,
             pin_head_mapping, pin_select_bruteforce, pin_select_golden, pin_select_invariants,
-            pin_sparse, pin_needles]
+            pin_sparse, pin_sparse_sink_gate, pin_needles]

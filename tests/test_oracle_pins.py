@@ -45,6 +45,14 @@ MUTANTS = [
     ("sparse_ignores_selection", "sel = sel[sel >= 0].astype(np.int64)", "sel = np.arange(int(sel.max()) + 1)"),
     ("sparse_keeps_padding", "sel = sel[sel >= 0].astype(np.int64)", "sel = sel.astype(np.int64)"),
     ("decode_truncated", "return (bits.astype(np.uint32) << 16)", "return (bits.astype(np.uint32) << 15)"),
+    ("sink_in_numerator", "return (e @ Vrows) / (np.exp(sink - M) + e.sum())",
+     "return (e @ Vrows + np.exp(sink - M)) / (np.exp(sink - M) + e.sum())"),
+    ("sink_ignored", "(np.exp(sink - M) + e.sum())", "e.sum()"),
+    ("sink_scaled_again", "np.exp(sink - M)", "np.exp(scale * sink - M)"),
+    ("sink_of_kv_head", "float(sink[hq])", "float(sink[g])"),
+    ("gate_exp", "out[b, c, hq] *= sigmoid(bf16_to_f64(gate[b, c, hq]))",
+     "out[b, c, hq] *= np.exp(bf16_to_f64(gate[b, c, hq]))"),
+    ("gate_sign_flipped", "1.0 / (1.0 + ex), ex / (1.0 + ex)", "ex / (1.0 + ex), 1.0 / (1.0 + ex)"),
 ]
 
 
