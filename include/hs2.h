@@ -124,6 +124,25 @@ hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16
                            const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out,
                            void* workspace, size_t workspace_bytes, void* stream);
 
+/* The same sparse-attention layer with the two per-layer parts the paper's
+ * sparse layers carry (Sec. "Experimental Setup": learnable per-head sink
+ * biases and sigmoid output gates).  Either may be NULL, and with both NULL
+ * this is hs2_sparse_attn.
+ *
+ *   sink    [Hq] float (device) or NULL: one logit per query head, in the
+ *           units of the scaled logits scale*<q, k_t>, that joins the softmax
+ *           normaliser without a value row:
+ *             out = sum_t e^(s_t - M) v_t / (e^(sink_h - M) + sum_t e^(s_t - M))
+ *   gate    [B, C, Hq, D] bf16 (device, 8-byte aligned) or NULL: gate logits;
+ *           the output is multiplied elementwise by 1 / (1 + e^(-gate))
+ *           before rounding to bf16 (the logits come from the layer's own
+ *           trained projection, outside this library)
+ * Other arguments, ownership and errors as for hs2_sparse_attn.               */
+hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                              const int32_t* len, const int32_t* idx, int32_t n_slots, const float* sink,
+                              const uint16_t* gate, uint16_t* out, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
 /* Selection alone, from caller-given pooled scores (test and diagnostics).
  * Runs exactly the selection kernels of hs2_full_attn_score_select on
  * scores [B, Hkv, C, max_len] float (device; entries [0, N) of each row are

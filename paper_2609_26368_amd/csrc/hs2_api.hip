@@ -499,14 +499,23 @@ hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, con
 hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
                            const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out, void* workspace,
                            size_t workspace_bytes, void* stream) {
+  return hs2_sparse_attn_ex(dims, q, K, V, len, idx, n_slots, nullptr, nullptr, out, workspace, workspace_bytes,
+                            stream);
+}
+
+hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                              const int32_t* len, const int32_t* idx, int32_t n_slots, const float* sink,
+                              const uint16_t* gate, uint16_t* out, void* workspace, size_t workspace_bytes,
+                              void* stream) {
   hs2_status st = check_dims(dims);
   if (st != HS2_OK) return st;
   if (n_slots < 1 || n_slots > kMaxLen) return fail(HS2_ERR_SHAPE, "n_slots must be in [1, 2^27]");
   if (!q || !K || !V || !len || !idx || !out || !workspace)
     return fail(HS2_ERR_NULL, "q, K, V, len, idx, out and workspace are required");
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
-      !aligned(len, 4) || !aligned(workspace, kAlign))
-    return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len 4-byte alignment");
+      !aligned(len, 4) || !aligned(workspace, kAlign) || (sink && !aligned(sink, 4)) || (gate && !aligned(gate, 8)))
+    return fail(HS2_ERR_ALIGN,
+                "q/K/V/out need 16-byte, workspace 256-byte, gate 8-byte, idx/len/sink 4-byte alignment");
   const DeviceInfo* di = try_device_info();
   Plan p;
   make_plan(dims, 0, n_slots, p, di);
@@ -560,6 +569,8 @@ hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16
   ca.tg = sp.TG;
   ca.split_tokens = 0;
   ca.sa_mode = 1;
+  ca.sink = sink;
+  ca.gate = gate;
   HS2_TRY_LAUNCH(KK_SA_COMBINE, s, launch_combine(ca, p.G, p.rows, s));
   return HS2_OK;
 }

@@ -394,6 +394,10 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   __syncthreads();
   M = fmaxf(fmaxf(s_wmax[0], s_wmax[1]), fmaxf(s_wmax[2], s_wmax[3]));
   Mt = fmaxf(fmaxf(s_wmax[4], s_wmax[5]), fmaxf(s_wmax[6], s_wmax[7]));
+  const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
+  // sink logit of this head in log2 units: joins the normaliser, no value row
+  const float sink2 = a.sink ? a.sink[g * a.G + h] * 1.4426950408889634f : -INFINITY;
+  M = fmaxf(M, sink2);
   float z = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (M != -INFINITY) {
@@ -424,11 +428,27 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
     o.z += s_o[j][dq].z;
     o.w += s_o[j][dq].w;
   }
+  if (sink2 != -INFINITY) Z += fast_exp2(sink2 - M);
   const float inv = Z > 0.f ? 1.f / Z : 0.f;
-  const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
+  o.x *= inv;
+  o.y *= inv;
+  o.z *= inv;
+  o.w *= inv;
+  if (a.gate) {  // out *= sigmoid(gate), elementwise
+    const uint2 gb = *(const uint2*)(a.gate + orow * HD + 4 * dq);
+    const float gv[4] = {bf16_bits_to_f32(gb.x & 0xFFFFu), bf16_bits_to_f32(gb.x >> 16), bf16_bits_to_f32(gb.y & 0xFFFFu),
+                         bf16_bits_to_f32(gb.y >> 16)};
+    float gsig[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gsig[j] = 1.f / (1.f + fast_exp2(-gv[j] * 1.4426950408889634f));
+    o.x *= gsig[0];
+    o.y *= gsig[1];
+    o.z *= gsig[2];
+    o.w *= gsig[3];
+  }
   uint2 packed;
-  packed.x = f32_to_bf16_bits(o.x * inv) | (f32_to_bf16_bits(o.y * inv) << 16);
-  packed.y = f32_to_bf16_bits(o.z * inv) | (f32_to_bf16_bits(o.w * inv) << 16);
+  packed.x = f32_to_bf16_bits(o.x) | (f32_to_bf16_bits(o.y) << 16);
+  packed.y = f32_to_bf16_bits(o.z) | (f32_to_bf16_bits(o.w) << 16);
   *(uint2*)(a.out + orow * HD + 4 * dq) = packed;
   if (dq == 0) {
     if (a.stats_log2) {

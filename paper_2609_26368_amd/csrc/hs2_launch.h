@@ -36,6 +36,8 @@ struct CombineArgs {
   int sa_mode;
   uint4* clear;         // 16-byte words zeroed by the kernel as a side job, or null
   int64_t n_clear;
+  const float* sink;    // [Hq] sink logits (natural units of the scaled logits) or null
+  const uint16_t* gate; // [B, C, Hq, D] bf16 output gate logits or null
 };
 
 struct PoolArgs {

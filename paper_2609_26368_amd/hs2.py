@@ -26,7 +26,8 @@ HS2_ERR_WORKSPACE = -4
 HS2_ERR_ALIGN = -5
 HS2_ERR_HIP = -6
 
-EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_select_from_scores",
+EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_sparse_attn_ex",
+            "hs2_select_from_scores",
             "hs2_status_string", "hs2_last_error", "hs2_timing_enable", "hs2_timing_reset", "hs2_timing_read"]
 
 
@@ -62,6 +63,8 @@ def load() -> ctypes.CDLL:
     lib.hs2_full_attn_score_select.restype = I32
     lib.hs2_sparse_attn.argtypes = [D, P, P, P, P, P, I32, P, P, SZ, P]
     lib.hs2_sparse_attn.restype = I32
+    lib.hs2_sparse_attn_ex.argtypes = [D, P, P, P, P, P, I32, P, P, P, P, SZ, P]
+    lib.hs2_sparse_attn_ex.restype = I32
     lib.hs2_select_from_scores.argtypes = [D, P, P, I32, I32, P, P, SZ, P]
     lib.hs2_select_from_scores.restype = I32
     lib.hs2_status_string.argtypes = [I32]
@@ -170,6 +173,25 @@ def hs2_sparse_attn(dims, q, K, V, len, idx, n_slots, out, workspace, stream=Non
                                   _stream(stream)))
 
 
+def hs2_sparse_attn_ex(dims, q, K, V, len, idx, n_slots, sink, gate, out, workspace, stream=None):
+    """Sparse-attention layer with per-head sink logits [Hq] float32 and/or
+    output gate logits [B, C, Hq, D] bf16 (either may be None)."""
+    dev = q.device
+    B, C, Hq, Hkv, D = dims.batch, dims.n_queries, dims.n_q_heads, dims.n_kv_heads, dims.head_dim
+    _expect(q, "q", (B, C, Hq, D), _BF16, dev)
+    _check_kv(dims, K, V, dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(idx, "idx", (B, Hkv, C, n_slots), (torch.int32,), dev)
+    _expect(out, "out", (B, C, Hq, D), _BF16, dev)
+    if sink is not None:
+        _expect(sink, "sink", (Hq,), (torch.float32,), dev)
+    if gate is not None:
+        _expect(gate, "gate", (B, C, Hq, D), _BF16, dev)
+    _check(load().hs2_sparse_attn_ex(ctypes.byref(dims), _ptr(q), _ptr(K), _ptr(V), _ptr(len), _ptr(idx),
+                                     int(n_slots), _ptr(sink), _ptr(gate), _ptr(out), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
 def hs2_select_from_scores(dims, scores, len, k, window, idx, workspace, stream=None):
     """Selection alone from given pooled scores [B, Hkv, C, max_len] float32."""
     dev = scores.device
@@ -243,9 +265,13 @@ class HybridBlock:
                                    stream)
         return out, idx
 
-    def sparse(self, q, K, V, lens, idx, out=None, stream=None):
+    def sparse(self, q, K, V, lens, idx, out=None, stream=None, sink=None, gate=None):
+        """One sparse layer; sink [Hq] float32 and gate [B, C, Hq, D] bf16 are optional."""
         d = self.dims
         if out is None:
             out = torch.empty((d.batch, d.n_queries, d.n_q_heads, d.head_dim), dtype=torch.bfloat16, device=q.device)
-        hs2_sparse_attn(d, q, K, V, lens, idx, idx.shape[-1], out, self.workspace, stream)
+        if sink is None and gate is None:
+            hs2_sparse_attn(d, q, K, V, lens, idx, idx.shape[-1], out, self.workspace, stream)
+        else:
+            hs2_sparse_attn_ex(d, q, K, V, lens, idx, idx.shape[-1], sink, gate, out, self.workspace, stream)
         return out

@@ -112,6 +112,22 @@ def test_sparse_and_select_reject_before_launch(lib):
     assert st == hs2.HS2_ERR_ALIGN
 
 
+def test_sparse_ex_rejects_before_launch(lib):
+    d = dims()
+    vp = ctypes.c_void_p
+
+    def call(sink=None, gate=None, n_slots=24, ws_bytes=1 << 40):
+        return lib.hs2_sparse_attn_ex(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), n_slots,
+                                      None if sink is None else vp(sink), None if gate is None else vp(gate),
+                                      vp(FAKE), vp(FAKE), ws_bytes, None)
+
+    assert call(n_slots=0) == hs2.HS2_ERR_SHAPE
+    assert call(sink=FAKE + 2) == hs2.HS2_ERR_ALIGN
+    assert call(gate=FAKE + 4) == hs2.HS2_ERR_ALIGN
+    assert "gate" in hs2.hs2_last_error()
+    assert call(sink=FAKE, gate=FAKE, ws_bytes=256) == hs2.HS2_ERR_WORKSPACE
+
+
 def test_status_strings(lib):
     for code in (hs2.HS2_OK, hs2.HS2_ERR_NULL, hs2.HS2_ERR_SHAPE, hs2.HS2_ERR_UNSUPPORTED, hs2.HS2_ERR_WORKSPACE,
                  hs2.HS2_ERR_ALIGN, hs2.HS2_ERR_HIP):

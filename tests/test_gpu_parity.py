@@ -189,6 +189,34 @@ def test_parity_scores_from_k(w, monkeypatch):
     parity_case(w, seed=7)
 
 
+SINK_GATE = [SMALL[1], SMALL[3], SMALL[4]]
+
+
+@pytest.mark.parametrize("w", SINK_GATE, ids=[w.name for w in SINK_GATE])
+def test_sparse_sink_and_gate(w):
+    """Sparse layers with per-head sink logits and sigmoid output gates, on the oracle's selection."""
+    hs2 = _hs2()
+    inp = W.make_inputs(w, seed=11)
+    B, C, Hq, D = w.batch, w.n_queries, w.n_q_heads, w.head_dim
+    note(f"[sink-gate] {w.name} lens={inp.lens.tolist()}")
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window)
+    rng = np.random.default_rng(5)
+    sink = (rng.standard_normal(Hq) * 3.0).astype(np.float32)  # some heads' sinks dominate their logits
+    gate = W.f32_to_bf16_bits((rng.standard_normal((B, C, Hq, D)) * 2.0).astype(np.float32))
+    blk = hs2.HybridBlock(B, C, Hq, w.n_kv_heads, D, inp.K.shape[2], w.k, w.window)
+    K, V = dev_bf16(inp.K), dev_bf16(inp.V)
+    lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
+    ridx = torch.from_numpy(ref["idx"]).cuda()
+    q = dev_bf16(inp.q_sa[0])
+    for s_, g_ in [(sink, None), (None, gate), (sink, gate)]:
+        got = blk.sparse(q, K, V, lens, ridx, sink=None if s_ is None else torch.from_numpy(s_).cuda(),
+                         gate=None if g_ is None else dev_bf16(g_))
+        torch.cuda.synchronize()
+        want = O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"], sink=s_, gate=g_)
+        CK.check_out(CK.bf16_bits_to_f64(host_bits(got)), want,
+                     f"sparse layer, sink={s_ is not None}, gate={g_ is not None}")
+
+
 # ---------------------------------------------------------------- selection alone: bit-exact
 def _select_case(B, Hkv, C, Lmax, lens, k, win, scores):
     hs2 = _hs2()
