@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sa-sink-gate", action="store_true",
+                    help="sparse layers with per-head sink logits and sigmoid output gates (hs2_sparse_attn_ex)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -157,11 +159,16 @@ def main():
     idx = torch.empty((B, Hkv, C, w.slots), dtype=torch.int32, device=dev)
     sa_out = [torch.empty_like(out) for _ in q_sa]
     stream = torch.cuda.current_stream()
+    sinks, gates = [None] * len(q_sa), [None] * len(q_sa)
+    if args.sa_sink_gate:  # synthetic per-layer sink logits and gate logits
+        g = torch.Generator(device="cpu").manual_seed(2609)
+        sinks = [torch.randn(Hq, generator=g).to(dev) for _ in q_sa]
+        gates = [torch.randn((B, C, Hq, D), generator=g).to(torch.bfloat16).to(dev) for _ in q_sa]
 
     def step():
         blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream)
-        for qs, o in zip(q_sa, sa_out):
-            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream)
+        for qs, o, sk, gt in zip(q_sa, sa_out, sinks, gates):
+            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream, sink=sk, gate=gt)
 
     for _ in range(args.warmup):
         step()
@@ -222,7 +229,8 @@ def main():
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": w.name, "batch": B, "ctx": w.ctx, "ctx_min": w.ctx_min or w.ctx,
                       "queries_per_seq": C, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D, "k": w.k,
-                      "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles},
+                      "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles,
+                      **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
            "roofline": roofline,
