@@ -50,6 +50,27 @@ FLT_MIN = np.float32(np.finfo(np.float32).tiny)
 # --------------------------------------------------------------------------
 # input decoding
 # --------------------------------------------------------------------------
+def e4m3_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Decode OCP FP8 E4M3 bits: sign, 4 exponent bits (bias 7), 3 mantissa
+    bits; exponent 0 holds the subnormals m/8 * 2^-6; exponent 15 with
+    mantissa 7 is NaN (the format has no infinities)."""
+    b = np.asarray(bits, dtype=np.uint8).astype(np.int64)
+    sign = np.where(b >> 7, -1.0, 1.0)
+    e = (b >> 3) & 15
+    m = (b & 7).astype(np.float64)
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e - 7.0))
+    return np.where((e == 15) & (m == 7), np.nan, sign * mag)
+
+
+def cache_rows(X: np.ndarray, b: int, g: int, rows, scale) -> np.ndarray:
+    """Rows of one (sequence, KV head) of a cache as float64: bf16 bits, or
+    E4M3 bits times that KV head's scale (the paper quotes its costs with an
+    FP8 KV cache, Sec. "Prefill computation and KV-cache storage")."""
+    if X.dtype == np.uint8:
+        return e4m3_to_f64(X[b, g, rows]) * float(scale[g])
+    return bf16_to_f64(X[b, g, rows])
+
+
 def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     """Exact value of bf16 bit patterns (uint16) as float64.
 
@@ -189,10 +210,11 @@ def _group_q(q: np.ndarray, b: int, g: int, G: int) -> np.ndarray:
     return bf16_to_f64(q[b, :, g * G:(g + 1) * G, :])
 
 
-def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None):
+def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None, k_scale=None, v_scale=None):
     """Full-attention layer, pooled scores and selection for a whole batch.
 
-    q: uint16 [B, C, Hq, D]; K, V: uint16 [B, Hkv, Lmax, D]; lens: int [B].
+    q: uint16 [B, C, Hq, D]; K, V: uint16 bf16 bits [B, Hkv, Lmax, D], or
+    uint8 E4M3 bits with float [Hkv] scales k_scale / v_scale; lens: int [B].
     ``groups`` optionally restricts the work to a list of (b, g) pairs; other
     entries of the results are left at zero / -1.
 
@@ -214,8 +236,8 @@ def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None):
     todo = groups if groups is not None else [(b, g) for b in range(B) for g in range(Hkv)]
     for b, g in todo:
         L = int(lens[b])
-        Kg = bf16_to_f64(K[b, g, :L])
-        Vg = bf16_to_f64(V[b, g, :L])
+        Kg = cache_rows(K, b, g, slice(0, L), k_scale)
+        Vg = cache_rows(V, b, g, slice(0, L), v_scale)
         o, m, z, p = full_attention_group(_group_q(q, b, g, G), Kg, Vg, L, scale)
         out[b, :, g * G:(g + 1) * G] = o
         M[b, :, g * G:(g + 1) * G] = m
@@ -253,7 +275,7 @@ def sigmoid(x):
     return np.where(x >= 0, 1.0 / (1.0 + ex), ex / (1.0 + ex))
 
 
-def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None):
+def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None, k_scale=None, v_scale=None):
     """Sparse-attention layer reusing the full-attention layer's cache and indices.
 
     Sec. "Cross-Layer KV Reuse": the sparse layer reads the KV entries of the
@@ -268,7 +290,8 @@ def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None
     gated-attention design; the gate logits come from a trained projection
     of the layer input, so they are an input here).
 
-    q: uint16 [B, C, Hq, D]; idx: int32 [B, Hkv, C, S].  Returns float64 out.
+    q: uint16 [B, C, Hq, D]; idx: int32 [B, Hkv, C, S]; K, V and their scales
+    as for full_attn_score_select.  Returns float64 out.
     """
     B, C, Hq, D = q.shape
     Hkv = K.shape[1]
@@ -281,8 +304,8 @@ def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None
         for c in range(C):
             sel = idx[b, g, c]
             sel = sel[sel >= 0].astype(np.int64)
-            Ks = bf16_to_f64(K[b, g, sel])
-            Vs = bf16_to_f64(V[b, g, sel])
+            Ks = cache_rows(K, b, g, sel, k_scale)
+            Vs = cache_rows(V, b, g, sel, v_scale)
             for h in range(G):
                 hq = g * G + h
                 if sink is None:
@@ -294,7 +317,7 @@ def sparse_attention(q, K, V, idx, scale=None, groups=None, sink=None, gate=None
     return out
 
 
-def hybrid_block(q_fa, q_sa, K, V, lens, k, window, scale=None, groups=None):
+def hybrid_block(q_fa, q_sa, K, V, lens, k, window, scale=None, groups=None, k_scale=None, v_scale=None):
     """One hybrid block: a full-attention layer then len(q_sa) sparse layers.
 
     Sec. "HySparse2 Overview" / "Cross-Layer KV Reuse": the sparse layers that
@@ -302,6 +325,7 @@ def hybrid_block(q_fa, q_sa, K, V, lens, k, window, scale=None, groups=None):
     Returns the full-attention result dict with an extra key "sa_out", the
     list of sparse-layer outputs.
     """
-    res = full_attn_score_select(q_fa, K, V, lens, k, window, scale, groups)
-    res["sa_out"] = [sparse_attention(qs, K, V, res["idx"], scale, groups) for qs in q_sa]
+    res = full_attn_score_select(q_fa, K, V, lens, k, window, scale, groups, k_scale, v_scale)
+    res["sa_out"] = [sparse_attention(qs, K, V, res["idx"], scale, groups, k_scale=k_scale, v_scale=v_scale)
+                     for qs in q_sa]
     return res

@@ -88,6 +88,33 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return ((u + rnd) >> 16).astype(np.uint16)
 
 
+E4M3_MAX = 448.0  # largest finite OCP FP8 E4M3 value
+
+
+def f32_to_e4m3_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to OCP FP8 E4M3 (nearest, ties to even), saturating
+    at +-448; returns uint8 bits.  (torch's cast does the rounding.)"""
+    import torch
+    t = torch.from_numpy(np.clip(np.ascontiguousarray(x, dtype=np.float32), -E4M3_MAX, E4M3_MAX))
+    return t.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def quantize_kv_e4m3(X: np.ndarray):
+    """bf16 cache bits [B, Hkv, L, D] -> (uint8 E4M3 bits, float32 scale [Hkv]):
+    one scale per KV head, max |x| / 448, so the head's largest value maps to
+    the largest finite E4M3 value (x ~ bits * scale)."""
+    B, Hkv = X.shape[:2]
+    out = np.empty(X.shape, dtype=np.uint8)
+    scale = np.ones(Hkv, dtype=np.float32)
+    for g in range(Hkv):
+        f = (X[:, g].astype(np.uint32) << 16).view(np.float32)
+        m = float(np.abs(f).max())
+        if m > 0:
+            scale[g] = np.float32(m / E4M3_MAX)
+        out[:, g] = f32_to_e4m3_bits(f / scale[g])
+    return out, scale
+
+
 def _rng(seed: int, *ids: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence([seed, *ids]))
 
@@ -156,14 +183,18 @@ class Inputs:
     w: Workload
     q_fa: np.ndarray            # uint16 [B, C, Hq, D]
     q_sa: list                  # n_sparse x uint16 [B, C, Hq, D]
-    K: np.ndarray               # uint16 [B, Hkv, Lmax, D]
+    K: np.ndarray               # uint16 bf16 bits [B, Hkv, Lmax, D], or uint8 E4M3 bits
     V: np.ndarray
     lens: np.ndarray            # int32 [B]
     needles: dict               # b -> positions
+    k_scale: np.ndarray | None = None  # float32 [Hkv] for an E4M3 cache (value = bits * scale)
+    v_scale: np.ndarray | None = None
 
 
-def make_inputs(w: Workload, seed: int = BASE_SEED, lmax: int | None = None) -> Inputs:
-    """Materialise every tensor of one decode step on the host."""
+def make_inputs(w: Workload, seed: int = BASE_SEED, lmax: int | None = None, kv: str = "bf16") -> Inputs:
+    """Materialise every tensor of one decode step on the host.  kv="fp8"
+    stores the cache as OCP E4M3 with one scale per KV head for K and for V
+    (quantised from the same bf16 values)."""
     lens = draw_lengths(w, seed)
     Lmax = int(lmax if lmax is not None else w.ctx)
     if lens.max() > Lmax:
@@ -192,4 +223,10 @@ def make_inputs(w: Workload, seed: int = BASE_SEED, lmax: int | None = None) -> 
             needles[b] = pos
             for g in range(w.n_kv_heads):
                 K[b, g, pos] = needle_key(w, q_fa, b, g)
+    if kv == "fp8":
+        K8, ks = quantize_kv_e4m3(K)
+        V8, vs = quantize_kv_e4m3(V)
+        return Inputs(w, q_fa, q_sa, K8, V8, lens, needles, ks, vs)
+    if kv != "bf16":
+        raise ValueError(f"unknown cache format {kv}")
     return Inputs(w, q_fa, q_sa, K, V, lens, needles)

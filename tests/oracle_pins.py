@@ -337,6 +337,52 @@ def pin_sparse_sink_gate(O):
             assert np.allclose(sf[0, c, hq], ref, rtol=1e-12, atol=1e-14)
 
 
+def pin_fp8_cache(O):
+    """E4M3 cache: decoding against torch, and the whole layer against the bf16 path and torch."""
+    allb = np.arange(256, dtype=np.uint8)
+    d = O.e4m3_to_f64(allb)
+    ref = torch.from_numpy(allb).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(np.isnan(d), np.isnan(ref)) and np.array_equal(d[~np.isnan(d)], ref[~np.isnan(ref)])
+    spot = {0x38: 1.0, 0x7E: 448.0, 0x01: 2.0 ** -9, 0x08: 2.0 ** -6, 0xB8: -1.0, 0x3C: 1.5, 0x47: 3.75}
+    for bt, v in spot.items():
+        assert O.e4m3_to_f64(np.array([bt], dtype=np.uint8))[0] == v, hex(bt)
+    assert np.isnan(O.e4m3_to_f64(np.array([0x7F, 0xFF], dtype=np.uint8))).all()
+    rng = np.random.default_rng(14)
+    B, C, Hq, Hkv, D, L = 1, 2, 4, 2, 16, 37
+    G = Hq // Hkv
+    q = _bits(rng, (B, C, Hq, D))
+    finite = np.array([b for b in range(256) if b not in (0x7F, 0xFF)], dtype=np.uint8)
+    K8 = rng.choice(finite, size=(B, Hkv, L, D))
+    V8 = rng.choice(finite, size=(B, Hkv, L, D))
+    lens = np.array([L])
+    # power-of-two scales: every cache value is a bf16 value too, so the E4M3
+    # cache and the bf16 cache holding the same numbers give identical results
+    ks, vs = np.array([2.0 ** -6, 2.0 ** -5]), np.array([2.0 ** -4, 2.0 ** -7])
+    Kf = O.e4m3_to_f64(K8) * ks[None, :, None, None]
+    Vf = O.e4m3_to_f64(V8) * vs[None, :, None, None]
+    Kb = f32_to_bf16_bits(Kf.astype(np.float32))
+    Vb = f32_to_bf16_bits(Vf.astype(np.float32))
+    assert np.array_equal(_f64(Kb), Kf) and np.array_equal(_f64(Vb), Vf)
+    r8 = O.hybrid_block(q, [q], K8, V8, lens, 6, 4, k_scale=ks, v_scale=vs)
+    rb = O.hybrid_block(q, [q], Kb, Vb, lens, 6, 4)
+    for key in ("out", "M", "Z", "P", "idx"):
+        assert np.array_equal(r8[key], rb[key]), key
+    assert np.array_equal(r8["sa_out"][0], rb["sa_out"][0])
+    # arbitrary per-head scales, different for K and V: torch attention on the
+    # dequantised cache
+    ks, vs = np.array([0.0123, 0.031]), np.array([0.27, 0.0052])
+    res = O.full_attn_score_select(q, K8, V8, lens, 6, 4, k_scale=ks, v_scale=vs)
+    scale = 1 / math.sqrt(D)
+    for c in range(C):
+        pos = L - C + c
+        for hq in range(Hq):
+            g = hq // G
+            Kd = (O.e4m3_to_f64(K8[0, g, :pos + 1]) * ks[g])[None]
+            Vd = (O.e4m3_to_f64(V8[0, g, :pos + 1]) * vs[g])[None]
+            want = _sdpa(_f64(q[0, c, hq])[None, None], Kd, Vd, scale)[0, 0]
+            assert np.allclose(res["out"][0, c, hq], want, rtol=1e-12, atol=1e-15), (c, hq)
+
+
 def pin_needles(O):
     """Planted keys aligned with a group's queries must all be selected."""
     w = Workload("needle_pin", 2, 700, 1, 8, 2, 32, 24, 16, 1, ctx_min=500, needles=6)
@@ -350,4 +396,4 @@ def pin_needles(O):
 
 ALL_PINS = [pin_bf16_decode, pin_attend_vs_library, pin_attend_special_cases, pin_full_group,
             pin_head_mapping, pin_select_bruteforce, pin_select_golden, pin_select_invariants,
-            pin_sparse, pin_sparse_sink_gate, pin_needles]
+            pin_sparse, pin_sparse_sink_gate, pin_fp8_cache, pin_needles]

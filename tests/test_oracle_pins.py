@@ -53,6 +53,10 @@ MUTANTS = [
     ("gate_exp", "out[b, c, hq] *= sigmoid(bf16_to_f64(gate[b, c, hq]))",
      "out[b, c, hq] *= np.exp(bf16_to_f64(gate[b, c, hq]))"),
     ("gate_sign_flipped", "1.0 / (1.0 + ex), ex / (1.0 + ex)", "ex / (1.0 + ex), 1.0 / (1.0 + ex)"),
+    ("e4m3_bias_8", "np.exp2(e - 7.0)", "np.exp2(e - 8.0)"),
+    ("e4m3_no_subnormals", "np.where(e == 0, m / 8.0 * 2.0 ** -6,", "np.where(e < 0, m / 8.0 * 2.0 ** -6,"),
+    ("v_with_k_scale", "Vg = cache_rows(V, b, g, slice(0, L), v_scale)", "Vg = cache_rows(V, b, g, slice(0, L), k_scale)"),
+    ("scale_of_head_0", "* float(scale[g])", "* float(scale[0])"),
 ]
 
 
