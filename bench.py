@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sa-sink-gate", action="store_true",
                     help="sparse layers with per-head sink logits and sigmoid output gates (hs2_sparse_attn_ex)")
+    ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
+                    help="cache format: bf16, or OCP E4M3 bytes with one scale per KV head (the _fp8 entry points)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -125,7 +127,7 @@ def main():
         copy_calibration()
         return
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, args.workload)
+        summarize_pmc(*args.summarize_pmc, args.workload + ("_fp8" if args.kv == "fp8" else ""))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
@@ -140,8 +142,8 @@ def main():
         __graft_entry__.build()
     w = W.WORKLOADS[args.workload]
     t = time.perf_counter()
-    inp = W.make_inputs(w)
-    log(f"[bench] inputs {w.name} generated in {time.perf_counter() - t:.1f}s lens={inp.lens.tolist()}")
+    inp = W.make_inputs(w, kv=args.kv)
+    log(f"[bench] inputs {w.name} ({args.kv} cache) generated in {time.perf_counter() - t:.1f}s lens={inp.lens.tolist()}")
     B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
     Lmax = inp.K.shape[2]
     dev = torch.device("cuda:0")
@@ -150,7 +152,12 @@ def main():
     def to_dev(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
 
-    K, V = to_dev(inp.K), to_dev(inp.V)
+    if args.kv == "fp8":
+        K, V = torch.from_numpy(inp.K).to(dev), torch.from_numpy(inp.V).to(dev)
+        kv_scales = (torch.from_numpy(inp.k_scale).to(dev), torch.from_numpy(inp.v_scale).to(dev))
+    else:
+        K, V = to_dev(inp.K), to_dev(inp.V)
+        kv_scales = None
     q_fa = to_dev(inp.q_fa)
     q_sa = [to_dev(x) for x in inp.q_sa]
     lens = torch.from_numpy(inp.lens).to(dev)
@@ -166,9 +173,9 @@ def main():
         gates = [torch.randn((B, C, Hq, D), generator=g).to(torch.bfloat16).to(dev) for _ in q_sa]
 
     def step():
-        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream)
+        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream, kv_scales=kv_scales)
         for qs, o, sk, gt in zip(q_sa, sa_out, sinks, gates):
-            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream, sink=sk, gate=gt)
+            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream, sink=sk, gate=gt, kv_scales=kv_scales)
 
     for _ in range(args.warmup):
         step()
@@ -201,7 +208,7 @@ def main():
 
     # algorithmic bytes (what the method must move; scratch and partials excluded)
     L = inp.lens.astype(np.int64)
-    kv_row = 2 * D * 2
+    kv_row = 2 * D * (1 if args.kv == "fp8" else 2)  # K and V row of one token and KV head
     q_bytes = B * C * Hq * D * 2
     fa_bytes = int(L.sum()) * Hkv * kv_row + q_bytes
     idx_h = idx.cpu().numpy()
@@ -210,7 +217,7 @@ def main():
     fa_avg_s = kernels["fa_split"]["avg_us"] * 1e-6
     achieved = fa_bytes / fa_avg_s / 1e9
     traffic = None  # HBM bytes per launch from calibrated counters, if taken on these kernels
-    tf = TRAFFIC_FILE.format(workload=w.name)
+    tf = TRAFFIC_FILE.format(workload=w.name + ("_fp8" if args.kv == "fp8" else ""))
     if os.path.exists(tf):
         with open(tf) as f:
             trec = json.load(f)
@@ -230,6 +237,7 @@ def main():
            "config": {"workload": w.name, "batch": B, "ctx": w.ctx, "ctx_min": w.ctx_min or w.ctx,
                       "queries_per_seq": C, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D, "k": w.k,
                       "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles,
+                      "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
                       **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
@@ -251,7 +259,8 @@ def cpu_baseline(w, inp, budget_s: float) -> dict:
     groups_all = [(b, g) for b in range(w.batch) for g in range(w.n_kv_heads)]
     done, t0 = [], time.perf_counter()
     for bg in groups_all:
-        O.hybrid_block(inp.q_fa, inp.q_sa, inp.K, inp.V, inp.lens, w.k, w.window, groups=[bg])
+        O.hybrid_block(inp.q_fa, inp.q_sa, inp.K, inp.V, inp.lens, w.k, w.window, groups=[bg],
+                       k_scale=inp.k_scale, v_scale=inp.v_scale)
         done.append(bg)
         if time.perf_counter() - t0 >= budget_s:
             break

@@ -66,7 +66,8 @@ typedef enum hs2_status {
 /* Shapes shared by every call of one hybrid block.
  *   q, out:  [batch, n_queries, n_q_heads, head_dim] contiguous bf16
  *   K, V:    element (b, g, t, d) at b*kv_stride_b + g*kv_stride_h + t*kv_stride_t + d
- *            (bf16; K and V share this layout; each token row is contiguous)    */
+ *            (bf16, or E4M3 bytes for the _fp8 entry points; K and V share
+ *            this layout; each token row is contiguous)                         */
 typedef struct hs2_dims {
   int32_t batch;       /* B >= 1                                                  */
   int32_t n_queries;   /* C: decode tokens per sequence, 1 .. 16                  */
@@ -142,6 +143,36 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
                               const int32_t* len, const int32_t* idx, int32_t n_slots, const float* sink,
                               const uint16_t* gate, uint16_t* out, void* workspace, size_t workspace_bytes,
                               void* stream);
+
+/* FP8 KV cache.  The paper sizes every KV cache it reports in FP8 storage
+ * (Sec. "Evaluation", paragraph on prefill computation and KV-cache storage);
+ * it does not fix the format or the scaling, so these entry points take
+ * OCP E4M3 bytes (bias 7, subnormals, no infinities, 0x7F/0xFF = NaN, largest
+ * finite 448) with one fp32 scale per KV head and tensor: the cache stands for
+ *   K(b, g, t, d) = k_scale[g] * e4m3(K8[...]),  V likewise with v_scale[g].
+ * The math is that of the bf16 entry points on these dequantised values
+ * (fp32 accumulation), so a cache holding the same values gives the same
+ * selection and, up to rounding order, the same outputs.
+ *
+ *   K8, V8   uint8 [..] with the element offsets of hs2_dims (one byte each);
+ *            kv_stride_b, kv_stride_h and kv_stride_t must be multiples of 16
+ *            (HS2_ERR_ALIGN), K8 and V8 16-byte aligned
+ *   k_scale, v_scale  [Hkv] float (device, 4-byte aligned), both required
+ *            (HS2_ERR_NULL); finite and > 0 for meaningful results
+ *   n_queries * (G rounded up to a power of two) must be <= 64
+ *            (HS2_ERR_UNSUPPORTED above that)
+ * Other arguments, outputs, ownership and errors as for
+ * hs2_full_attn_score_select and hs2_sparse_attn_ex respectively; the same
+ * hs2_workspace_bytes() covers both cache formats.                            */
+hs2_status hs2_full_attn_score_select_fp8(const hs2_dims* dims, const uint16_t* q, const uint8_t* K8,
+                                          const uint8_t* V8, const float* k_scale, const float* v_scale,
+                                          const int32_t* len, int32_t k, int32_t window, uint16_t* out,
+                                          int32_t* idx, float* stats, float* scores, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const uint8_t* K8, const uint8_t* V8,
+                               const float* k_scale, const float* v_scale, const int32_t* len, const int32_t* idx,
+                               int32_t n_slots, const float* sink, const uint16_t* gate, uint16_t* out,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* Selection alone, from caller-given pooled scores (test and diagnostics).
  * Runs exactly the selection kernels of hs2_full_attn_score_select on

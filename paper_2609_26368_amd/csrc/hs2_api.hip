@@ -68,6 +68,7 @@ struct Plan {
   int64_t rows;               // selection rows B * Hkv * C
   int64_t score_stride, bitmap_words, cand_cap;
   int sel_nchunks;
+  bool kv8;                   // E4M3 cache
   bool pool_logits;           // scores from logits stored by the full-attention kernel
   int64_t logit_stride;
   // workspace layout of hs2_full_attn_score_select / hs2_select_from_scores
@@ -121,8 +122,8 @@ size_t carve(size_t& cur, size_t bytes) {
 // on one compute unit (runtime occupancy query).
 struct DeviceInfo {
   int cus = 256;
-  int fa_wgs[4][kFaVariants] = {};  // [log2 RT][variant]; 0 = unknown
-  int pool_wgs[4][7][17] = {};      // k_pool: [log2 RT][log2 Gp][C]; 0 = unknown
+  int fa_wgs[2][4][kFaVariants] = {};  // [E4M3 cache][log2 RT][variant]; 0 = unknown
+  int pool_wgs[2][4][7][17] = {};      // k_pool: [E4M3 cache][log2 RT][log2 Gp][C]; 0 = unknown
 };
 
 int ilog2(int v) {
@@ -137,7 +138,9 @@ int ilog2(int v) {
 // eight.
 int default_fa_variant(int RT) { return RT >= 8 ? 1 : RT == 1 ? 2 : 5; }
 
-void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const DeviceInfo* di) {
+// kv8: the cache is E4M3 (ring kernels only)
+void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const DeviceInfo* di, bool kv8 = false) {
+  p.kv8 = kv8;
   p.B = d->batch;
   p.C = d->n_queries;
   p.Hq = d->n_q_heads;
@@ -154,7 +157,8 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
   p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT));
-  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || !fa_variant_exists(p.RT, p.fa_variant))
+  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || !fa_variant_exists(p.RT, p.fa_variant) ||
+      (kv8 && p.fa_variant == 1))
     p.fa_variant = default_fa_variant(p.RT);
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
@@ -163,7 +167,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   // (one round, no tail), each a whole number of 64-token tiles and at least
   // 256 tokens (a split's partial costs 16 RT rows of D + 4 floats)
   const int lrt = p.RT >= 8 ? 3 : p.RT >= 4 ? 2 : p.RT >= 2 ? 1 : 0;
-  const int wgs_cu = di && di->fa_wgs[lrt][p.fa_variant] > 0 ? di->fa_wgs[lrt][p.fa_variant] : 4;
+  const int wgs_cu = di && di->fa_wgs[kv8][lrt][p.fa_variant] > 0 ? di->fa_wgs[kv8][lrt][p.fa_variant] : 4;
   const int64_t slots = (int64_t)(di ? di->cus : 256) * wgs_cu * std::max(1, env_int("HS2_FA_ROUNDS", 1));
   const int64_t per_unit = std::max<int64_t>(1, slots / p.units);
   const int align = fa_split_align(p.RT, p.fa_variant);
@@ -174,7 +178,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   p.fa_nsplit = (int)cdiv(p.Lmax, split);
   // score pass over K: the same one-round rule for its own kernel; at most
   // 32768 tokens per split (16-bit histogram counters in LDS)
-  const int pool_cu = di && p.C <= 16 ? di->pool_wgs[lrt][ilog2(p.Gp)][p.C] : 0;
+  const int pool_cu = di && p.C <= 16 ? di->pool_wgs[kv8][lrt][ilog2(p.Gp)][p.C] : 0;
   const int64_t pslots = (int64_t)(di ? di->cus : 256) * (pool_cu > 0 ? pool_cu : 4);
   int psplit = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, std::max<int64_t>(1, pslots / p.units)), 64));
   psplit = env_int("HS2_POOL_SPLIT", psplit);
@@ -271,15 +275,16 @@ hs2_status ensure_device_init(const DeviceInfo** info) {
     DeviceInfo di;
     if ((e = hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
       return fail(HS2_ERR_HIP, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
-    for (int l = 0; l < 4; ++l) {
-      for (int v = 0; v < kFaVariants; ++v)
-        if ((e = fa_wgs_per_cu(1 << l, v, &di.fa_wgs[l][v])) != hipSuccess)
-          return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
-      for (int lg = 0; lg < 7; ++lg)
-        for (int c = 1; c <= 16; ++c)
-          if ((e = pool_wgs_per_cu(1 << l, 1 << lg, c, &di.pool_wgs[l][lg][c])) != hipSuccess)
+    for (int f = 0; f < 2; ++f)
+      for (int l = 0; l < 4; ++l) {
+        for (int v = 0; v < kFaVariants; ++v)
+          if ((e = fa_wgs_per_cu(1 << l, v, f == 1, &di.fa_wgs[f][l][v])) != hipSuccess)
             return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
-    }
+        for (int lg = 0; lg < 7; ++lg)
+          for (int c = 1; c <= 16; ++c)
+            if ((e = pool_wgs_per_cu(1 << l, 1 << lg, c, f == 1, &di.pool_wgs[f][l][lg][c])) != hipSuccess)
+              return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+      }
     g_dev[dev] = di;
     g_dev_done[dev] = true;
   }
@@ -358,20 +363,44 @@ const char* hs2_last_error(void) { return g_last_error.c_str(); }
 
 size_t hs2_workspace_bytes(const hs2_dims* dims, int32_t k, int32_t window) {
   if (check_dims(dims) != HS2_OK || check_budget(k, window) != HS2_OK) return 0;
-  Plan p;
-  make_plan(dims, k, window, p, try_device_info());
-  SaPlan sp;
-  make_sa_plan(p, k + window, sp);
-  return std::max(p.fa_bytes, sp.bytes);
+  const DeviceInfo* di = try_device_info();
+  size_t bytes = 0;
+  for (int kv8 = 0; kv8 < 2; ++kv8) {  // enough for either cache format
+    Plan p;
+    make_plan(dims, k, window, p, di, kv8 == 1);
+    SaPlan sp;
+    make_sa_plan(p, k + window, sp);
+    bytes = std::max(bytes, std::max(p.fa_bytes, sp.bytes));
+  }
+  return bytes;
 }
 
-hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
-                                      const int32_t* len, int32_t k, int32_t window, uint16_t* out, int32_t* idx,
-                                      float* stats, float* scores, void* workspace, size_t workspace_bytes,
-                                      void* stream) {
+}  // extern "C"
+
+namespace {
+
+// E4M3 cache: K and V are byte arrays with one float scale per KV head each;
+// their strides must keep every 16-byte load aligned
+hs2_status check_fp8(const hs2_dims* dims, const float* k_scale, const float* v_scale) {
+  if (!k_scale || !v_scale) return fail(HS2_ERR_NULL, "k_scale and v_scale are required for an FP8 cache");
+  if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return fail(HS2_ERR_ALIGN, "scales need 4-byte alignment");
+  if (dims->kv_stride_t % 16 || dims->kv_stride_h % 16 || dims->kv_stride_b % 16)
+    return fail(HS2_ERR_ALIGN, "FP8 cache strides must be multiples of 16 elements");
+  const int rows = dims->n_queries * next_pow2(dims->n_q_heads / dims->n_kv_heads);
+  if (rows > 64)
+    return fail(HS2_ERR_UNSUPPORTED, "FP8 cache: n_queries * pow2(G) = %d exceeds 64 query rows per KV head", rows);
+  return HS2_OK;
+}
+
+hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K, const void* V, const float* k_scale,
+                          const float* v_scale, const int32_t* len, int32_t k, int32_t window, uint16_t* out,
+                          int32_t* idx, float* stats, float* scores, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  const bool kv8 = k_scale != nullptr;
   hs2_status st = check_dims(dims);
   if (st != HS2_OK) return st;
   if ((st = check_budget(k, window)) != HS2_OK) return st;
+  if (kv8 && (st = check_fp8(dims, k_scale, v_scale)) != HS2_OK) return st;
   if (!q || !K || !V || !len || !out || !idx || !workspace)
     return fail(HS2_ERR_NULL, "q, K, V, len, out, idx and workspace are required");
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
@@ -379,7 +408,7 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
     return fail(HS2_ERR_ALIGN, "q/K/V/out need 16-byte, workspace 256-byte, idx/len/scores 4-byte alignment");
   const DeviceInfo* di = try_device_info();
   Plan p;
-  make_plan(dims, k, window, p, di);
+  make_plan(dims, k, window, p, di, kv8);
   if (workspace_bytes < p.fa_bytes)
     return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
   if ((st = ensure_device_init(&di)) != HS2_OK) return st;
@@ -393,8 +422,9 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
 
   FaArgs fa{};
   fa.q = q;
-  fa.K = K;
-  fa.V = V;
+  fa.K = (const uint16_t*)K;
+  fa.V = (const uint16_t*)V;
+  fa.k_scale = k_scale;
   fa.len = len;
   fa.part_o = (float*)(ws + p.off_part_o);
   fa.part_ml = (float*)(ws + p.off_part_ml);
@@ -435,13 +465,15 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   ca.split_tokens = p.fa_split;
   ca.sa_mode = 0;
   // the histogram and the per-row counters (contiguous) start at zero
+  ca.v_scale = v_scale;
   ca.clear = (uint4*)(ws + p.off_hist);
   ca.n_clear = (int64_t)(p.off_state - p.off_hist + sizeof(int32_t) * p.rows * 8) / 16;
   HS2_TRY_LAUNCH(KK_COMBINE, s, launch_combine(ca, std::min(16 * p.RT, p.C * p.Gp), p.units, s));
 
   PoolArgs pa{};
   pa.q = q;
-  pa.K = K;
+  pa.K = (const uint16_t*)K;
+  pa.k_scale = k_scale;
   pa.len = len;
   pa.stats_log2 = stats_log2;
   pa.scores = sc;
@@ -463,16 +495,33 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
   pa.n_split = p.pool_nsplit;
   pa.logits = fa.logits;
   pa.logit_stride = p.logit_stride;
-  if (p.pool_logits) {
+  if (p.pool_logits)
     HS2_TRY_LAUNCH(KK_POOL_LOGITS, s, launch_pool_logits(pa, s));
-  } else if (env_int("HS2_POOL_HIST_SEPARATE", 0)) {
-    pa.hist = nullptr;
+  else
     HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
-    HS2_TRY_LAUNCH(KK_SEL_HIST, s, launch_sel_hist(sa, p.sel_nchunks, s));
-  } else {
-    HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
-  }
   return run_selection_tail(p, sa, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                      const int32_t* len, int32_t k, int32_t window, uint16_t* out, int32_t* idx,
+                                      float* stats, float* scores, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+  return full_attn_impl(dims, q, K, V, nullptr, nullptr, len, k, window, out, idx, stats, scores, workspace,
+                        workspace_bytes, stream);
+}
+
+hs2_status hs2_full_attn_score_select_fp8(const hs2_dims* dims, const uint16_t* q, const uint8_t* K,
+                                          const uint8_t* V, const float* k_scale, const float* v_scale,
+                                          const int32_t* len, int32_t k, int32_t window, uint16_t* out,
+                                          int32_t* idx, float* stats, float* scores, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  if (!k_scale || !v_scale) return fail(HS2_ERR_NULL, "k_scale and v_scale are required for an FP8 cache");
+  return full_attn_impl(dims, q, K, V, k_scale, v_scale, len, k, window, out, idx, stats, scores, workspace,
+                        workspace_bytes, stream);
 }
 
 hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
@@ -503,13 +552,19 @@ hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16
                             stream);
 }
 
-hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
-                              const int32_t* len, const int32_t* idx, int32_t n_slots, const float* sink,
-                              const uint16_t* gate, uint16_t* out, void* workspace, size_t workspace_bytes,
-                              void* stream) {
+}  // extern "C"
+
+namespace {
+
+hs2_status sparse_impl(const hs2_dims* dims, const uint16_t* q, const void* K, const void* V, const float* k_scale,
+                       const float* v_scale, const int32_t* len, const int32_t* idx, int32_t n_slots,
+                       const float* sink, const uint16_t* gate, uint16_t* out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  const bool kv8 = k_scale != nullptr;
   hs2_status st = check_dims(dims);
   if (st != HS2_OK) return st;
   if (n_slots < 1 || n_slots > kMaxLen) return fail(HS2_ERR_SHAPE, "n_slots must be in [1, 2^27]");
+  if (kv8 && (st = check_fp8(dims, k_scale, v_scale)) != HS2_OK) return st;
   if (!q || !K || !V || !len || !idx || !out || !workspace)
     return fail(HS2_ERR_NULL, "q, K, V, len, idx, out and workspace are required");
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
@@ -518,7 +573,7 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
                 "q/K/V/out need 16-byte, workspace 256-byte, gate 8-byte, idx/len/sink 4-byte alignment");
   const DeviceInfo* di = try_device_info();
   Plan p;
-  make_plan(dims, 0, n_slots, p, di);
+  make_plan(dims, 0, n_slots, p, di, kv8);
   SaPlan sp;
   make_sa_plan(p, n_slots, sp);
   if (workspace_bytes < sp.bytes)
@@ -528,8 +583,9 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
   char* ws = (char*)workspace;
   SaArgs a{};
   a.q = q;
-  a.K = K;
-  a.V = V;
+  a.K = (const uint16_t*)K;
+  a.V = (const uint16_t*)V;
+  a.k_scale = k_scale;
   a.len = len;
   a.idx = idx;
   a.part_o = (float*)(ws + sp.off_part_o);
@@ -571,8 +627,30 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
   ca.sa_mode = 1;
   ca.sink = sink;
   ca.gate = gate;
+  ca.v_scale = v_scale;
   HS2_TRY_LAUNCH(KK_SA_COMBINE, s, launch_combine(ca, p.G, p.rows, s));
   return HS2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                              const int32_t* len, const int32_t* idx, int32_t n_slots, const float* sink,
+                              const uint16_t* gate, uint16_t* out, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  return sparse_impl(dims, q, K, V, nullptr, nullptr, len, idx, n_slots, sink, gate, out, workspace,
+                     workspace_bytes, stream);
+}
+
+hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const uint8_t* K, const uint8_t* V,
+                               const float* k_scale, const float* v_scale, const int32_t* len, const int32_t* idx,
+                               int32_t n_slots, const float* sink, const uint16_t* gate, uint16_t* out,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  if (!k_scale || !v_scale) return fail(HS2_ERR_NULL, "k_scale and v_scale are required for an FP8 cache");
+  return sparse_impl(dims, q, K, V, k_scale, v_scale, len, idx, n_slots, sink, gate, out, workspace,
+                     workspace_bytes, stream);
 }
 
 hs2_status hs2_timing_enable(int32_t on) {

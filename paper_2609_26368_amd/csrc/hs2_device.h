@@ -393,6 +393,43 @@ __device__ inline void softmax_pv_swz(WaveState<RPW>& st, const unsigned char* s
 // No workgroup barrier: the wave only waits for its own direct LDS loads.
 constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
+// ---------------------------------------------------------------- FP8 cache rows
+// An FP8 (OCP E4M3) cache row is 128 bytes.  Rows are staged raw (row-major,
+// 128 B each) by the same 16-byte direct LDS loads -- a 1 KB load covers 8
+// rows -- and converted into the bf16 stage layout above, so every bf16
+// operand read is shared by both cache formats.
+
+// Four E4M3 values (the bytes of w, low first) -> four bf16 in two packed
+// words, exactly (every E4M3 value is a bf16 value): gfx950's scaled
+// conversion with scale 1, bytes 0-1 and (op_sel) bytes 2-3.
+__device__ inline uint2 e4m3x4_to_bf16x4(uint32_t w) {
+  uint32_t lo, hi;
+  asm("v_cvt_scalef32_pk_bf16_fp8 %0, %1, 1.0" : "=v"(lo) : "v"(w));
+  asm("v_cvt_scalef32_pk_bf16_fp8 %0, %1, 1.0 op_sel:[1,0,0]" : "=v"(hi) : "v"(w));
+  return make_uint2(lo, hi);
+}
+
+// Convert NR staged E4M3 rows (raw, 128 B each) into bf16 stage rows at stg
+// (chunk c of row r at position c ^ (r & 15)); threads tid of NTHR.  A job is
+// one 16-byte raw piece: 16 values, two bf16 chunks.
+template <int NR, int NTHR>
+__device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
+  constexpr int JOBS = NR * 8;
+#pragma unroll
+  for (int k = 0; k < (JOBS + NTHR - 1) / NTHR; ++k) {
+    const int j = tid + k * NTHR;
+    if (JOBS % NTHR == 0 || j < JOBS) {
+      const int r = j >> 3, p = j & 7;
+      const uint4 v = *(const uint4*)(raw + r * 128 + 16 * p);
+      const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
+      const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
+      unsigned char* rp = stg + r * STAGE_ROW_BYTES;
+      *(uint4*)(rp + 16 * ((2 * p) ^ (r & 15))) = make_uint4(a.x, a.y, b.x, b.y);
+      *(uint4*)(rp + 16 * ((2 * p + 1) ^ (r & 15))) = make_uint4(c.x, c.y, d.x, d.y);
+    }
+  }
+}
+
 // s_waitcnt vmcnt(per_stage * stages) for stages in [0, 5] (larger values
 // wait as for 5; counts above the 6-bit field wait for 63: both only wait
 // longer than needed)

@@ -149,14 +149,22 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // streams through a private ring with NS - 1 stages in flight; with one wave
 // there is no barrier at all, with two waves one barrier per stage.  One
 // partial (m, l, O) per split.
-template <int RT, int NWV, int TW, int NS, int TGW>
+// KV8: the cache is E4M3 bytes with one scale per KV head (k_scale folds
+// into the logit scale, v_scale is applied by the merge); each token group
+// stages raw rows in its ring and converts the current tile into one bf16
+// tile before computing on it.
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
-  constexpr int NB = TW / 16;             // 16-row blocks per stage
-  constexpr int LPM = TW / 4 / NWV;       // 1 KB loads per matrix per stage per wave
-  constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
+  constexpr int NB = TW / 16;                              // 16-row blocks per stage
+  constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;          // bytes of a staged cache row
+  constexpr int LPM = TW * RB / 1024 / NWV;                // 1 KB loads per matrix per stage per wave
+  constexpr int SB = 2 * TW * RB;                          // ring stage: K rows then V rows
+  constexpr int TB = KV8 ? 2 * TW * STAGE_ROW_BYTES : 0;   // converted bf16 tile
+  constexpr int GB = NS * SB + TB;                         // LDS of one token group
+  static_assert(LPM >= 1, "each wave loads at least one 1 KB piece per matrix and stage");
   static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
-  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HD * 4 <= TGW * NS * SB,
+  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HD * 4 <= TGW * GB,
                 "the merge fits in the rings");
   extern __shared__ __align__(16) unsigned char smem[];
 
@@ -182,11 +190,15 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     rpos[rr] = c < a.C ? Lv - a.C + c : Lv - 1;  // padding rows see everything
   }
   const int min_pos = Lv - a.C;
-  const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
-  const uint16_t* Kbg = a.K + kvoff;
-  const uint16_t* Vbg = a.V + kvoff;
-  const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * NS * SB);
-  unsigned char* ring_p = smem + tg * NS * SB;
+  constexpr int ESZ = KV8 ? 1 : 2;  // bytes per cache element
+  const int64_t kvoff = ((int64_t)b * a.stride_b + (int64_t)g * a.stride_h) * ESZ;
+  const unsigned char* Kbg = (const unsigned char*)a.K + kvoff;
+  const unsigned char* Vbg = (const unsigned char*)a.V + kvoff;
+  const int64_t stride_t = a.stride_t * ESZ;  // bytes
+  const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
+  const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * GB);
+  unsigned char* ring_p = smem + tg * GB;
+  unsigned char* tile_p = ring_p + NS * SB;  // KV8: the converted tile
   // logits output of a single row tile (C G <= 16 query rows): this lane's
   // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
   float* lrow = nullptr;
@@ -197,29 +209,33 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       lrow = a.logits + (((int64_t)b * a.Hkv + g) * a.C * a.G + c * a.G + h) * a.logit_stride;
   }
 
-  // per-lane part of each load's element offset: row * stride + swizzled chunk
+  // per-lane part of each load's byte offset: bf16 rows are 4 per 1 KB load,
+  // swizzled chunks; E4M3 rows are 8 per load, raw
+  constexpr int RPL = 1024 / RB;  // rows per 1 KB load
+  auto lane_offset = [&](int row, int t) -> int64_t {
+    return KV8 ? (int64_t)t * stride_t + 16 * (lane & 7) : (int64_t)t * stride_t + 16 * ((lane & 15) ^ (row & 15));
+  };
   int64_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
-    const int row = 4 * (wave * LPM + u) + (lane >> 4);
-    lane_off[u] = (int64_t)row * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+    const int row = RPL * (wave * LPM + u) + lane / (64 / RPL);
+    lane_off[u] = lane_offset(row, row);
   }
   auto issue = [&](int tile) {
     const int t0 = t_begin + tile * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
-    const int64_t tile_off = (int64_t)t0 * a.stride_t;
+    const int64_t tile_off = (int64_t)t0 * stride_t;
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
       int64_t off = tile_off + lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; masked below
-        const int row = 4 * n + (lane >> 4);
-        const int t = min(t0 + row, t_end - 1);
-        off = (int64_t)t * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+        const int row = RPL * n + lane / (64 / RPL);
+        off = lane_offset(row, min(t0 + row, t_end - 1));
       }
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
-      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * STAGE_ROW_BYTES + 1024 * n));
+      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
     }
   };
 
@@ -234,9 +250,14 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     // logits stores also count in vmcnt; they only make this wait longer
     if (i < ntiles) wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
     if (NWV * TGW > 1) __syncthreads();
-    if (i >= ntiles) continue;
-    if (i + NS - 1 < ntiles) issue(i + NS - 1);
+    if (i < ntiles && i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = ring_p + (i % NS) * SB;
+    if constexpr (KV8) {
+      if (i < ntiles) convert_rows_e4m3<2 * TW, 64 * NWV>(stg, tile_p, 64 * wave + lane);
+      if (NWV * TGW > 1) __syncthreads();  // every group's tile converted
+      stg = tile_p;
+    }
+    if (i >= ntiles) continue;
     const int t0 = t_begin + i * TW;
     f32x4 S[NB][RPW];
 #pragma unroll
@@ -244,7 +265,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     if constexpr (RT == 1) {  // the lane's 4 consecutive tokens; the row stride covers whole tiles
       if (lrow)
 #pragma unroll
-        for (int bi = 0; bi < NB; ++bi) *(f32x4*)(lrow + t0 + 16 * bi + 4 * (lane >> 4)) = S[bi][0] * a.c2;
+        for (int bi = 0; bi < NB; ++bi) *(f32x4*)(lrow + t0 + 16 * bi + 4 * (lane >> 4)) = S[bi][0] * c2;
     }
     const bool full = (t0 + TW <= t_end) && (t0 + TW - 1 <= min_pos);
 #pragma unroll
@@ -253,7 +274,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       for (int rr = 0; rr < RPW; ++rr)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
-          float v = S[bi][rr][ii] * a.c2;
+          float v = S[bi][rr][ii] * c2;
           if (!full) {
             const int t = t0 + 16 * bi + 4 * (lane >> 4) + ii;
             if (t >= t_end || t > rpos[rr]) v = -INFINITY;
@@ -429,7 +450,7 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
     o.w += s_o[j][dq].w;
   }
   if (sink2 != -INFINITY) Z += fast_exp2(sink2 - M);
-  const float inv = Z > 0.f ? 1.f / Z : 0.f;
+  const float inv = (Z > 0.f ? 1.f / Z : 0.f) * (a.v_scale ? a.v_scale[g] : 1.f);
   o.x *= inv;
   o.y *= inv;
   o.z *= inv;
@@ -556,23 +577,30 @@ __device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g,
 // rows), every wave reads the whole tile as the MFMA B operand against its
 // own query row tiles held in registers.  Dynamic LDS: ring + C packed
 // first-level histograms (16-bit counters; a split has < 65536 tokens).
-template <int RT, int GP>
+// KV8: E4M3 cache with one K scale per KV head (folded into the logit
+// scale); raw rows are staged and converted like in k_fa_ring.
+template <int RT, int GP, bool KV8 = false>
 struct PoolShape {
   static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
   static constexpr int RPW = RT == 1 ? 1 : (TPQ > 2 ? TPQ : 2);  // row tiles per wave
   static constexpr int NWV = RT / RPW;
-  static constexpr int TW = 16, NS = 4;
-  static constexpr int SB = TW * STAGE_ROW_BYTES;
+  static constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;      // bytes of a staged row
+  // whole 1 KB loads for every wave: E4M3 tiles of 8 NWV rows when that is more than 16
+  static constexpr int TW = (KV8 && 8 * NWV > 16) ? 8 * NWV : 16, NS = 4;
+  static constexpr int SB = TW * RB;                          // ring stage
+  static constexpr int TB = KV8 ? TW * STAGE_ROW_BYTES : 0;   // converted tile
+  static constexpr int LDS = NS * SB + TB;                    // before the histograms
 };
-template <int RT, int GP>
+template <int RT, int GP, bool KV8>
 __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
-  using PS = PoolShape<RT, GP>;
-  constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB;
+  using PS = PoolShape<RT, GP, KV8>;
+  constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB, RB = PS::RB;
   constexpr int NB = TW / 16;
-  constexpr int LPM = TW / 4 / NWV;  // 1 KB loads per stage per wave
-  static_assert(LPM >= 1, "each wave loads at least one 1 KB piece per stage");
+  constexpr int LPM = TW * RB / 1024 / NWV;  // 1 KB loads per stage per wave
+  static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  uint32_t* hist = (uint32_t*)(smem + NS * SB);  // [C][NBINS/2]
+  unsigned char* tile_p = smem + NS * SB;            // KV8: the converted tile
+  uint32_t* hist = (uint32_t*)(smem + PS::LDS);       // [C][NBINS/2]
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -592,27 +620,33 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   float fac[RPW][4], msub[RPW][4];
   pool_row_consts<RPW, GP>(a, b, g, rt0, lane, fac, msub);
 
-  const uint16_t* Kbg = a.K + (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
+  constexpr int ESZ = KV8 ? 1 : 2;  // bytes per cache element
+  const unsigned char* Kbg = (const unsigned char*)a.K + ((int64_t)b * a.stride_b + (int64_t)g * a.stride_h) * ESZ;
+  const int64_t stride_t = a.stride_t * ESZ;
+  const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem);
+  constexpr int RPL = 1024 / RB;  // rows per 1 KB load
+  auto lane_offset = [&](int row, int t) -> int64_t {
+    return KV8 ? (int64_t)t * stride_t + 16 * (lane & 7) : (int64_t)t * stride_t + 16 * ((lane & 15) ^ (row & 15));
+  };
   int64_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
-    const int row = 4 * (wave * LPM + u) + (lane >> 4);
-    lane_off[u] = (int64_t)row * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+    const int row = RPL * (wave * LPM + u) + lane / (64 / RPL);
+    lane_off[u] = lane_offset(row, row);
   }
   auto issue = [&](int tile) {
     const int t0 = t_begin + tile * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
-    const int64_t tile_off = (int64_t)t0 * a.stride_t;
+    const int64_t tile_off = (int64_t)t0 * stride_t;
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
       int64_t off = tile_off + lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; never emitted
-        const int row = 4 * n + (lane >> 4);
-        const int t = min(t0 + row, t_end - 1);
-        off = (int64_t)t * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+        const int row = RPL * n + lane / (64 / RPL);
+        off = lane_offset(row, min(t0 + row, t_end - 1));
       }
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
     }
@@ -638,6 +672,11 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     if (NWV > 1) __syncthreads();
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = smem + (i % NS) * SB;
+    if constexpr (KV8) {
+      convert_rows_e4m3<TW, 64 * NWV>(stg, tile_p, tid);
+      if (NWV > 1) __syncthreads();
+      stg = tile_p;
+    }
     const int t0 = t_begin + i * TW;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
@@ -653,7 +692,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
       }
-      pool_emit_block<RPW, GP>(acc, a.c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
+      pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
     }
   }
   __syncthreads();
@@ -1061,14 +1100,19 @@ __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
 // entries are staged in LDS first; each stage then gathers its rows straight
 // into the ring (per-lane addresses), invalid entries (< 0 or >= len) read
 // row 0 and are masked out of the softmax.
-template <int RT, int NWV, int TW, int NS>
+template <int RT, int NWV, int TW, int NS, bool KV8>
 __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   constexpr int RPW = RT / NWV;
   constexpr int NB = TW / 16;
-  constexpr int LPM = TW / 4 / NWV;
-  constexpr int SB = 2 * TW * STAGE_ROW_BYTES;
+  constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;  // bytes of a staged cache row
+  constexpr int RPL = 1024 / RB;                    // rows per 1 KB load
+  constexpr int LPM = TW * RB / 1024 / NWV;
+  constexpr int SB = 2 * TW * RB;
+  constexpr int TB = KV8 ? 2 * TW * STAGE_ROW_BYTES : 0;  // converted tile
+  static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  int32_t* sidx = (int32_t*)(smem + NS * SB);  // [split_slots]
+  unsigned char* tile_p = smem + NS * SB;                  // KV8: the converted tile
+  int32_t* sidx = (int32_t*)(smem + NS * SB + TB);        // [split_slots]
 
   const int split = blockIdx.x;
   const int64_t unit = blockIdx.y;
@@ -1104,9 +1148,12 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));
   __syncthreads();
 
-  const int64_t kvoff = (int64_t)b * a.stride_b + (int64_t)g * a.stride_h;
-  const uint16_t* Kbg = a.K + kvoff;
-  const uint16_t* Vbg = a.V + kvoff;
+  constexpr int ESZ = KV8 ? 1 : 2;  // bytes per cache element
+  const int64_t kvoff = ((int64_t)b * a.stride_b + (int64_t)g * a.stride_h) * ESZ;
+  const unsigned char* Kbg = (const unsigned char*)a.K + kvoff;
+  const unsigned char* Vbg = (const unsigned char*)a.V + kvoff;
+  const int64_t stride_t = a.stride_t * ESZ;
+  const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem);
   uint32_t vmask[NS];  // row-validity bits of each ring stage (wave-uniform)
 
@@ -1116,14 +1163,15 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
-      const int row = 4 * n + (lane >> 4);
+      const int row = RPL * n + lane / (64 / RPL);
       const int t = sidx[tile * TW + row];
-      const int64_t off = (int64_t)(t < 0 ? 0 : t) * a.stride_t + 8 * ((lane & 15) ^ (row & 15));
+      const int64_t off = (int64_t)(t < 0 ? 0 : t) * stride_t +
+                          (KV8 ? 16 * (lane & 7) : 16 * ((lane & 15) ^ (row & 15)));
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
-      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * STAGE_ROW_BYTES + 1024 * n));
-      const uint64_t bal = __ballot(t >= 0);  // lanes 16j .. 16j+15 hold row 4n + j
+      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
+      const uint64_t bal = __ballot(t >= 0);  // lanes (64 / RPL) j .. hold row RPL n + j
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mask |= (uint32_t)((bal >> (16 * j)) & 1ull) << (4 * n + j);
+      for (int j = 0; j < RPL; ++j) mask |= (uint32_t)((bal >> ((64 / RPL) * j)) & 1ull) << (RPL * n + j);
     }
     return mask;
   };
@@ -1146,13 +1194,17 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
       for (int k = 0; k < NS; ++k)
         if (k == (i + NS - 1) % NS) vmask[k] = mnew;
     }
+    const unsigned char* stg = smem + (i % NS) * SB;
+    if constexpr (KV8) {  // converted tile complete at the barrier below (one wave: in order)
+      convert_rows_e4m3<2 * TW, 64 * NWV>(stg, tile_p, threadIdx.x);
+      stg = tile_p;
+    }
     if (NWV > 1) {  // both waves' row bits
       __shared__ uint32_t s_mask[2];
       if (lane == 0) s_mask[wave] = m_i;
       __syncthreads();
       m_i = s_mask[0] | s_mask[1];
     }
-    const unsigned char* stg = smem + (i % NS) * SB;
     f32x4 S[NB][RPW];
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
@@ -1163,7 +1215,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
           const int row = 16 * bi + 4 * (lane >> 4) + ii;
-          S[bi][rr][ii] = ((m_i >> row) & 1u) ? S[bi][rr][ii] * a.c2 : -INFINITY;
+          S[bi][rr][ii] = ((m_i >> row) & 1u) ? S[bi][rr][ii] * c2 : -INFINITY;
         }
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
@@ -1232,14 +1284,23 @@ static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t
   return e;
 }
 
-hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs) {
+// LDS of a full-attention ring kernel: per token group the ring of raw rows
+// (bf16 256 B or E4M3 128 B) and, for E4M3, one converted bf16 tile
+constexpr size_t fa_ring_lds(int tw, int ns, int tgw, bool kv8) {
+  return (size_t)tgw * ((size_t)ns * 2 * tw * (kv8 ? 128 : STAGE_ROW_BYTES) + (kv8 ? 2 * tw * STAGE_ROW_BYTES : 0));
+}
+
+hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
   *wgs = 0;
-#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw)                                                          \
-  if (variant == v && RT == rt)                                                                         \
-    return occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw>, 64 * nwv * tgw,         \
-                            (size_t)tgw * ns * 2 * tw * STAGE_ROW_BYTES);
+#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw)                                                                   \
+  if (variant == v && RT == rt)                                                                                  \
+    return kv8 ? occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true>, 64 * nwv * tgw,        \
+                                  fa_ring_lds(tw, ns, tgw, true))                                                \
+               : occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false>, 64 * nwv * tgw,       \
+                                  fa_ring_lds(tw, ns, tgw, false));
   HS2_RING_VARIANTS(HS2_RING_OCC)
 #undef HS2_RING_OCC
+  if (kv8) return hipSuccess;  // E4M3 only through the ring kernels
   const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
   switch (RT) {
     case 1: return occupancy_capped(wgs, (const void*)k_fa_split<1>, 64 * FaShape<1>::NW, sm);
@@ -1254,12 +1315,17 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) 
   dim3 grid(a.n_split, a.Hkv, a.B);
 #define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw)                                                       \
   if (variant == v && RT == rt) {                                                                       \
-    HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw>), grid, dim3(64 * nwv * tgw),                         \
-               (size_t)tgw * ns * 2 * tw * STAGE_ROW_BYTES, s, a);                                     \
+    if (a.k_scale)                                                                                      \
+      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, true>), grid, dim3(64 * nwv * tgw),                  \
+                 fa_ring_lds(tw, ns, tgw, true), s, a);                                                 \
+    else                                                                                                \
+      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, false>), grid, dim3(64 * nwv * tgw),                 \
+                 fa_ring_lds(tw, ns, tgw, false), s, a);                                                \
     return hipGetLastError();                                                                          \
   }
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
 #undef HS2_RING_LAUNCH
+  if (a.k_scale) return hipErrorInvalidValue;  // E4M3 only through the ring kernels
   const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
   switch (RT) {
     case 1: HS2_LAUNCH(k_fa_split<1>, grid, dim3(64 * FaShape<1>::NW), sm, s, a); break;
@@ -1271,8 +1337,9 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) 
   return hipGetLastError();
 }
 
+template <int RT, int GP, bool KV8>
 size_t pool_smem_bytes(int C) {
-  return (size_t)PoolShape<1, 1>::NS * PoolShape<1, 1>::SB + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
+  return (size_t)PoolShape<RT, GP, KV8>::LDS + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
 }
 
 // pool kernels for every (row tiles, padded group) pair the planner can produce:
@@ -1290,24 +1357,33 @@ hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t pool_wgs_per_cu(int RT, int Gp, int C, int* wgs) {
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int* wgs) {
   *wgs = 0;
-#define HS2_POOL_OCC(rt, gp)                                                                                   \
-  if (RT == rt && Gp == gp)                                                                                    \
-    return occupancy_capped(wgs, (const void*)k_pool<rt, gp>, 64 * PoolShape<rt, gp>::NWV, pool_smem_bytes(C));
+#define HS2_POOL_OCC(rt, gp)                                                                                  \
+  if (RT == rt && Gp == gp)                                                                                   \
+    return kv8 ? occupancy_capped(wgs, (const void*)k_pool<rt, gp, true>, 64 * PoolShape<rt, gp>::NWV,         \
+                                  pool_smem_bytes<rt, gp, true>(C))                                           \
+               : occupancy_capped(wgs, (const void*)k_pool<rt, gp, false>, 64 * PoolShape<rt, gp>::NWV,        \
+                                  pool_smem_bytes<rt, gp, false>(C));
   HS2_POOL_CASES(HS2_POOL_OCC)
 #undef HS2_POOL_OCC
   return hipSuccess;
 }
 
+template <int RT, int GP, bool KV8>
+hipError_t launch_pool_one(const PoolArgs& a, dim3 grid, int hc, hipStream_t s) {
+  HS2_LAUNCH((k_pool<RT, GP, KV8>), grid, dim3(64 * PoolShape<RT, GP, KV8>::NWV), (pool_smem_bytes<RT, GP, KV8>(hc)),
+             s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-  const size_t sm = pool_smem_bytes(a.hist ? a.C : 0);
-#define HS2_POOL_LAUNCH(rt, gp)                                                                   \
-  if (RT == rt && a.Gp == gp) {                                                                   \
-    HS2_LAUNCH((k_pool<rt, gp>), grid, dim3(64 * PoolShape<rt, gp>::NWV), sm, s, a);              \
-    return hipGetLastError();                                                                     \
-  }
+  const int hc = a.hist ? a.C : 0;  // histograms in LDS
+#define HS2_POOL_LAUNCH(rt, gp)                                                              \
+  if (RT == rt && a.Gp == gp)                                                                \
+    return a.k_scale ? launch_pool_one<rt, gp, true>(a, grid, hc, s)                         \
+                     : launch_pool_one<rt, gp, false>(a, grid, hc, s);
   HS2_POOL_CASES(HS2_POOL_LAUNCH)
 #undef HS2_POOL_LAUNCH
   return hipErrorInvalidValue;
@@ -1319,21 +1395,25 @@ hipError_t set_pool_smem_limits() {
   // dynamic LDS above 64 KB must be allowed explicitly
   const int big = 150 * 1024;  // leaves room for static LDS; no kernel asks for more
   hipError_t e = hipSuccess;
-#define HS2_POOL_ATTR(rt, gp) \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_POOL_ATTR(rt, gp)                                                                                    \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   HS2_POOL_CASES(HS2_POOL_ATTR)
 #undef HS2_POOL_ATTR
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<1>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<2>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<4>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<8>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw) \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw)                                                                   \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
   HS2_RING_VARIANTS(HS2_RING_ATTR)
 #undef HS2_RING_ATTR
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<1, 1, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<2, 1, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<4, 2, SAR_TW, SAR_NS>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_SA_ATTR(rt, nwv)                                                                                     \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
+  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  HS2_SA_ATTR(1, 1) HS2_SA_ATTR(2, 1) HS2_SA_ATTR(4, 2)
+#undef HS2_SA_ATTR
   return e;
 }
 
@@ -1361,20 +1441,26 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t sa_smem_bytes(int split_slots) {
-  return (size_t)SAR_NS * 2 * SAR_TW * STAGE_ROW_BYTES + sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
+size_t sa_smem_bytes(int split_slots, bool kv8) {
+  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? 128 : STAGE_ROW_BYTES) + (kv8 ? 2 * SAR_TW * STAGE_ROW_BYTES : 0) +
+         sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
 }
 
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, (unsigned)((int64_t)a.B * a.Hkv * a.C));
-  const size_t sm = sa_smem_bytes(a.split_slots);
-  switch (RT) {
-    case 1: HS2_LAUNCH((k_sa_ring<1, 1, SAR_TW, SAR_NS>), grid, dim3(64), sm, s, a); break;
-    case 2: HS2_LAUNCH((k_sa_ring<2, 1, SAR_TW, SAR_NS>), grid, dim3(64), sm, s, a); break;
-    case 4: HS2_LAUNCH((k_sa_ring<4, 2, SAR_TW, SAR_NS>), grid, dim3(128), sm, s, a); break;
-    default: return hipErrorInvalidValue;
+  const bool kv8 = a.k_scale != nullptr;
+  const size_t sm = sa_smem_bytes(a.split_slots, kv8);
+#define HS2_SA_LAUNCH(rt, nwv)                                                                   \
+  if (RT == rt) {                                                                                \
+    if (kv8)                                                                                     \
+      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true>), grid, dim3(64 * nwv), sm, s, a);    \
+    else                                                                                         \
+      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false>), grid, dim3(64 * nwv), sm, s, a);   \
+    return hipGetLastError();                                                                    \
   }
-  return hipGetLastError();
+  HS2_SA_LAUNCH(1, 1) HS2_SA_LAUNCH(2, 1) HS2_SA_LAUNCH(4, 2)
+#undef HS2_SA_LAUNCH
+  return hipErrorInvalidValue;
 }
 
 }  // namespace hs2

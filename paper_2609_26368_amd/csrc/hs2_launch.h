@@ -19,6 +19,7 @@ struct FaArgs {
   int split_tokens, n_split;
   float* logits;   // [B*Hkv][C*G][logit_stride] logits in log2 units (ring kernels), or null
   int64_t logit_stride;
+  const float* k_scale;  // [Hkv] for an E4M3 cache (K, V are then byte arrays), else null
 };
 
 struct CombineArgs {
@@ -38,6 +39,7 @@ struct CombineArgs {
   int64_t n_clear;
   const float* sink;    // [Hq] sink logits (natural units of the scaled logits) or null
   const uint16_t* gate; // [B, C, Hq, D] bf16 output gate logits or null
+  const float* v_scale; // [Hkv] E4M3 cache: output scale of each KV head, or null
 };
 
 struct PoolArgs {
@@ -49,6 +51,7 @@ struct PoolArgs {
   uint32_t* hist;       // [rows][NBINS]
   const float* logits;  // [B*Hkv][C*G][logit_stride] (k_pool_logits)
   int64_t logit_stride;
+  const float* k_scale;  // [Hkv] for an E4M3 cache, else null
   int64_t stride_b, stride_h, stride_t;
   int64_t score_stride;
   float c2;
@@ -82,6 +85,7 @@ struct SaArgs {
   float c2;
   int B, C, Hq, Hkv, G, max_len;
   int n_slots, split_slots, n_split;
+  const float* k_scale;  // [Hkv] for an E4M3 cache, else null
 };
 
 constexpr int kFaVariants = 6;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
@@ -90,14 +94,13 @@ int fa_split_align(int RT, int variant);   // split lengths are multiples of thi
 bool fa_variant_exists(int RT, int variant);
 // workgroups of the full-attention kernel (RT, variant) resident per compute
 // unit on the current device (0 if that kernel does not exist)
-hipError_t fa_wgs_per_cu(int RT, int variant, int* wgs);
-hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
+hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs);
+hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);  // a.k_scale: E4M3 cache
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s);
-size_t pool_smem_bytes(int C);
 // workgroups of k_pool (RT, Gp) with C queries resident per compute unit
-hipError_t pool_wgs_per_cu(int RT, int Gp, int C, int* wgs);
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int* wgs);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);

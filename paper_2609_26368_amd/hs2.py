@@ -27,7 +27,7 @@ HS2_ERR_ALIGN = -5
 HS2_ERR_HIP = -6
 
 EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_sparse_attn_ex",
-            "hs2_select_from_scores",
+            "hs2_full_attn_score_select_fp8", "hs2_sparse_attn_fp8", "hs2_select_from_scores",
             "hs2_status_string", "hs2_last_error", "hs2_timing_enable", "hs2_timing_reset", "hs2_timing_read"]
 
 
@@ -65,6 +65,10 @@ def load() -> ctypes.CDLL:
     lib.hs2_sparse_attn.restype = I32
     lib.hs2_sparse_attn_ex.argtypes = [D, P, P, P, P, P, I32, P, P, P, P, SZ, P]
     lib.hs2_sparse_attn_ex.restype = I32
+    lib.hs2_full_attn_score_select_fp8.argtypes = [D, P, P, P, P, P, P, I32, I32, P, P, P, P, P, SZ, P]
+    lib.hs2_full_attn_score_select_fp8.restype = I32
+    lib.hs2_sparse_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, I32, P, P, P, P, SZ, P]
+    lib.hs2_sparse_attn_fp8.restype = I32
     lib.hs2_select_from_scores.argtypes = [D, P, P, I32, I32, P, P, SZ, P]
     lib.hs2_select_from_scores.restype = I32
     lib.hs2_status_string.argtypes = [I32]
@@ -120,16 +124,25 @@ def _expect(t, name, shape, dtypes, device):
 _BF16 = (torch.bfloat16, torch.int16, torch.uint16)
 
 
-def _check_kv(dims, K, V, device):
+_FP8 = (torch.uint8, torch.float8_e4m3fn)
+
+
+def _check_kv(dims, K, V, device, fp8=False):
+    dtypes, what = (_FP8, "E4M3 (uint8)") if fp8 else (_BF16, "bf16")
     for name, t in (("K", K), ("V", V)):
-        if t.dtype not in _BF16 or t.device != device:
-            raise ValueError(f"{name}: bf16 tensor on {device} expected")
+        if t.dtype not in dtypes or t.device != device:
+            raise ValueError(f"{name}: {what} tensor on {device} expected")
         # largest element offset the kernels may touch must lie inside the tensor's storage
         last = ((dims.batch - 1) * dims.kv_stride_b + (dims.n_kv_heads - 1) * dims.kv_stride_h
                 + (dims.max_len - 1) * dims.kv_stride_t + dims.head_dim)
-        avail = t.untyped_storage().nbytes() // 2 - t.storage_offset()
+        avail = t.untyped_storage().nbytes() // t.element_size() - t.storage_offset()
         if last > avail:
             raise ValueError(f"{name}: strides address {last} elements, storage holds {avail}")
+
+
+def _check_scales(dims, k_scale, v_scale, device):
+    for name, t in (("k_scale", k_scale), ("v_scale", v_scale)):
+        _expect(t, name, (dims.n_kv_heads,), (torch.float32,), device)
 
 
 def hs2_workspace_bytes(dims: hs2_dims, k: int, window: int) -> int:
@@ -192,6 +205,52 @@ def hs2_sparse_attn_ex(dims, q, K, V, len, idx, n_slots, sink, gate, out, worksp
                                      workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
+def hs2_full_attn_score_select_fp8(dims, q, K8, V8, k_scale, v_scale, len, k, window, out, idx, stats=None,
+                                   scores=None, workspace=None, stream=None):
+    """hs2_full_attn_score_select over an E4M3 cache (uint8 K8/V8, fp32 scales [Hkv])."""
+    dev = q.device
+    B, C, Hq, Hkv, D, L = dims.batch, dims.n_queries, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.max_len
+    _expect(q, "q", (B, C, Hq, D), _BF16, dev)
+    _check_kv(dims, K8, V8, dev, fp8=True)
+    _check_scales(dims, k_scale, v_scale, dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(out, "out", (B, C, Hq, D), _BF16, dev)
+    _expect(idx, "idx", (B, Hkv, C, k + window), (torch.int32,), dev)
+    if stats is not None:
+        _expect(stats, "stats", (B, C, Hq, 2), (torch.float32,), dev)
+    if scores is not None:
+        _expect(scores, "scores", (B, Hkv, C, L), (torch.float32,), dev)
+    need = hs2_workspace_bytes(dims, k, window)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace of {need} bytes required")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(load().hs2_full_attn_score_select_fp8(ctypes.byref(dims), _ptr(q), _ptr(K8), _ptr(V8), _ptr(k_scale),
+                                                 _ptr(v_scale), _ptr(len), int(k), int(window), _ptr(out), _ptr(idx),
+                                                 _ptr(stats), _ptr(scores), _ptr(workspace), ws_bytes,
+                                                 _stream(stream)))
+
+
+def hs2_sparse_attn_fp8(dims, q, K8, V8, k_scale, v_scale, len, idx, n_slots, sink, gate, out, workspace,
+                        stream=None):
+    """hs2_sparse_attn_ex over an E4M3 cache (sink and gate may be None)."""
+    dev = q.device
+    B, C, Hq, Hkv, D = dims.batch, dims.n_queries, dims.n_q_heads, dims.n_kv_heads, dims.head_dim
+    _expect(q, "q", (B, C, Hq, D), _BF16, dev)
+    _check_kv(dims, K8, V8, dev, fp8=True)
+    _check_scales(dims, k_scale, v_scale, dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(idx, "idx", (B, Hkv, C, n_slots), (torch.int32,), dev)
+    _expect(out, "out", (B, C, Hq, D), _BF16, dev)
+    if sink is not None:
+        _expect(sink, "sink", (Hq,), (torch.float32,), dev)
+    if gate is not None:
+        _expect(gate, "gate", (B, C, Hq, D), _BF16, dev)
+    _check(load().hs2_sparse_attn_fp8(ctypes.byref(dims), _ptr(q), _ptr(K8), _ptr(V8), _ptr(k_scale), _ptr(v_scale),
+                                      _ptr(len), _ptr(idx), int(n_slots), _ptr(sink), _ptr(gate), _ptr(out),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+
+
 def hs2_select_from_scores(dims, scores, len, k, window, idx, workspace, stream=None):
     """Selection alone from given pooled scores [B, Hkv, C, max_len] float32."""
     dev = scores.device
@@ -242,6 +301,7 @@ class HybridBlock:
 
     ``full(q, K, V, lens)`` runs the full-attention layer and selection and
     returns (out, idx); ``sparse(q, K, V, lens, idx)`` runs one sparse layer.
+    With ``kv_scales=(k_scale, v_scale)`` K and V are an E4M3 (uint8) cache.
     """
 
     def __init__(self, batch, n_queries, n_q_heads, n_kv_heads, head_dim, max_len, k, window, device="cuda",
@@ -254,23 +314,30 @@ class HybridBlock:
         self.workspace = torch.empty(need, dtype=torch.uint8, device=device)
         self.device = torch.device(device)
 
-    def full(self, q, K, V, lens, stats=None, scores=None, out=None, idx=None, stream=None):
+    def full(self, q, K, V, lens, stats=None, scores=None, out=None, idx=None, stream=None, kv_scales=None):
         d = self.dims
         if out is None:
             out = torch.empty((d.batch, d.n_queries, d.n_q_heads, d.head_dim), dtype=torch.bfloat16, device=q.device)
         if idx is None:
             idx = torch.empty((d.batch, d.n_kv_heads, d.n_queries, self.k + self.window), dtype=torch.int32,
                               device=q.device)
-        hs2_full_attn_score_select(d, q, K, V, lens, self.k, self.window, out, idx, stats, scores, self.workspace,
-                                   stream)
+        if kv_scales is None:
+            hs2_full_attn_score_select(d, q, K, V, lens, self.k, self.window, out, idx, stats, scores,
+                                       self.workspace, stream)
+        else:
+            hs2_full_attn_score_select_fp8(d, q, K, V, kv_scales[0], kv_scales[1], lens, self.k, self.window, out,
+                                           idx, stats, scores, self.workspace, stream)
         return out, idx
 
-    def sparse(self, q, K, V, lens, idx, out=None, stream=None, sink=None, gate=None):
+    def sparse(self, q, K, V, lens, idx, out=None, stream=None, sink=None, gate=None, kv_scales=None):
         """One sparse layer; sink [Hq] float32 and gate [B, C, Hq, D] bf16 are optional."""
         d = self.dims
         if out is None:
             out = torch.empty((d.batch, d.n_queries, d.n_q_heads, d.head_dim), dtype=torch.bfloat16, device=q.device)
-        if sink is None and gate is None:
+        if kv_scales is not None:
+            hs2_sparse_attn_fp8(d, q, K, V, kv_scales[0], kv_scales[1], lens, idx, idx.shape[-1], sink, gate, out,
+                                self.workspace, stream)
+        elif sink is None and gate is None:
             hs2_sparse_attn(d, q, K, V, lens, idx, idx.shape[-1], out, self.workspace, stream)
         else:
             hs2_sparse_attn_ex(d, q, K, V, lens, idx, idx.shape[-1], sink, gate, out, self.workspace, stream)

@@ -128,6 +128,58 @@ def test_sparse_ex_rejects_before_launch(lib):
     assert call(sink=FAKE, gate=FAKE, ws_bytes=256) == hs2.HS2_ERR_WORKSPACE
 
 
+def test_fp8_entry_points_reject_before_launch(lib):
+    vp = ctypes.c_void_p
+
+    def full(d, ks=FAKE, vs=FAKE, K=FAKE, ws_bytes=1 << 40):
+        return lib.hs2_full_attn_score_select_fp8(ctypes.byref(d), vp(FAKE), vp(K), vp(FAKE),
+                                                  None if ks is None else vp(ks), None if vs is None else vp(vs),
+                                                  vp(FAKE), 16, 8, vp(FAKE), vp(FAKE), None, None, vp(FAKE),
+                                                  ws_bytes, None)
+
+    def sparse(d, ks=FAKE, vs=FAKE, n_slots=24):
+        return lib.hs2_sparse_attn_fp8(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE),
+                                       None if ks is None else vp(ks), None if vs is None else vp(vs), vp(FAKE),
+                                       vp(FAKE), n_slots, None, None, vp(FAKE), vp(FAKE), 1 << 40, None)
+
+    d = dims()
+    for call in (full, sparse):
+        assert call(d, ks=None) == hs2.HS2_ERR_NULL
+        assert call(d, vs=None) == hs2.HS2_ERR_NULL
+        assert "scale" in hs2.hs2_last_error()
+        assert call(d, ks=FAKE + 2) == hs2.HS2_ERR_ALIGN
+        # one byte per element: strides must keep 16-byte loads aligned
+        assert call(dims(kv_strides=(4096 * 136 * 4, 4096 * 136, 136))) == hs2.HS2_ERR_ALIGN
+        # at most 64 query rows per KV head (C * pow2(G))
+        assert call(dims(n_queries=4, n_q_heads=32, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
+        assert call(dims(head_dim=64)) == hs2.HS2_ERR_UNSUPPORTED
+    assert full(d, K=FAKE + 8) == hs2.HS2_ERR_ALIGN
+    assert sparse(d, n_slots=0) == hs2.HS2_ERR_SHAPE
+    need = hs2.hs2_workspace_bytes(d, 16, 8)
+    assert full(d, ws_bytes=need - 256) == hs2.HS2_ERR_WORKSPACE
+
+
+def test_fp8_binding_checks_dtypes_before_calling():
+    import torch
+    d = dims(batch=1, max_len=64)
+    q = torch.zeros((1, 1, 32, 128), dtype=torch.bfloat16)
+    K8 = torch.zeros((1, 4, 64, 128), dtype=torch.uint8)
+    Kb = torch.zeros((1, 4, 64, 128), dtype=torch.bfloat16)
+    sc = torch.ones(4, dtype=torch.float32)
+    lens = torch.full((1,), 64, dtype=torch.int32)
+    out = torch.zeros((1, 1, 32, 128), dtype=torch.bfloat16)
+    idx = torch.zeros((1, 4, 1, 8), dtype=torch.int32)
+    ws = torch.zeros(1 << 20, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="E4M3"):  # a bf16 cache passed as FP8
+        hs2.hs2_full_attn_score_select_fp8(d, q, Kb, Kb, sc, sc, lens, 4, 4, out, idx, workspace=ws)
+    with pytest.raises(ValueError, match="k_scale"):
+        hs2.hs2_full_attn_score_select_fp8(d, q, K8, K8, torch.ones(3), sc, lens, 4, 4, out, idx, workspace=ws)
+    with pytest.raises(ValueError, match="v_scale"):
+        hs2.hs2_sparse_attn_fp8(d, q, K8, K8, sc, None, lens, idx, 8, None, None, out, ws)
+    with pytest.raises(ValueError, match="bf16"):  # an FP8 cache passed to the bf16 entry point
+        hs2.hs2_sparse_attn(d, q, K8, K8, lens, idx, 8, out, ws)
+
+
 def test_status_strings(lib):
     for code in (hs2.HS2_OK, hs2.HS2_ERR_NULL, hs2.HS2_ERR_SHAPE, hs2.HS2_ERR_UNSUPPORTED, hs2.HS2_ERR_WORKSPACE,
                  hs2.HS2_ERR_ALIGN, hs2.HS2_ERR_HIP):

@@ -1,0 +1,128 @@
+"""GPU parity of the FP8 (OCP E4M3) cache entry points.
+
+The cache is quantised on the host with one scale per KV head (the input
+generator's recipe); the oracle decodes the same bytes and scales in fp64, so
+the bar is the bf16 path's.  A second check needs no oracle: with
+power-of-two scales, a bf16 cache holding the dequantised values is the same
+cache, and the bf16 and FP8 entry points must agree bit for bit when both use
+the same splits.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hs2_oracle as O
+from paper_2609_26368_amd import workloads as W
+from tests import checker as CK
+from tests.test_gpu_parity import SMALL, dev_bf16, host_bits, note, parity_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_fp8_parity_small(w):
+    parity_case(w, kv="fp8")
+
+
+HEADS = [  # (Hq, Hkv, C) with C * pow2(G) <= 64 query rows per KV head
+    (12, 4, 1), (8, 8, 3), (16, 1, 2), (32, 1, 2), (6, 2, 5), (8, 2, 16),
+]
+
+
+@pytest.mark.parametrize("Hq,Hkv,C", HEADS, ids=[f"{a}q{b}kv_C{c}" for a, b, c in HEADS])
+def test_fp8_head_layouts(Hq, Hkv, C):
+    w = W.Workload(f"fp8_heads_{Hq}_{Hkv}_{C}", 2, 1500, C, Hq, Hkv, 128, 200, 48, 2, ctx_min=700)
+    parity_case(w, seed=5, kv="fp8")
+
+
+EDGES = [
+    # (name, batch, ctx, ctx_min, C, k, window)
+    ("single_token", 1, 1, 0, 1, 5, 3),
+    ("one_tile_plus_one", 1, 65, 0, 1, 10, 5),
+    ("k_exceeds_candidates", 2, 300, 150, 2, 400, 16),
+    ("window_only", 1, 900, 0, 3, 0, 50),
+]
+
+
+@pytest.mark.parametrize("name,B,ctx,ctx_min,C,k,win", EDGES, ids=[e[0] for e in EDGES])
+def test_fp8_edges(name, B, ctx, ctx_min, C, k, win):
+    w = W.Workload("fp8_" + name, B, ctx, C, 16, 2, 128, k, win, 1, ctx_min=ctx_min)
+    parity_case(w, seed=7, kv="fp8")
+
+
+def test_fp8_padded_capacity():
+    w = W.Workload("fp8_capacity", 3, 1000, 2, 16, 4, 128, 96, 32, 1, ctx_min=300)
+    parity_case(w, seed=9, lmax=1531, kv="fp8")
+
+
+def test_fp8_sparse_sink_and_gate():
+    from paper_2609_26368_amd import hs2
+    w = SMALL[3]
+    inp = W.make_inputs(w, seed=11, kv="fp8")
+    B, C, Hq, D = w.batch, w.n_queries, w.n_q_heads, w.head_dim
+    note(f"[fp8 sink-gate] {w.name} lens={inp.lens.tolist()}")
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, k_scale=inp.k_scale,
+                                   v_scale=inp.v_scale)
+    rng = np.random.default_rng(5)
+    sink = (rng.standard_normal(Hq) * 3.0).astype(np.float32)
+    gate = W.f32_to_bf16_bits((rng.standard_normal((B, C, Hq, D)) * 2.0).astype(np.float32))
+    blk = hs2.HybridBlock(B, C, Hq, w.n_kv_heads, D, inp.K.shape[2], w.k, w.window)
+    K, V = torch.from_numpy(inp.K).cuda(), torch.from_numpy(inp.V).cuda()
+    sc = (torch.from_numpy(inp.k_scale).cuda(), torch.from_numpy(inp.v_scale).cuda())
+    lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
+    got = blk.sparse(dev_bf16(inp.q_sa[0]), K, V, lens, torch.from_numpy(ref["idx"]).cuda(),
+                     sink=torch.from_numpy(sink).cuda(), gate=dev_bf16(gate), kv_scales=sc)
+    torch.cuda.synchronize()
+    want = O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"], sink=sink, gate=gate, k_scale=inp.k_scale,
+                              v_scale=inp.v_scale)
+    CK.check_out(CK.bf16_bits_to_f64(host_bits(got)), want, "FP8 sparse layer with sink and gate")
+
+
+SAME = [  # (workload, FA split, score split): one row tile, two, and four
+    (SMALL[0], 512, 1024),
+    (SMALL[3], 1024, 1024),
+    (W.Workload("fp8_same_32q1kv", 2, 3000, 2, 32, 1, 128, 300, 40, 1, ctx_min=1200), 768, 512),
+]
+
+
+@pytest.mark.parametrize("w,fa_split,pool_split", SAME, ids=[s[0].name for s in SAME])
+def test_fp8_equals_bf16_on_the_dequantised_cache(w, fa_split, pool_split, monkeypatch):
+    """Power-of-two scales: the bf16 cache of the dequantised values is
+    exactly the same cache, so both entry points give identical bits."""
+    from paper_2609_26368_amd import hs2
+    monkeypatch.setenv("HS2_FA_SPLIT", str(fa_split))
+    monkeypatch.setenv("HS2_POOL_SPLIT", str(pool_split))
+    inp = W.make_inputs(w, seed=13, kv="fp8")
+    B, C, Hq, Hkv, D, L = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim, inp.K.shape[2]
+    ks = np.array([2.0 ** -(3 + g % 3) for g in range(Hkv)], dtype=np.float32)
+    vs = np.array([2.0 ** -(2 + g % 2) for g in range(Hkv)], dtype=np.float32)
+    Kb = W.f32_to_bf16_bits((O.e4m3_to_f64(inp.K) * ks[None, :, None, None]).astype(np.float32))
+    Vb = W.f32_to_bf16_bits((O.e4m3_to_f64(inp.V) * vs[None, :, None, None]).astype(np.float32))
+    note(f"[fp8 = bf16] {w.name} lens={inp.lens.tolist()}")
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, L, w.k, w.window)
+    lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
+    q, qs = dev_bf16(inp.q_fa), dev_bf16(inp.q_sa[0])
+    K8, V8 = torch.from_numpy(inp.K).cuda(), torch.from_numpy(inp.V).cuda()
+    sc = (torch.from_numpy(ks).cuda(), torch.from_numpy(vs).cuda())
+    Kd, Vd = dev_bf16(Kb), dev_bf16(Vb)
+    stats8 = torch.empty((B, C, Hq, 2), dtype=torch.float32, device="cuda")
+    statsb = torch.empty_like(stats8)
+    sc8 = torch.zeros((B, Hkv, C, L), dtype=torch.float32, device="cuda")
+    scb = torch.zeros_like(sc8)
+    out8, idx8 = blk.full(q, K8, V8, lens, stats=stats8, scores=sc8, kv_scales=sc)
+    out8, idx8 = out8.clone(), idx8.clone()
+    outb, idxb = blk.full(q, Kd, Vd, lens, stats=statsb, scores=scb)
+    sa8 = blk.sparse(qs, K8, V8, lens, idxb, kv_scales=sc).clone()
+    sab = blk.sparse(qs, Kd, Vd, lens, idxb)
+    torch.cuda.synchronize()
+    assert torch.equal(idx8, idxb), "selection"
+    assert torch.equal(out8.view(torch.int16), outb.view(torch.int16)), "full-attention output"
+    assert torch.equal(stats8, statsb), "stats"
+    # candidate scores [0, N) of each row are specified; later entries are not
+    for b in range(B):
+        for c in range(C):
+            n = max(0, int(inp.lens[b]) - C + c - w.window + 1)
+            assert torch.equal(sc8[b, :, c, :n], scb[b, :, c, :n]), ("scores", b, c)
+    assert torch.equal(sa8.view(torch.int16), sab.view(torch.int16)), "sparse layer"

@@ -40,6 +40,14 @@ def note(msg: str):
     sys.stdout.flush()
 
 
+def dev_cache(inp):
+    """K, V on the device and the scales of an E4M3 cache (None for bf16)."""
+    if inp.k_scale is None:
+        return dev_bf16(inp.K), dev_bf16(inp.V), None
+    return (torch.from_numpy(inp.K).cuda(), torch.from_numpy(inp.V).cuda(),
+            (torch.from_numpy(inp.k_scale).cuda(), torch.from_numpy(inp.v_scale).cuda()))
+
+
 def run_gpu(inp, oracle_idx=None):
     """Hybrid block on the GPU; returns host copies of every result."""
     hs2 = _hs2()
@@ -47,19 +55,19 @@ def run_gpu(inp, oracle_idx=None):
     B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
     Lmax = inp.K.shape[2]
     blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window)
-    K, V = dev_bf16(inp.K), dev_bf16(inp.V)
+    K, V, sc = dev_cache(inp)
     lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
     stats = torch.empty((B, C, Hq, 2), dtype=torch.float32, device="cuda")
     scores = torch.zeros((B, Hkv, C, Lmax), dtype=torch.float32, device="cuda")
     q_fa = dev_bf16(inp.q_fa)
     # with the scores and statistics requested, then the plain call (scores in the workspace)
-    out_s, idx_s = blk.full(q_fa, K, V, lens, stats=stats, scores=scores)
-    out, idx = blk.full(q_fa, K, V, lens)
-    sa = [blk.sparse(dev_bf16(qs), K, V, lens, idx) for qs in inp.q_sa]
+    out_s, idx_s = blk.full(q_fa, K, V, lens, stats=stats, scores=scores, kv_scales=sc)
+    out, idx = blk.full(q_fa, K, V, lens, kv_scales=sc)
+    sa = [blk.sparse(dev_bf16(qs), K, V, lens, idx, kv_scales=sc) for qs in inp.q_sa]
     sa_ref_idx = None
     if oracle_idx is not None:
         ridx = torch.from_numpy(oracle_idx).cuda()
-        sa_ref_idx = [blk.sparse(dev_bf16(qs), K, V, lens, ridx) for qs in inp.q_sa]
+        sa_ref_idx = [blk.sparse(dev_bf16(qs), K, V, lens, ridx, kv_scales=sc) for qs in inp.q_sa]
     torch.cuda.synchronize()
     res = {"out": CK.bf16_bits_to_f64(host_bits(out)), "idx": idx.cpu().numpy(), "stats": stats.cpu().numpy(),
            "scores": scores.cpu().numpy(), "sa": [CK.bf16_bits_to_f64(host_bits(t)) for t in sa],
@@ -88,18 +96,20 @@ def compare(inp, ref, gpu, groups=None):
     assert np.array_equal(gpu["idx_with_scores"], gpu["idx"]), "selection depends on where the scores are kept"
     assert np.array_equal(gpu["out_with_scores"], gpu["out"]), "full-attention output depends on the score request"
     for li, qs in enumerate(inp.q_sa):
-        ref_sa = O.sparse_attention(qs, inp.K, inp.V, ref["idx"], groups=groups)
+        ref_sa = O.sparse_attention(qs, inp.K, inp.V, ref["idx"], groups=groups, k_scale=inp.k_scale,
+                                    v_scale=inp.v_scale)
         CK.check_out(gpu["sa_ref_idx"][li], ref_sa, f"sparse layer {li} (oracle selection)", rows)
         if r_idx["swaps"] == 0:
             CK.check_out(gpu["sa"][li], ref_sa, f"sparse layer {li} (own selection)", rows)
     return {**r_out, **r_sc, **r_idx}
 
 
-def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None):
-    inp = W.make_inputs(w, seed=seed, lmax=lmax)
-    note(f"[parity] {w.name} seed={seed} lens={inp.lens.tolist()} C={w.n_queries} Hq={w.n_q_heads} "
+def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None, kv="bf16"):
+    inp = W.make_inputs(w, seed=seed, lmax=lmax, kv=kv)
+    note(f"[parity] {w.name} kv={kv} seed={seed} lens={inp.lens.tolist()} C={w.n_queries} Hq={w.n_q_heads} "
          f"Hkv={w.n_kv_heads} k={w.k} W={w.window}")
-    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, groups=groups)
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, groups=groups,
+                                   k_scale=inp.k_scale, v_scale=inp.v_scale)
     gpu = run_gpu(inp, oracle_idx=ref["idx"])
     r = compare(inp, ref, gpu, groups)
     note(f"[parity] {w.name}: {r}")
