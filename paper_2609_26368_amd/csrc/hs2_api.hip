@@ -21,7 +21,6 @@ namespace {
 
 using namespace hs2;
 
-constexpr int kHeadDim = 128;
 constexpr int kMaxQueries = 16;
 constexpr int kMaxRows = 128;           // C * Gp
 constexpr int kMaxGroup = 64;
@@ -90,12 +89,16 @@ hs2_status check_dims(const hs2_dims* d) {
   if (d->n_q_heads % d->n_kv_heads)
     return fail(HS2_ERR_SHAPE, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", d->n_q_heads, d->n_kv_heads);
   if (d->max_len < 1 || d->max_len > kMaxLen) return fail(HS2_ERR_SHAPE, "max_len must be in [1, 2^27]");
-  if (d->head_dim != kHeadDim) return fail(HS2_ERR_UNSUPPORTED, "head_dim %d not supported (only 128)", d->head_dim);
+  if (d->head_dim != 128 && d->head_dim != 256)
+    return fail(HS2_ERR_UNSUPPORTED, "head_dim %d not supported (128 or 256)", d->head_dim);
   const int G = d->n_q_heads / d->n_kv_heads;
   if (G > kMaxGroup) return fail(HS2_ERR_UNSUPPORTED, "query heads per KV head %d > %d", G, kMaxGroup);
   if (d->n_queries * next_pow2(G) > kMaxRows)
     return fail(HS2_ERR_UNSUPPORTED, "n_queries * pow2(G) = %d exceeds %d query rows per KV head",
                 d->n_queries * next_pow2(G), kMaxRows);
+  if (d->head_dim == 256 && d->n_queries * next_pow2(G) > 64)
+    return fail(HS2_ERR_UNSUPPORTED, "head_dim 256: n_queries * pow2(G) = %d exceeds 64 query rows per KV head",
+                d->n_queries * next_pow2(G));
   if (d->kv_stride_t < d->head_dim || d->kv_stride_t % 8 || d->kv_stride_h < 0 || d->kv_stride_h % 8 ||
       d->kv_stride_b < 0 || d->kv_stride_b % 8)
     return fail(HS2_ERR_ALIGN, "KV strides must be non-negative multiples of 8 elements, kv_stride_t >= head_dim");
@@ -123,7 +126,7 @@ size_t carve(size_t& cur, size_t bytes) {
 struct DeviceInfo {
   int cus = 256;
   int fa_wgs[2][4][kFaVariants] = {};  // [E4M3 cache][log2 RT][variant]; 0 = unknown
-  int pool_wgs[2][4][7][17] = {};      // k_pool: [E4M3 cache][log2 RT][log2 Gp][C]; 0 = unknown
+  int pool_wgs[2][2][4][7][17] = {};   // k_pool: [head dim 256][E4M3 cache][log2 RT][log2 Gp][C]; 0 = unknown
 };
 
 int ilog2(int v) {
@@ -135,8 +138,8 @@ int ilog2(int v) {
 // Measured on MI355X with one-round splits: 32-token tiles in 3 stages for
 // one row tile; 16-token tiles in 3 stages and two token groups merged in
 // LDS (half the split partials) for two and four; the workgroup kernel for
-// eight.
-int default_fa_variant(int RT) { return RT >= 8 ? 1 : RT == 1 ? 2 : 5; }
+// eight.  Head dim 256: one row tile per wave, 16-token tiles in 3 stages.
+int default_fa_variant(int RT, int hd) { return hd == 256 ? 6 : RT >= 8 ? 1 : RT == 1 ? 2 : 5; }
 
 // kv8: the cache is E4M3 (ring kernels only)
 void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const DeviceInfo* di, bool kv8 = false) {
@@ -156,10 +159,10 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   p.c2 = (float)(scale * 1.4426950408889634);
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
-  p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT));
-  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || !fa_variant_exists(p.RT, p.fa_variant) ||
+  p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT, p.D));
+  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || fa_variant_head_dim(p.RT, p.fa_variant) != p.D ||
       (kv8 && p.fa_variant == 1))
-    p.fa_variant = default_fa_variant(p.RT);
+    p.fa_variant = default_fa_variant(p.RT, p.D);
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
   p.rows = p.units * p.C;
@@ -178,7 +181,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   p.fa_nsplit = (int)cdiv(p.Lmax, split);
   // score pass over K: the same one-round rule for its own kernel; at most
   // 32768 tokens per split (16-bit histogram counters in LDS)
-  const int pool_cu = di && p.C <= 16 ? di->pool_wgs[kv8][lrt][ilog2(p.Gp)][p.C] : 0;
+  const int pool_cu = di && p.C <= 16 ? di->pool_wgs[p.D == 256][kv8][lrt][ilog2(p.Gp)][p.C] : 0;
   const int64_t pslots = (int64_t)(di ? di->cus : 256) * (pool_cu > 0 ? pool_cu : 4);
   int psplit = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, std::max<int64_t>(1, pslots / p.units)), 64));
   psplit = env_int("HS2_POOL_SPLIT", psplit);
@@ -198,7 +201,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int64_t prow = 16 * p.RT;
   const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
   size_t cur = 0;
-  p.off_part_o = carve(cur, sizeof(float) * p.units * nslot * prow * kHeadDim);
+  p.off_part_o = carve(cur, sizeof(float) * p.units * nslot * prow * p.D);
   p.off_part_ml = carve(cur, sizeof(float) * p.units * nslot * prow * 4);
   p.off_stats = carve(cur, sizeof(float) * (size_t)p.B * p.C * p.Hq * 2);
   p.off_scores = carve(cur, sizeof(float) * p.rows * p.score_stride);
@@ -223,7 +226,7 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
   s.nsplit = (int)cdiv(n_slots, split);
   const int64_t prow = 16 * s.RT;
   size_t cur = 0;
-  s.off_part_o = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * kHeadDim);
+  s.off_part_o = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * p.D);
   s.off_part_ml = carve(cur, sizeof(float) * p.rows * s.nsplit * s.TG * prow * 4);
   s.bytes = (size_t)round_up((int64_t)cur, kAlign);
 }
@@ -280,10 +283,12 @@ hs2_status ensure_device_init(const DeviceInfo** info) {
         for (int v = 0; v < kFaVariants; ++v)
           if ((e = fa_wgs_per_cu(1 << l, v, f == 1, &di.fa_wgs[f][l][v])) != hipSuccess)
             return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
-        for (int lg = 0; lg < 7; ++lg)
-          for (int c = 1; c <= 16; ++c)
-            if ((e = pool_wgs_per_cu(1 << l, 1 << lg, c, f == 1, &di.pool_wgs[f][l][lg][c])) != hipSuccess)
-              return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
+        for (int h = 0; h < 2; ++h)
+          for (int lg = 0; lg < 7; ++lg)
+            for (int c = 1; c <= 16; ++c)
+              if ((e = pool_wgs_per_cu(1 << l, 1 << lg, c, f == 1, h ? 256 : 128, &di.pool_wgs[h][f][l][lg][c])) !=
+                  hipSuccess)
+                return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
       }
     g_dev[dev] = di;
     g_dev_done[dev] = true;
@@ -466,6 +471,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   ca.sa_mode = 0;
   // the histogram and the per-row counters (contiguous) start at zero
   ca.v_scale = v_scale;
+  ca.hd = p.D;
   ca.clear = (uint4*)(ws + p.off_hist);
   ca.n_clear = (int64_t)(p.off_state - p.off_hist + sizeof(int32_t) * p.rows * 8) / 16;
   HS2_TRY_LAUNCH(KK_COMBINE, s, launch_combine(ca, std::min(16 * p.RT, p.C * p.Gp), p.units, s));
@@ -474,6 +480,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   pa.q = q;
   pa.K = (const uint16_t*)K;
   pa.k_scale = k_scale;
+  pa.hd = p.D;
   pa.len = len;
   pa.stats_log2 = stats_log2;
   pa.scores = sc;
@@ -586,6 +593,7 @@ hs2_status sparse_impl(const hs2_dims* dims, const uint16_t* q, const void* K, c
   a.K = (const uint16_t*)K;
   a.V = (const uint16_t*)V;
   a.k_scale = k_scale;
+  a.hd = p.D;
   a.len = len;
   a.idx = idx;
   a.part_o = (float*)(ws + sp.off_part_o);
@@ -628,6 +636,7 @@ hs2_status sparse_impl(const hs2_dims* dims, const uint16_t* q, const void* K, c
   ca.sink = sink;
   ca.gate = gate;
   ca.v_scale = v_scale;
+  ca.hd = p.D;
   HS2_TRY_LAUNCH(KK_SA_COMBINE, s, launch_combine(ca, p.G, p.rows, s));
   return HS2_OK;
 }

@@ -21,7 +21,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int HD = 128;         // head dim served by these kernels
+constexpr int HD = 128;         // head dim of the workgroup kernel; the ring kernels take theirs as a parameter
 constexpr int TILE = 64;        // cache rows per LDS stage
 constexpr int NT = 256;         // threads per workgroup
 constexpr int KPAD = HD + 8;    // K / Q row stride in LDS (bf16): 272 B, conflict-free 16-B reads
@@ -152,12 +152,13 @@ __device__ inline float max_xor32(float x) { const float2 p = lane_pair32(x); re
 __device__ inline float sum_xor16(float x) { const float2 p = lane_pair16(x); return p.x + p.y; }
 __device__ inline float sum_xor32(float x) { const float2 p = lane_pair32(x); return p.x + p.y; }
 
-template <int RPW>
+template <int RPW, int HDIM = HD>
 struct WaveState {
+  static constexpr int NBC = HDIM / 16;  // 16-column blocks of O
   float m[RPW];   // reference maximum the probabilities are taken against
   float mt[RPW];  // true running maximum (for the reported statistics)
   float l[RPW];
-  f32x4 o[RPW][8];
+  f32x4 o[RPW][NBC];
   __device__ inline void init() {
 #pragma unroll
     for (int r = 0; r < RPW; ++r) {
@@ -165,7 +166,7 @@ struct WaveState {
       mt[r] = -INFINITY;
       l[r] = 0.f;
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) o[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int nb = 0; nb < NBC; ++nb) o[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
 };
@@ -194,8 +195,9 @@ __device__ inline void qk_block(const TileLds& s, int blk, const uint4 (&q)[RPW]
 // accumulators are rescaled rarely; the true maximum is tracked in mt.
 constexpr float LAZY_MARGIN = 8.f;
 
-template <int RPW, int BPW>
-__device__ inline void online_softmax(WaveState<RPW>& st, f32x4 (&S)[BPW][RPW], uint2 (&pa)[BPW][RPW], int lane) {
+template <int RPW, int BPW, int HDIM>
+__device__ inline void online_softmax(WaveState<RPW, HDIM>& st, f32x4 (&S)[BPW][RPW], uint2 (&pa)[BPW][RPW],
+                                      int lane) {
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     float mx = -INFINITY;
@@ -213,7 +215,7 @@ __device__ inline void online_softmax(WaveState<RPW>& st, f32x4 (&S)[BPW][RPW], 
 #pragma unroll
       for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * (lane >> 4) + i);
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb)
+      for (int nb = 0; nb < WaveState<RPW, HDIM>::NBC; ++nb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) st.o[rr][nb][i] *= a4[i];
     }
@@ -252,9 +254,10 @@ __device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const in
   }
 }
 
-// Write one wave's partial for its RPW row tiles: (m ref, l, m true, 0) and O.
-template <int RPW>
-__device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict__ part_o,
+// Write one wave's partial for its RPW row tiles: (m ref, l, m true, 0) and O
+// (rows of HDIM floats).
+template <int RPW, int HDIM>
+__device__ inline void store_partial(const WaveState<RPW, HDIM>& st, float* __restrict__ part_o,
                                      float* __restrict__ part_ml, int64_t slot_base_row, int rt0, int lane) {
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
@@ -264,9 +267,9 @@ __device__ inline void store_partial(const WaveState<RPW>& st, float* __restrict
     if (lane < 16) *(float4*)(part_ml + (row0 + lane) * 4) = make_float4(st.m[rr], l, st.mt[rr], 0.f);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float* dst = part_o + (row0 + 4 * (lane >> 4) + i) * HD + (lane & 15);
+      float* dst = part_o + (row0 + 4 * (lane >> 4) + i) * HDIM + (lane & 15);
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) dst[16 * nb] = st.o[rr][nb][i];
+      for (int nb = 0; nb < WaveState<RPW, HDIM>::NBC; ++nb) dst[16 * nb] = st.o[rr][nb][i];
     }
   }
 }
@@ -341,19 +344,21 @@ __device__ inline void wait_stage_loads(int tiles) {
   }
 }
 
-template <int RPW>
-__device__ inline void qk_block_swz(const unsigned char* stg, int blk, const uint4 (&q)[RPW][4], f32x4 (&S)[RPW],
+// Logits S^T = K . Q^T of the 16 staged rows of block blk; rows of 64 NKK
+// bytes (head dim 32 NKK), swizzled chunks.
+template <int RPW, int NKK>
+__device__ inline void qk_block_swz(const unsigned char* stg, int blk, const uint4 (&q)[RPW][NKK], f32x4 (&S)[RPW],
                                     int lane) {
   const int row = 16 * blk + (lane & 15);
-  const unsigned char* rp = stg + row * STAGE_ROW_BYTES;
-  uint4 a4[4];
+  const unsigned char* rp = stg + row * (64 * NKK);
+  uint4 a4[NKK];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) a4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+  for (int kk = 0; kk < NKK; ++kk) a4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(a4[kk], q[rr][kk], acc);
+    for (int kk = 0; kk < NKK; ++kk) acc = mfma_k32(a4[kk], q[rr][kk], acc);
     S[rr] = acc;
   }
 }
@@ -394,8 +399,8 @@ __device__ inline void softmax_pv_swz(WaveState<RPW>& st, const unsigned char* s
 constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
 // ---------------------------------------------------------------- FP8 cache rows
-// An FP8 (OCP E4M3) cache row is 128 bytes.  Rows are staged raw (row-major,
-// 128 B each) by the same 16-byte direct LDS loads -- a 1 KB load covers 8
+// An FP8 (OCP E4M3) cache row is HDIM bytes.  Rows are staged raw (row-major)
+// by the same 16-byte direct LDS loads -- a 1 KB load covers 1024 / HDIM
 // rows -- and converted into the bf16 stage layout above, so every bf16
 // operand read is shared by both cache formats.
 
@@ -409,21 +414,22 @@ __device__ inline uint2 e4m3x4_to_bf16x4(uint32_t w) {
   return make_uint2(lo, hi);
 }
 
-// Convert NR staged E4M3 rows (raw, 128 B each) into bf16 stage rows at stg
-// (chunk c of row r at position c ^ (r & 15)); threads tid of NTHR.  A job is
-// one 16-byte raw piece: 16 values, two bf16 chunks.
-template <int NR, int NTHR>
+// Convert NR staged E4M3 rows (raw, HDIM bytes each) into bf16 stage rows at
+// stg (2 HDIM bytes; chunk c of row r at position c ^ (r & 15)); threads tid
+// of NTHR.  A job is one 16-byte raw piece: 16 values, two bf16 chunks.
+template <int NR, int NTHR, int HDIM = HD>
 __device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
-  constexpr int JOBS = NR * 8;
+  constexpr int PPR = HDIM / 16;  // raw pieces per row
+  constexpr int JOBS = NR * PPR;
 #pragma unroll
   for (int k = 0; k < (JOBS + NTHR - 1) / NTHR; ++k) {
     const int j = tid + k * NTHR;
     if (JOBS % NTHR == 0 || j < JOBS) {
-      const int r = j >> 3, p = j & 7;
-      const uint4 v = *(const uint4*)(raw + r * 128 + 16 * p);
+      const int r = j / PPR, p = j % PPR;
+      const uint4 v = *(const uint4*)(raw + r * HDIM + 16 * p);
       const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
       const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
-      unsigned char* rp = stg + r * STAGE_ROW_BYTES;
+      unsigned char* rp = stg + r * (2 * HDIM);
       *(uint4*)(rp + 16 * ((2 * p) ^ (r & 15))) = make_uint4(a.x, a.y, b.x, b.y);
       *(uint4*)(rp + 16 * ((2 * p + 1) ^ (r & 15))) = make_uint4(c.x, c.y, d.x, d.y);
     }
@@ -447,13 +453,14 @@ __device__ inline void wait_ring(int stages) {
 }
 
 // V operand of P.V for block blk, columns 16 nb .. 16 nb + 15, read
-// transposed from the row-major swizzled V rows at `vbase`.
+// transposed from the row-major swizzled V rows (2 HDIM bytes) at `vbase`.
+template <int HDIM = HD>
 __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int nb, int lane) {
   const int kq = lane & 15;
   const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
   const int col = 16 * nb + 4 * (kq & 3);
   const int pos = (col >> 3) ^ (row & 15);
-  const unsigned char* p = vbase + row * STAGE_ROW_BYTES + 16 * pos + 2 * (col & 7);
+  const unsigned char* p = vbase + row * (2 * HDIM) + 16 * pos + 2 * (col & 7);
   const i16x4_lds v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_lds*)(p));
   return __builtin_bit_cast(uint2, v);
 }

@@ -26,18 +26,20 @@ __device__ inline int clamp_len(const int32_t* len, int b, int max_len) {
   return L < 0 ? 0 : (L > max_len ? max_len : L);
 }
 
-// Load B operands (Q^T) of query row tile rt for this lane: row 16 rt + (lane & 15).
-__device__ inline void load_q_tile(uint4 (&q)[4], const uint16_t* __restrict__ qbase, int rt, int lane, int Gp,
+// Load B operands (Q^T) of query row tile rt for this lane: row 16 rt + (lane & 15)
+// (head dim 32 NKK).
+template <int NKK>
+__device__ inline void load_q_tile(uint4 (&q)[NKK], const uint16_t* __restrict__ qbase, int rt, int lane, int Gp,
                                    int G, int C, int Hq, int g, int b) {
   const int r = 16 * rt + (lane & 15);
   const int c = r / Gp, h = r % Gp;
   if (c < C && h < G) {
-    const uint16_t* p = qbase + (((int64_t)b * C + c) * Hq + g * G + h) * HD + 8 * (lane >> 4);
+    const uint16_t* p = qbase + (((int64_t)b * C + c) * Hq + g * G + h) * (32 * NKK) + 8 * (lane >> 4);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) q[kk] = *(const uint4*)(p + 32 * kk);
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const uint4*)(p + 32 * kk);
   } else {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) q[kk] = make_uint4(0, 0, 0, 0);
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = make_uint4(0, 0, 0, 0);
   }
 }
 
@@ -152,19 +154,22 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // KV8: the cache is E4M3 bytes with one scale per KV head (k_scale folds
 // into the logit scale, v_scale is applied by the merge); each token group
 // stages raw rows in its ring and converts the current tile into one bf16
-// tile before computing on it.
-template <int RT, int NWV, int TW, int NS, int TGW, bool KV8>
+// tile before computing on it.  HDIM: head dim (128 or 256).
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
   constexpr int NB = TW / 16;                              // 16-row blocks per stage
-  constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;          // bytes of a staged cache row
+  constexpr int NKK = HDIM / 32;                           // 32-wide k steps of the logits
+  constexpr int SRB = 2 * HDIM;                            // bytes of a bf16 stage row
+  constexpr int RB = KV8 ? HDIM : SRB;                     // bytes of a staged cache row
+  constexpr int CPR = RB / 16;                             // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;                // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * RB;                          // ring stage: K rows then V rows
-  constexpr int TB = KV8 ? 2 * TW * STAGE_ROW_BYTES : 0;   // converted bf16 tile
+  constexpr int TB = KV8 ? 2 * TW * SRB : 0;               // converted bf16 tile
   constexpr int GB = NS * SB + TB;                         // LDS of one token group
-  static_assert(LPM >= 1, "each wave loads at least one 1 KB piece per matrix and stage");
+  static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads for every wave and stage");
   static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
-  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HD * 4 <= TGW * GB,
+  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HDIM * 4 <= TGW * GB,
                 "the merge fits in the rings");
   extern __shared__ __align__(16) unsigned char smem[];
 
@@ -181,7 +186,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   const int nloop = (min(Lv, split * a.split_tokens + part) - split * a.split_tokens + TW - 1) / TW;  // group 0's
   const int rt0 = wave * RPW;
 
-  uint4 q[RPW][4];
+  uint4 q[RPW][NKK];
   int rpos[RPW];
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
@@ -209,16 +214,18 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       lrow = a.logits + (((int64_t)b * a.Hkv + g) * a.C * a.G + c * a.G + h) * a.logit_stride;
   }
 
-  // per-lane part of each load's byte offset: bf16 rows are 4 per 1 KB load,
-  // swizzled chunks; E4M3 rows are 8 per load, raw
+  // per-lane part of each load's byte offset: a 1 KB load covers RPL rows of
+  // CPR chunks (lane / CPR = row, lane % CPR = chunk slot); bf16 rows are
+  // swizzled, E4M3 rows raw
   constexpr int RPL = 1024 / RB;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * (lane & 7) : (int64_t)t * stride_t + 16 * ((lane & 15) ^ (row & 15));
+    return KV8 ? (int64_t)t * stride_t + 16 * (lane % CPR)
+               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
   };
   int64_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
-    const int row = RPL * (wave * LPM + u) + lane / (64 / RPL);
+    const int row = RPL * (wave * LPM + u) + lane / CPR;
     lane_off[u] = lane_offset(row, row);
   }
   auto issue = [&](int tile) {
@@ -231,7 +238,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       const int n = wave * LPM + u;
       int64_t off = tile_off + lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; masked below
-        const int row = RPL * n + lane / (64 / RPL);
+        const int row = RPL * n + lane / CPR;
         off = lane_offset(row, min(t0 + row, t_end - 1));
       }
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
@@ -239,7 +246,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     }
   };
 
-  WaveState<RPW> st;
+  WaveState<RPW, HDIM> st;
   st.init();
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
@@ -253,7 +260,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     if (i < ntiles && i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = ring_p + (i % NS) * SB;
     if constexpr (KV8) {
-      if (i < ntiles) convert_rows_e4m3<2 * TW, 64 * NWV>(stg, tile_p, 64 * wave + lane);
+      if (i < ntiles) convert_rows_e4m3<2 * TW, 64 * NWV, HDIM>(stg, tile_p, 64 * wave + lane);
       if (NWV * TGW > 1) __syncthreads();  // every group's tile converted
       stg = tile_p;
     }
@@ -283,12 +290,12 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         }
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
-    const unsigned char* vbase = stg + TW * STAGE_ROW_BYTES;
+    const unsigned char* vbase = stg + TW * SRB;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        const uint2 vb = v_operand_tr_at(vbase, bi, nb, lane);
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
 #pragma unroll
         for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
       }
@@ -302,7 +309,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     constexpr int ROWS = 16 * RT;
     __syncthreads();
     float* mlL = (float*)smem;              // [TGW][ROWS][4]: (m ref, l, m true, -)
-    float* oL = mlL + TGW * ROWS * 4;       // [TGW - 1][ROWS][HD]: the other groups' O
+    float* oL = mlL + TGW * ROWS * 4;       // [TGW - 1][ROWS][HDIM]: the other groups' O
 #pragma unroll
     for (int rr = 0; rr < RPW; ++rr) {
       const float l = sum_xor32(sum_xor16(st.l[rr]));
@@ -312,8 +319,8 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int nb = 0; nb < 8; ++nb)
-            oL[((tg - 1) * ROWS + row0 + 4 * (lane >> 4) + i) * HD + 16 * nb + (lane & 15)] = st.o[rr][nb][i];
+          for (int nb = 0; nb < HDIM / 16; ++nb)
+            oL[((tg - 1) * ROWS + row0 + 4 * (lane >> 4) + i) * HDIM + 16 * nb + (lane & 15)] = st.o[rr][nb][i];
     }
     __syncthreads();
     if (tg > 0) return;
@@ -348,12 +355,12 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         const int R = row0 + 4 * (lane >> 4) + i;
         float f[TGW], M;
         weights(R, f, M);
-        float* dst = a.part_o + (slot_base_row + R) * HD + (lane & 15);
+        float* dst = a.part_o + (slot_base_row + R) * HDIM + (lane & 15);
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
+        for (int nb = 0; nb < HDIM / 16; ++nb) {
           float o = st.o[rr][nb][i] * f[0];
 #pragma unroll
-          for (int j = 1; j < TGW; ++j) o += oL[((j - 1) * ROWS + R) * HD + 16 * nb + (lane & 15)] * f[j];
+          for (int j = 1; j < TGW; ++j) o += oL[((j - 1) * ROWS + R) * HDIM + 16 * nb + (lane & 15)] * f[j];
           dst[16 * nb] = o;
         }
       }
@@ -362,17 +369,20 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
 }
 
 // ============================================================================ combine
-// grid (rows_per_unit, units), 256 threads = 8 slot groups x 32 column quads.
+// grid (rows_per_unit, units), 256 threads = 256 / NQ slot groups x NQ =
+// HDIM / 4 column quads.
 // FA: unit = (b, g), row r = c * Gp + h; slots valid = ceil(Lv / split) * TG.
 // SA: unit = (b, g, c), row = h; all n_split * TG slots written.
+template <int HDIM>
 __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
+  constexpr int NQ = HDIM / 4, SG = 256 / NQ;
   __shared__ float s_wmax[8];
-  __shared__ float s_z[8];
-  __shared__ float4 s_o[8][32];
+  __shared__ float s_z[SG];
+  __shared__ float4 s_o[SG][NQ];
   const int r = blockIdx.x;
   const int64_t unit = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sg = tid >> 5, dq = tid & 31;
+  const int sg = tid / NQ, dq = tid % NQ;
   if (a.clear) {  // zero the selection histogram and counters for the kernels that follow
     const int64_t nb = (int64_t)gridDim.x * gridDim.y, bid = unit * gridDim.x + r;
     for (int64_t i = bid * 256 + tid; i < a.n_clear; i += nb * 256) a.clear[i] = make_uint4(0, 0, 0, 0);
@@ -422,13 +432,13 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   float z = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (M != -INFINITY) {
-    for (int s = sg; s < nvalid; s += 8) {
+    for (int s = sg; s < nvalid; s += SG) {
       const int64_t pr = base + (int64_t)s * a.rows;
       const float m = a.part_ml[pr * 4];
       if (m == -INFINITY) continue;
       const float w = fast_exp2(m - M);
       z += a.part_ml[pr * 4 + 1] * w;
-      const float4 o = *(const float4*)(a.part_o + pr * HD + 4 * dq);
+      const float4 o = *(const float4*)(a.part_o + pr * HDIM + 4 * dq);
       acc.x += o.x * w;
       acc.y += o.y * w;
       acc.z += o.z * w;
@@ -442,7 +452,7 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   float Z = 0.f;
   float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
+  for (int j = 0; j < SG; ++j) {
     Z += s_z[j];
     o.x += s_o[j][dq].x;
     o.y += s_o[j][dq].y;
@@ -456,7 +466,7 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   o.z *= inv;
   o.w *= inv;
   if (a.gate) {  // out *= sigmoid(gate), elementwise
-    const uint2 gb = *(const uint2*)(a.gate + orow * HD + 4 * dq);
+    const uint2 gb = *(const uint2*)(a.gate + orow * HDIM + 4 * dq);
     const float gv[4] = {bf16_bits_to_f32(gb.x & 0xFFFFu), bf16_bits_to_f32(gb.x >> 16), bf16_bits_to_f32(gb.y & 0xFFFFu),
                          bf16_bits_to_f32(gb.y >> 16)};
     float gsig[4];
@@ -470,7 +480,7 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   uint2 packed;
   packed.x = f32_to_bf16_bits(o.x) | (f32_to_bf16_bits(o.y) << 16);
   packed.y = f32_to_bf16_bits(o.z) | (f32_to_bf16_bits(o.w) << 16);
-  *(uint2*)(a.out + orow * HD + 4 * dq) = packed;
+  *(uint2*)(a.out + orow * HDIM + 4 * dq) = packed;
   if (dq == 0) {
     if (a.stats_log2) {
       a.stats_log2[orow * 2] = M;
@@ -578,24 +588,30 @@ __device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g,
 // own query row tiles held in registers.  Dynamic LDS: ring + C packed
 // first-level histograms (16-bit counters; a split has < 65536 tokens).
 // KV8: E4M3 cache with one K scale per KV head (folded into the logit
-// scale); raw rows are staged and converted like in k_fa_ring.
-template <int RT, int GP, bool KV8 = false>
+// scale); raw rows are staged and converted like in k_fa_ring.  HDIM: head
+// dim (128 or 256).
+template <int RT, int GP, bool KV8 = false, int HDIM = HD>
 struct PoolShape {
   static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
   static constexpr int RPW = RT == 1 ? 1 : (TPQ > 2 ? TPQ : 2);  // row tiles per wave
   static constexpr int NWV = RT / RPW;
-  static constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;      // bytes of a staged row
-  // whole 1 KB loads for every wave: E4M3 tiles of 8 NWV rows when that is more than 16
-  static constexpr int TW = (KV8 && 8 * NWV > 16) ? 8 * NWV : 16, NS = 4;
+  static constexpr int SRB = 2 * HDIM;                        // bytes of a bf16 stage row
+  static constexpr int RB = KV8 ? HDIM : SRB;                 // bytes of a staged row
+  static constexpr int RPL = 1024 / RB;                       // rows per 1 KB load
+  // whole 1 KB loads for every wave: at least 16 rows, RPL NWV when more
+  static constexpr int TW = RPL * NWV > 16 ? RPL * NWV : 16;
+  static constexpr int NS = HDIM > 128 ? 3 : 4;
   static constexpr int SB = TW * RB;                          // ring stage
-  static constexpr int TB = KV8 ? TW * STAGE_ROW_BYTES : 0;   // converted tile
+  static constexpr int TB = KV8 ? TW * SRB : 0;               // converted tile
   static constexpr int LDS = NS * SB + TB;                    // before the histograms
 };
-template <int RT, int GP, bool KV8>
+template <int RT, int GP, bool KV8, int HDIM>
 __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
-  using PS = PoolShape<RT, GP, KV8>;
-  constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB, RB = PS::RB;
+  using PS = PoolShape<RT, GP, KV8, HDIM>;
+  constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB, RB = PS::RB, SRB = PS::SRB;
   constexpr int NB = TW / 16;
+  constexpr int NKK = HDIM / 32;
+  constexpr int CPR = RB / 16;               // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;  // 1 KB loads per stage per wave
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
@@ -614,7 +630,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   const int rt0 = wave * RPW;
 
   for (int i = tid; i < a.C * (NBINS / 2); i += 64 * NWV) hist[i] = 0;
-  uint4 q[RPW][4];
+  uint4 q[RPW][NKK];
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) load_q_tile(q[rr], a.q, rt0 + rr, lane, GP, a.G, a.C, a.Hq, g, b);
   float fac[RPW][4], msub[RPW][4];
@@ -625,14 +641,15 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   const int64_t stride_t = a.stride_t * ESZ;
   const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem);
-  constexpr int RPL = 1024 / RB;  // rows per 1 KB load
+  constexpr int RPL = PS::RPL;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * (lane & 7) : (int64_t)t * stride_t + 16 * ((lane & 15) ^ (row & 15));
+    return KV8 ? (int64_t)t * stride_t + 16 * (lane % CPR)
+               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
   };
   int64_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
-    const int row = RPL * (wave * LPM + u) + lane / (64 / RPL);
+    const int row = RPL * (wave * LPM + u) + lane / CPR;
     lane_off[u] = lane_offset(row, row);
   }
   auto issue = [&](int tile) {
@@ -645,7 +662,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
       const int n = wave * LPM + u;
       int64_t off = tile_off + lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; never emitted
-        const int row = RPL * n + lane / (64 / RPL);
+        const int row = RPL * n + lane / CPR;
         off = lane_offset(row, min(t0 + row, t_end - 1));
       }
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
@@ -673,7 +690,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = smem + (i % NS) * SB;
     if constexpr (KV8) {
-      convert_rows_e4m3<TW, 64 * NWV>(stg, tile_p, tid);
+      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_p, tid);
       if (NWV > 1) __syncthreads();
       stg = tile_p;
     }
@@ -681,16 +698,16 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
       const int row = 16 * bi + (lane & 15);
-      const unsigned char* rp = stg + row * STAGE_ROW_BYTES;
-      uint4 k4[4];
+      const unsigned char* rp = stg + row * SRB;
+      uint4 k4[NKK];
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+      for (int kk = 0; kk < NKK; ++kk) k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
       f32x4 acc[RPW];
 #pragma unroll
       for (int rr = 0; rr < RPW; ++rr) {
         acc[rr] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
+        for (int kk = 0; kk < NKK; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
       }
       pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
     }
@@ -1100,15 +1117,18 @@ __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
 // entries are staged in LDS first; each stage then gathers its rows straight
 // into the ring (per-lane addresses), invalid entries (< 0 or >= len) read
 // row 0 and are masked out of the softmax.
-template <int RT, int NWV, int TW, int NS, bool KV8>
+template <int RT, int NWV, int TW, int NS, bool KV8, int HDIM>
 __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   constexpr int RPW = RT / NWV;
   constexpr int NB = TW / 16;
-  constexpr int RB = KV8 ? 128 : STAGE_ROW_BYTES;  // bytes of a staged cache row
-  constexpr int RPL = 1024 / RB;                    // rows per 1 KB load
+  constexpr int NKK = HDIM / 32;
+  constexpr int SRB = 2 * HDIM;                 // bytes of a bf16 stage row
+  constexpr int RB = KV8 ? HDIM : SRB;          // bytes of a staged cache row
+  constexpr int RPL = 1024 / RB;                // rows per 1 KB load
+  constexpr int CPR = RB / 16;                  // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;
   constexpr int SB = 2 * TW * RB;
-  constexpr int TB = KV8 ? 2 * TW * STAGE_ROW_BYTES : 0;  // converted tile
+  constexpr int TB = KV8 ? 2 * TW * SRB : 0;    // converted tile
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
   unsigned char* tile_p = smem + NS * SB;                  // KV8: the converted tile
@@ -1132,17 +1152,17 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
     int t = i < nslots ? irow[i] : -1;
     sidx[i] = (t >= 0 && t < Lv) ? t : -1;
   }
-  uint4 q[RPW][4];
+  uint4 q[RPW][NKK];
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     const int h = 16 * (rt0 + rr) + (lane & 15);
     if (h < a.G) {
-      const uint16_t* p = a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HD + 8 * (lane >> 4);
+      const uint16_t* p = a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HDIM + 8 * (lane >> 4);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) q[rr][kk] = *(const uint4*)(p + 32 * kk);
+      for (int kk = 0; kk < NKK; ++kk) q[rr][kk] = *(const uint4*)(p + 32 * kk);
     } else {
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) q[rr][kk] = make_uint4(0, 0, 0, 0);
+      for (int kk = 0; kk < NKK; ++kk) q[rr][kk] = make_uint4(0, 0, 0, 0);
     }
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));
@@ -1163,20 +1183,20 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
-      const int row = RPL * n + lane / (64 / RPL);
+      const int row = RPL * n + lane / CPR;
       const int t = sidx[tile * TW + row];
       const int64_t off = (int64_t)(t < 0 ? 0 : t) * stride_t +
-                          (KV8 ? 16 * (lane & 7) : 16 * ((lane & 15) ^ (row & 15)));
+                          (KV8 ? 16 * (lane % CPR) : 16 * ((lane % CPR) ^ (row & 15)));
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
       dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
-      const uint64_t bal = __ballot(t >= 0);  // lanes (64 / RPL) j .. hold row RPL n + j
+      const uint64_t bal = __ballot(t >= 0);  // lanes CPR j .. hold row RPL n + j
 #pragma unroll
-      for (int j = 0; j < RPL; ++j) mask |= (uint32_t)((bal >> ((64 / RPL) * j)) & 1ull) << (RPL * n + j);
+      for (int j = 0; j < RPL; ++j) mask |= (uint32_t)((bal >> (CPR * j)) & 1ull) << (RPL * n + j);
     }
     return mask;
   };
 
-  WaveState<RPW> st;
+  WaveState<RPW, HDIM> st;
   st.init();
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
@@ -1196,14 +1216,16 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
     }
     const unsigned char* stg = smem + (i % NS) * SB;
     if constexpr (KV8) {  // converted tile complete at the barrier below (one wave: in order)
-      convert_rows_e4m3<2 * TW, 64 * NWV>(stg, tile_p, threadIdx.x);
+      convert_rows_e4m3<2 * TW, 64 * NWV, HDIM>(stg, tile_p, threadIdx.x);
       stg = tile_p;
     }
-    if (NWV > 1) {  // both waves' row bits
-      __shared__ uint32_t s_mask[2];
+    if (NWV > 1) {  // every wave's row bits
+      __shared__ uint32_t s_mask[NWV];
       if (lane == 0) s_mask[wave] = m_i;
       __syncthreads();
-      m_i = s_mask[0] | s_mask[1];
+      m_i = 0;
+#pragma unroll
+      for (int w = 0; w < NWV; ++w) m_i |= s_mask[w];
     }
     f32x4 S[NB][RPW];
 #pragma unroll
@@ -1219,12 +1241,12 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
         }
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
-    const unsigned char* vbase = stg + TW * STAGE_ROW_BYTES;
+    const unsigned char* vbase = stg + TW * SRB;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        const uint2 vb = v_operand_tr_at(vbase, bi, nb, lane);
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
 #pragma unroll
         for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
       }
@@ -1237,28 +1259,30 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 #define HS2_LAUNCH(kernel, grid, block, shmem, stream, arg) \
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
-// Full attention kernel variants (planner default 0):
-//   0: ring kernel, 16-row stages x 4, one wave (RT <= 2) or two waves (RT = 4)
-//   1: workgroup kernel (shared stages, 4 or 8 waves)
-//   2: ring kernel, 32-row stages x 3;  3: 16-row stages x 3;  4: 16 x 4, one wave
-// RT = 8 always uses the workgroup kernel.
-#define HS2_RING_VARIANTS(X)                 \
-  X(0, 1, 1, 16, 4, 1) X(0, 2, 1, 16, 4, 1) X(0, 4, 2, 16, 4, 1) \
-  X(2, 1, 1, 32, 3, 1) X(2, 2, 1, 32, 3, 1) X(2, 4, 2, 32, 3, 1) \
-  X(3, 1, 1, 16, 3, 1) X(3, 2, 1, 16, 3, 1) X(3, 4, 2, 16, 3, 1) \
-  X(5, 1, 1, 32, 3, 1) X(5, 2, 1, 16, 3, 2) X(5, 4, 2, 16, 3, 2)
+// Full attention kernel variants (the planner's defaults: head dim 128 with
+// RT = 1 -> 2, RT = 2 or 4 -> 5, RT = 8 -> 1; head dim 256 -> 6):
+//   1: workgroup kernel (64-row stages shared by 4 or 8 waves), head dim 128
+//   0, 2, 3, 5: ring kernels of head dim 128; 6: ring kernels of head dim 256
+// Columns: variant, RT, waves per token group, stage rows, stages, token
+// groups, head dim.
+#define HS2_RING_VARIANTS(X)                                                        \
+  X(0, 1, 1, 16, 4, 1, 128) X(0, 2, 1, 16, 4, 1, 128) X(0, 4, 2, 16, 4, 1, 128)     \
+  X(2, 1, 1, 32, 3, 1, 128) X(2, 2, 1, 32, 3, 1, 128) X(2, 4, 2, 32, 3, 1, 128)     \
+  X(3, 1, 1, 16, 3, 1, 128) X(3, 2, 1, 16, 3, 1, 128) X(3, 4, 2, 16, 3, 1, 128)     \
+  X(5, 1, 1, 32, 3, 1, 128) X(5, 2, 1, 16, 3, 2, 128) X(5, 4, 2, 16, 3, 2, 128)     \
+  X(6, 1, 1, 16, 3, 1, 256) X(6, 2, 2, 16, 3, 1, 256) X(6, 4, 4, 16, 3, 1, 256)
 
-bool fa_variant_exists(int RT, int variant) {
-  if (variant == 1) return RT == 1 || RT == 2 || RT == 4 || RT == 8;  // workgroup kernel
-#define HS2_RING_HAS(v, rt, nwv, tw, ns, tgw) \
-  if (variant == v && RT == rt) return true;
-  HS2_RING_VARIANTS(HS2_RING_HAS)
-#undef HS2_RING_HAS
-  return false;
+int fa_variant_head_dim(int RT, int variant) {
+  if (variant == 1) return RT == 1 || RT == 2 || RT == 4 || RT == 8 ? 128 : 0;  // workgroup kernel
+#define HS2_RING_HD(v, rt, nwv, tw, ns, tgw, hd) \
+  if (variant == v && RT == rt) return hd;
+  HS2_RING_VARIANTS(HS2_RING_HD)
+#undef HS2_RING_HD
+  return 0;
 }
 
 int fa_split_align(int RT, int variant) {
-#define HS2_RING_ALIGN(v, rt, nwv, tw, ns, tgw) \
+#define HS2_RING_ALIGN(v, rt, nwv, tw, ns, tgw, hd) \
   if (variant == v && RT == rt) return 64 * tgw;
   HS2_RING_VARIANTS(HS2_RING_ALIGN)
 #undef HS2_RING_ALIGN
@@ -1266,7 +1290,7 @@ int fa_split_align(int RT, int variant) {
 }
 
 int fa_token_groups(int RT, int variant) {
-  if (RT < 8 && variant != 1) return 1;
+  if (variant != 1) return 1;
   switch (RT) {
     case 1: return FaShape<1>::TGN;
     case 2: return FaShape<2>::TGN;
@@ -1285,22 +1309,22 @@ static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t
 }
 
 // LDS of a full-attention ring kernel: per token group the ring of raw rows
-// (bf16 256 B or E4M3 128 B) and, for E4M3, one converted bf16 tile
-constexpr size_t fa_ring_lds(int tw, int ns, int tgw, bool kv8) {
-  return (size_t)tgw * ((size_t)ns * 2 * tw * (kv8 ? 128 : STAGE_ROW_BYTES) + (kv8 ? 2 * tw * STAGE_ROW_BYTES : 0));
+// (bf16 2 hd bytes or E4M3 hd bytes) and, for E4M3, one converted bf16 tile
+constexpr size_t fa_ring_lds(int tw, int ns, int tgw, bool kv8, int hd) {
+  return (size_t)tgw * ((size_t)ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? 2 * tw * 2 * hd : 0));
 }
 
 hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
   *wgs = 0;
-#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw)                                                                   \
-  if (variant == v && RT == rt)                                                                                  \
-    return kv8 ? occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true>, 64 * nwv * tgw,        \
-                                  fa_ring_lds(tw, ns, tgw, true))                                                \
-               : occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false>, 64 * nwv * tgw,       \
-                                  fa_ring_lds(tw, ns, tgw, false));
+#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw, hd)                                                                  \
+  if (variant == v && RT == rt)                                                                                   \
+    return kv8 ? occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>, 64 * nwv * tgw,     \
+                                  fa_ring_lds(tw, ns, tgw, true, hd))                                             \
+               : occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>, 64 * nwv * tgw,    \
+                                  fa_ring_lds(tw, ns, tgw, false, hd));
   HS2_RING_VARIANTS(HS2_RING_OCC)
 #undef HS2_RING_OCC
-  if (kv8) return hipSuccess;  // E4M3 only through the ring kernels
+  if (kv8 || variant != 1) return hipSuccess;  // E4M3 only through the ring kernels
   const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
   switch (RT) {
     case 1: return occupancy_capped(wgs, (const void*)k_fa_split<1>, 64 * FaShape<1>::NW, sm);
@@ -1313,19 +1337,19 @@ hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw)                                                       \
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd)                                                   \
   if (variant == v && RT == rt) {                                                                       \
     if (a.k_scale)                                                                                      \
-      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, true>), grid, dim3(64 * nwv * tgw),                  \
-                 fa_ring_lds(tw, ns, tgw, true), s, a);                                                 \
+      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>), grid, dim3(64 * nwv * tgw),              \
+                 fa_ring_lds(tw, ns, tgw, true, hd), s, a);                                             \
     else                                                                                                \
-      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, false>), grid, dim3(64 * nwv * tgw),                 \
-                 fa_ring_lds(tw, ns, tgw, false), s, a);                                                \
+      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>), grid, dim3(64 * nwv * tgw),             \
+                 fa_ring_lds(tw, ns, tgw, false, hd), s, a);                                            \
     return hipGetLastError();                                                                          \
   }
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
 #undef HS2_RING_LAUNCH
-  if (a.k_scale) return hipErrorInvalidValue;  // E4M3 only through the ring kernels
+  if (a.k_scale || variant != 1) return hipErrorInvalidValue;  // E4M3 only through the ring kernels
   const size_t sm = (size_t)FA_STAGES * STAGE_BYTES;
   switch (RT) {
     case 1: HS2_LAUNCH(k_fa_split<1>, grid, dim3(64 * FaShape<1>::NW), sm, s, a); break;
@@ -1337,18 +1361,19 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) 
   return hipGetLastError();
 }
 
-template <int RT, int GP, bool KV8>
+template <int RT, int GP, bool KV8, int HDIM>
 size_t pool_smem_bytes(int C) {
-  return (size_t)PoolShape<RT, GP, KV8>::LDS + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
+  return (size_t)PoolShape<RT, GP, KV8, HDIM>::LDS + (size_t)C * (NBINS / 2) * sizeof(uint32_t);
 }
 
 // pool kernels for every (row tiles, padded group) pair the planner can produce:
-// RT = pow2(ceil(C * GP / 16)) with C <= 16 and C * GP <= 128
-#define HS2_POOL_CASES(X) \
+// RT = pow2(ceil(C * GP / 16)) with C <= 16 and C * GP <= 128; the E4M3 and
+// head-dim-256 kernels serve at most 64 query rows (RT <= 4)
+#define HS2_POOL_CASES_64(X)                                  \
   X(1, 1) X(1, 2) X(1, 4) X(1, 8) X(1, 16)                    \
   X(2, 1) X(2, 2) X(2, 4) X(2, 8) X(2, 16) X(2, 32)           \
-  X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)                  \
-  X(8, 8) X(8, 16) X(8, 32) X(8, 64)
+  X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)
+#define HS2_POOL_CASES_128(X) X(8, 8) X(8, 16) X(8, 32) X(8, 64)
 
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
   const int64_t chunks = ((int64_t)a.max_len + LOGIT_CHUNK - 1) / LOGIT_CHUNK;
@@ -1357,68 +1382,99 @@ hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int* wgs) {
+template <int RT, int GP, bool KV8, int HDIM>
+hipError_t pool_occupancy(int* wgs, int C) {
+  return occupancy_capped(wgs, (const void*)k_pool<RT, GP, KV8, HDIM>, 64 * PoolShape<RT, GP>::NWV,
+                          pool_smem_bytes<RT, GP, KV8, HDIM>(C));
+}
+
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int hd, int* wgs) {
   *wgs = 0;
-#define HS2_POOL_OCC(rt, gp)                                                                                  \
-  if (RT == rt && Gp == gp)                                                                                   \
-    return kv8 ? occupancy_capped(wgs, (const void*)k_pool<rt, gp, true>, 64 * PoolShape<rt, gp>::NWV,         \
-                                  pool_smem_bytes<rt, gp, true>(C))                                           \
-               : occupancy_capped(wgs, (const void*)k_pool<rt, gp, false>, 64 * PoolShape<rt, gp>::NWV,        \
-                                  pool_smem_bytes<rt, gp, false>(C));
-  HS2_POOL_CASES(HS2_POOL_OCC)
+#define HS2_POOL_OCC(rt, gp)                                                              \
+  if (RT == rt && Gp == gp) {                                                             \
+    if (hd == 256) return kv8 ? pool_occupancy<rt, gp, true, 256>(wgs, C)                 \
+                              : pool_occupancy<rt, gp, false, 256>(wgs, C);               \
+    return kv8 ? pool_occupancy<rt, gp, true, 128>(wgs, C) : pool_occupancy<rt, gp, false, 128>(wgs, C); \
+  }
+  HS2_POOL_CASES_64(HS2_POOL_OCC)
+#undef HS2_POOL_OCC
+#define HS2_POOL_OCC(rt, gp) \
+  if (RT == rt && Gp == gp && hd == 128 && !kv8) return pool_occupancy<rt, gp, false, 128>(wgs, C);
+  HS2_POOL_CASES_128(HS2_POOL_OCC)
 #undef HS2_POOL_OCC
   return hipSuccess;
 }
 
-template <int RT, int GP, bool KV8>
+template <int RT, int GP, bool KV8, int HDIM>
 hipError_t launch_pool_one(const PoolArgs& a, dim3 grid, int hc, hipStream_t s) {
-  HS2_LAUNCH((k_pool<RT, GP, KV8>), grid, dim3(64 * PoolShape<RT, GP, KV8>::NWV), (pool_smem_bytes<RT, GP, KV8>(hc)),
-             s, a);
+  HS2_LAUNCH((k_pool<RT, GP, KV8, HDIM>), grid, dim3(64 * PoolShape<RT, GP>::NWV),
+             (pool_smem_bytes<RT, GP, KV8, HDIM>(hc)), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
   const int hc = a.hist ? a.C : 0;  // histograms in LDS
-#define HS2_POOL_LAUNCH(rt, gp)                                                              \
-  if (RT == rt && a.Gp == gp)                                                                \
-    return a.k_scale ? launch_pool_one<rt, gp, true>(a, grid, hc, s)                         \
-                     : launch_pool_one<rt, gp, false>(a, grid, hc, s);
-  HS2_POOL_CASES(HS2_POOL_LAUNCH)
+  const bool kv8 = a.k_scale != nullptr;
+#define HS2_POOL_LAUNCH(rt, gp)                                                               \
+  if (RT == rt && a.Gp == gp) {                                                               \
+    if (a.hd == 256) return kv8 ? launch_pool_one<rt, gp, true, 256>(a, grid, hc, s)          \
+                                : launch_pool_one<rt, gp, false, 256>(a, grid, hc, s);        \
+    return kv8 ? launch_pool_one<rt, gp, true, 128>(a, grid, hc, s)                           \
+               : launch_pool_one<rt, gp, false, 128>(a, grid, hc, s);                         \
+  }
+  HS2_POOL_CASES_64(HS2_POOL_LAUNCH)
+#undef HS2_POOL_LAUNCH
+#define HS2_POOL_LAUNCH(rt, gp) \
+  if (RT == rt && a.Gp == gp && a.hd == 128 && !kv8) return launch_pool_one<rt, gp, false, 128>(a, grid, hc, s);
+  HS2_POOL_CASES_128(HS2_POOL_LAUNCH)
 #undef HS2_POOL_LAUNCH
   return hipErrorInvalidValue;
 }
 
+// sparse-attention ring kernels: (RT, waves) per head dim; 16-row stages x 4
 constexpr int SAR_TW = 16, SAR_NS = 4;
+#define HS2_SA_SHAPES(X) X(1, 1, 128) X(2, 1, 128) X(4, 2, 128) X(1, 1, 256) X(2, 2, 256) X(4, 4, 256)
 
 hipError_t set_pool_smem_limits() {
   // dynamic LDS above 64 KB must be allowed explicitly
   const int big = 150 * 1024;  // leaves room for static LDS; no kernel asks for more
   hipError_t e = hipSuccess;
-#define HS2_POOL_ATTR(rt, gp)                                                                                    \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_pool<rt, gp, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  HS2_POOL_CASES(HS2_POOL_ATTR)
+  auto allow = [&](const void* fn) {
+    if (e == hipSuccess) e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+  };
+#define HS2_POOL_ATTR(rt, gp)                           \
+  allow((const void*)k_pool<rt, gp, false, 128>);       \
+  allow((const void*)k_pool<rt, gp, true, 128>);        \
+  allow((const void*)k_pool<rt, gp, false, 256>);       \
+  allow((const void*)k_pool<rt, gp, true, 256>);
+  HS2_POOL_CASES_64(HS2_POOL_ATTR)
 #undef HS2_POOL_ATTR
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<1>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<2>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<4>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_split<8>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw)                                                                   \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
+#define HS2_POOL_ATTR(rt, gp) allow((const void*)k_pool<rt, gp, false, 128>);
+  HS2_POOL_CASES_128(HS2_POOL_ATTR)
+#undef HS2_POOL_ATTR
+  allow((const void*)k_fa_split<1>);
+  allow((const void*)k_fa_split<2>);
+  allow((const void*)k_fa_split<4>);
+  allow((const void*)k_fa_split<8>);
+#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw, hd)               \
+  allow((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>); \
+  allow((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>);
   HS2_RING_VARIANTS(HS2_RING_ATTR)
 #undef HS2_RING_ATTR
-#define HS2_SA_ATTR(rt, nwv)                                                                                     \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false>, hipFuncAttributeMaxDynamicSharedMemorySize, big); \
-  if (e == hipSuccess) e = hipFuncSetAttribute((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true>, hipFuncAttributeMaxDynamicSharedMemorySize, big);
-  HS2_SA_ATTR(1, 1) HS2_SA_ATTR(2, 1) HS2_SA_ATTR(4, 2)
+#define HS2_SA_ATTR(rt, nwv, hd)                                          \
+  allow((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false, hd>);     \
+  allow((const void*)k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true, hd>);
+  HS2_SA_SHAPES(HS2_SA_ATTR)
 #undef HS2_SA_ATTR
   return e;
 }
 
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s) {
-  HS2_LAUNCH(k_combine, dim3(rows_per_unit, (unsigned)units), dim3(256), 0, s, a);
+  if (a.hd == 256)
+    HS2_LAUNCH(k_combine<256>, dim3(rows_per_unit, (unsigned)units), dim3(256), 0, s, a);
+  else
+    HS2_LAUNCH(k_combine<128>, dim3(rows_per_unit, (unsigned)units), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1441,24 +1497,24 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t sa_smem_bytes(int split_slots, bool kv8) {
-  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? 128 : STAGE_ROW_BYTES) + (kv8 ? 2 * SAR_TW * STAGE_ROW_BYTES : 0) +
+size_t sa_smem_bytes(int split_slots, bool kv8, int hd) {
+  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? hd : 2 * hd) + (kv8 ? 2 * SAR_TW * 2 * hd : 0) +
          sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
 }
 
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s) {
   dim3 grid(a.n_split, (unsigned)((int64_t)a.B * a.Hkv * a.C));
   const bool kv8 = a.k_scale != nullptr;
-  const size_t sm = sa_smem_bytes(a.split_slots, kv8);
-#define HS2_SA_LAUNCH(rt, nwv)                                                                   \
-  if (RT == rt) {                                                                                \
-    if (kv8)                                                                                     \
-      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true>), grid, dim3(64 * nwv), sm, s, a);    \
-    else                                                                                         \
-      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false>), grid, dim3(64 * nwv), sm, s, a);   \
-    return hipGetLastError();                                                                    \
+  const size_t sm = sa_smem_bytes(a.split_slots, kv8, a.hd);
+#define HS2_SA_LAUNCH(rt, nwv, hdim)                                                                 \
+  if (RT == rt && a.hd == hdim) {                                                                    \
+    if (kv8)                                                                                         \
+      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, true, hdim>), grid, dim3(64 * nwv), sm, s, a);  \
+    else                                                                                             \
+      HS2_LAUNCH((k_sa_ring<rt, nwv, SAR_TW, SAR_NS, false, hdim>), grid, dim3(64 * nwv), sm, s, a); \
+    return hipGetLastError();                                                                        \
   }
-  HS2_SA_LAUNCH(1, 1) HS2_SA_LAUNCH(2, 1) HS2_SA_LAUNCH(4, 2)
+  HS2_SA_SHAPES(HS2_SA_LAUNCH)
 #undef HS2_SA_LAUNCH
   return hipErrorInvalidValue;
 }

@@ -40,6 +40,7 @@ struct CombineArgs {
   const float* sink;    // [Hq] sink logits (natural units of the scaled logits) or null
   const uint16_t* gate; // [B, C, Hq, D] bf16 output gate logits or null
   const float* v_scale; // [Hkv] E4M3 cache: output scale of each KV head, or null
+  int hd;               // head dim (128 or 256)
 };
 
 struct PoolArgs {
@@ -52,6 +53,7 @@ struct PoolArgs {
   const float* logits;  // [B*Hkv][C*G][logit_stride] (k_pool_logits)
   int64_t logit_stride;
   const float* k_scale;  // [Hkv] for an E4M3 cache, else null
+  int hd;                // head dim (128 or 256)
   int64_t stride_b, stride_h, stride_t;
   int64_t score_stride;
   float c2;
@@ -86,12 +88,14 @@ struct SaArgs {
   int B, C, Hq, Hkv, G, max_len;
   int n_slots, split_slots, n_split;
   const float* k_scale;  // [Hkv] for an E4M3 cache, else null
+  int hd;                // head dim (128 or 256)
 };
 
-constexpr int kFaVariants = 6;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
+constexpr int kFaVariants = 7;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
 int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
-bool fa_variant_exists(int RT, int variant);
+// head dim served by full-attention kernel (RT, variant), 0 if there is none
+int fa_variant_head_dim(int RT, int variant);
 // workgroups of the full-attention kernel (RT, variant) resident per compute
 // unit on the current device (0 if that kernel does not exist)
 hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs);
@@ -99,8 +103,8 @@ hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int rows_per_unit, int64_t units, hipStream_t s);
 hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s);
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s);
-// workgroups of k_pool (RT, Gp) with C queries resident per compute unit
-hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int* wgs);
+// workgroups of k_pool (RT, Gp, cache format, head dim) with C queries resident per compute unit
+hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int hd, int* wgs);
 hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);

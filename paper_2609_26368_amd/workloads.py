@@ -69,6 +69,10 @@ WORKLOADS = {
     "chunk8_128k_b4": Workload("chunk8_128k_b4", 4, 131072, 8, 32, 4, 128, 4096, 256, 3),
     # long-context stress at 512K, batch 2, 64 query / 8 KV heads
     "stress_512k_b2_64q8kv": Workload("stress_512k_b2_64q8kv", 2, 524288, 1, 64, 8, 128, 8192, 512, 3),
+    # the paper's own head layout at 128K, batch 8: MQA with 64 query heads on
+    # one KV head and head dim 256 (Sec. "Experimental Setup", table of the
+    # attention configurations), 1024 global + 128 local tokens (same section)
+    "paper_mqa64_d256_128k_b8": Workload("paper_mqa64_d256_128k_b8", 8, 131072, 1, 64, 1, 256, 1024, 128, 3),
 }
 
 

@@ -56,6 +56,10 @@ def test_workspace_bytes(lib):
     assert hs2.hs2_workspace_bytes(d, 0, 0) == 0
     assert hs2.hs2_workspace_bytes(d, -1, 5) == 0
     assert hs2.hs2_workspace_bytes(dims(head_dim=64), 8, 8) == 0
+    # head dim 256: partials twice as wide; at most 64 query rows per KV head
+    assert hs2.hs2_workspace_bytes(dims(head_dim=256), 256, 64) > n
+    assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_q_heads=64, n_kv_heads=1), 1024, 128) > 0
+    assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1), 16, 8) == 0
 
 
 FAKE = 1 << 20  # a 256-byte aligned non-null address; never dereferenced on the error paths
@@ -77,6 +81,11 @@ def test_full_attn_rejects_before_launch(lib):
     assert call_full(lib, dims(n_queries=0)) == hs2.HS2_ERR_SHAPE
     assert call_full(lib, dims(n_queries=17)) == hs2.HS2_ERR_SHAPE
     assert call_full(lib, dims(head_dim=64)) == hs2.HS2_ERR_UNSUPPORTED
+    assert call_full(lib, dims(head_dim=192)) == hs2.HS2_ERR_UNSUPPORTED
+    assert call_full(lib, dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
+    assert "256" in hs2.hs2_last_error()
+    # kv_stride_t must cover the head dim
+    assert call_full(lib, dims(head_dim=256, kv_strides=(4096 * 128 * 4, 4096 * 128, 128))) == hs2.HS2_ERR_ALIGN
     assert call_full(lib, dims(n_q_heads=128, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED  # G = 128
     assert call_full(lib, dims(n_q_heads=64, n_kv_heads=2, n_queries=8)) == hs2.HS2_ERR_UNSUPPORTED  # 256 rows
     assert call_full(lib, dims(max_len=0)) == hs2.HS2_ERR_SHAPE
