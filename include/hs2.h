@@ -74,7 +74,9 @@ typedef struct hs2_dims {
   int32_t n_q_heads;   /* Hq >= 1                                                 */
   int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, G = Hq / Hkv <= 64,            */
                        /*   C * (G rounded up to a power of two) <= 128           */
-  int32_t head_dim;    /* D: 128 (other values: HS2_ERR_UNSUPPORTED)              */
+  int32_t head_dim;    /* D: 128, or 256 (the paper's head dim, Sec. "Experimental */
+                       /*   Setup") with C * pow2(G) <= 64; other values and      */
+                       /*   larger groups: HS2_ERR_UNSUPPORTED                     */
   int32_t max_len;     /* Lmax: cache capacity per sequence, 1 .. 2^27 tokens     */
   int64_t kv_stride_b; /* elements; multiple of 8                                 */
   int64_t kv_stride_h; /* elements; multiple of 8                                 */

@@ -51,7 +51,8 @@ def pin_bf16_decode(O):
 # ---------------------------------------------------------------- attention
 def pin_attend_vs_library(O):
     rng = np.random.default_rng(2)
-    for n, D, scale in [(1, 8, 0.3), (37, 16, 0.25), (300, 128, 1 / math.sqrt(128)), (5, 4, 2.0)]:
+    for n, D, scale in [(1, 8, 0.3), (37, 16, 0.25), (300, 128, 1 / math.sqrt(128)), (5, 4, 2.0),
+                        (90, 256, 1 / math.sqrt(256))]:
         q = _f64(_bits(rng, D))
         K = _f64(_bits(rng, (n, D), 2.0))
         V = _f64(_bits(rng, (n, D)))
@@ -111,7 +112,7 @@ def _chunk_reference(qg, K, V, L, scale):
 
 def pin_full_group(O):
     rng = np.random.default_rng(4)
-    for C, G, L, D in [(1, 1, 50, 16), (3, 4, 41, 32), (8, 2, 64, 8), (2, 8, 9, 16)]:
+    for C, G, L, D in [(1, 1, 50, 16), (3, 4, 41, 32), (8, 2, 64, 8), (2, 8, 9, 16), (1, 64, 40, 256)]:
         qg = _f64(_bits(rng, (C, G, D)))
         K = _f64(_bits(rng, (L + 5, D)))
         V = _f64(_bits(rng, (L + 5, D)))
