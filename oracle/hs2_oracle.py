@@ -34,7 +34,10 @@ Readings taken where the paper is silent (each is listed in the design doc):
   * pooled scores below FLT_MIN count as +0 when ranking;
   * index rows are ascending and padded with -1 to k + window slots;
   * sparse layers use a plain renormalised softmax over the selected tokens
-    (no sink term).
+    (no sink term);
+  * block-level selection (the comparison granularity): a block's score is
+    the sum of its candidate tokens' pooled scores; the k / block best
+    blocks before the window are taken, the last one cut short by it.
 
 Every function here is pinned in tests/test_oracle_pins.py against closed
 forms, a library attention routine, brute-force subset enumeration and
@@ -203,6 +206,54 @@ def select_row(P_row: np.ndarray, pos: int, k: int, window: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
+# block-level selection: the granularity of the predecessor HySparse, which
+# the paper compares against (Sec. "Ablation 1: Token-Level versus
+# Block-Level Sparsity": blocks of 64 tokens, the same 1,024-token global
+# budget, the same local window).  How a block is scored is not restated
+# there; reading: a block's score is its share of the attention mass, the
+# sum of the pooled scores of its candidate tokens.
+# --------------------------------------------------------------------------
+def block_scores(P_row: np.ndarray, N: int, block: int) -> np.ndarray:
+    """float32 score of each block [j*block, (j+1)*block) clipped to the N
+    candidates: the float64 sum of its tokens' ranking values, rounded once."""
+    nb = -(-int(N) // int(block))
+    vals = rank_key(P_row[:N]).astype(np.float64)
+    out = np.zeros(nb, dtype=np.float32)
+    for j in range(nb):
+        out[j] = np.float32(vals[j * block: min((j + 1) * block, N)].sum())
+    return out
+
+
+def topk_blocks_outside_window(P_row: np.ndarray, pos: int, k: int, window: int, block: int) -> np.ndarray:
+    """The k / block best candidate blocks (score descending, then block index
+    ascending), in rank order.  Candidates are the tokens before the window;
+    the last block may be cut short by the window."""
+    N = max(0, int(pos) - int(window) + 1)
+    kb = int(k) // int(block)
+    if N == 0 or kb <= 0:
+        return np.zeros(0, dtype=np.int64)
+    key = rank_key(block_scores(P_row, N, block)).astype(np.float64)
+    j = np.arange(key.size)
+    order = np.lexsort((j, -key))
+    return order[: min(kb, key.size)].astype(np.int64)
+
+
+def select_row_blocks(P_row: np.ndarray, pos: int, k: int, window: int, block: int) -> np.ndarray:
+    """Block-level selection row: the tokens (before the window) of the best
+    k / block blocks, union the window; ascending, -1 padded to k + window."""
+    S = int(k) + int(window)
+    if pos < 0:
+        return np.full(S, -1, dtype=np.int32)
+    N = max(0, int(pos) - int(window) + 1)
+    parts = [np.arange(j * block, min((j + 1) * block, N), dtype=np.int64)
+             for j in topk_blocks_outside_window(P_row, pos, k, window, block)]
+    sel = np.sort(np.concatenate(parts + [forced_window(pos, window)]))
+    row = np.full(S, -1, dtype=np.int32)
+    row[: sel.size] = sel
+    return row
+
+
+# --------------------------------------------------------------------------
 # whole-batch steps
 # --------------------------------------------------------------------------
 def _group_q(q: np.ndarray, b: int, g: int, G: int) -> np.ndarray:
@@ -210,8 +261,11 @@ def _group_q(q: np.ndarray, b: int, g: int, G: int) -> np.ndarray:
     return bf16_to_f64(q[b, :, g * G:(g + 1) * G, :])
 
 
-def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None, k_scale=None, v_scale=None):
+def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None, k_scale=None, v_scale=None,
+                           block=None):
     """Full-attention layer, pooled scores and selection for a whole batch.
+    ``block``: block-level selection with blocks of that many tokens (k a
+    multiple of it) instead of token-level.
 
     q: uint16 [B, C, Hq, D]; K, V: uint16 bf16 bits [B, Hkv, Lmax, D], or
     uint8 E4M3 bits with float [Hkv] scales k_scale / v_scale; lens: int [B].
@@ -245,7 +299,10 @@ def full_attn_score_select(q, K, V, lens, k, window, scale=None, groups=None, k_
         P[b, g, :, :L] = p
         pos = query_positions(L, C)
         for c in range(C):
-            idx[b, g, c] = select_row(P[b, g, c], int(pos[c]), k, window)
+            if block:
+                idx[b, g, c] = select_row_blocks(P[b, g, c], int(pos[c]), k, window, block)
+            else:
+                idx[b, g, c] = select_row(P[b, g, c], int(pos[c]), k, window)
     return {"out": out, "M": M, "Z": Z, "P": P, "idx": idx}
 
 

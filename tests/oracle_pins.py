@@ -235,6 +235,88 @@ def pin_select_invariants(O):
             assert min(scores[top]) >= max(scores[rest])
 
 
+# ---------------------------------------------------------------- block-level selection
+def _brute_force_select_blocks(scores, pos, k, window, block):
+    """Enumerate every (k // block)-subset of the candidate blocks; keep the
+    largest sum of block scores, then the lexicographically smallest block
+    tuple.  Block scores: numpy's segment sums of the candidates' ranking
+    values, rounded to float32."""
+    N = max(0, pos - window + 1)
+    nb = -(-N // block)
+    vals = np.array([0.0 if s < np.finfo(np.float32).tiny else float(s) for s in scores[:N]])
+    sums = [float(np.float32(x)) for x in np.add.reduceat(vals, np.arange(0, N, block))] if N else []
+    best = None
+    for sub in itertools.combinations(range(nb), min(k // block, nb)):
+        key = (-sum(sums[j] for j in sub), sub)
+        if best is None or key < best:
+            best = key
+    chosen = [t for j in (best[1] if best else ()) for t in range(j * block, min((j + 1) * block, N))]
+    win = list(range(max(0, pos - window + 1), pos + 1))
+    row = sorted(chosen + win)
+    return row + [-1] * (k + window - len(row))
+
+
+def pin_select_blocks(O):
+    """Block-level selection: brute force, the token rule at block 1, a
+    hand-worked fixture and invariants."""
+    rng = np.random.default_rng(16)
+    for _ in range(80):
+        n = int(rng.integers(1, 15))
+        pos = n - 1
+        block = int(rng.integers(1, 5))
+        k = int(rng.integers(0, 9))
+        window = int(rng.integers(0, 5))
+        if k + window == 0:
+            continue
+        scores = rng.integers(0, 4, size=n).astype(np.float32) / np.float32(4)  # exact sums, many ties
+        got = O.select_row_blocks(scores, pos, k, window, block)
+        want = _brute_force_select_blocks([float(x) for x in scores], pos, k, window, block)
+        assert list(got) == want, (scores, pos, k, window, block, got, want)
+    for _ in range(30):  # blocks of one token: the token-level rule
+        n = int(rng.integers(1, 300))
+        k, window = int(rng.integers(0, 60)), int(rng.integers(0, 30))
+        if k + window == 0:
+            continue
+        scores = (rng.integers(0, 20, size=n) / 16).astype(np.float32)
+        assert np.array_equal(O.select_row_blocks(scores, n - 1, k, window, 1), O.select_row(scores, n - 1, k, window))
+    with open(os.path.join(GOLDEN, "selection_blocks_hand.txt")) as f:
+        rows = [ln for ln in f if ln.strip() and not ln.startswith("#")]
+    assert len(rows) >= 8
+    for ln in rows:
+        head, sc, exp = ln.split("|")
+        pos, k, window, block = (int(x) for x in head.split())
+        scores = np.array([float(x) for x in sc.split()], dtype=np.float32)
+        got = O.select_row_blocks(scores, pos, k, window, block)
+        assert list(got) == [int(x) for x in exp.split()], (ln, list(got))
+    for _ in range(40):  # invariants at larger sizes
+        n = int(rng.integers(1, 3000))
+        pos = n - 1
+        block = int(2 ** rng.integers(4, 8))
+        k = block * int(rng.integers(0, 12))
+        window = int(rng.integers(0, 200))
+        if k + window == 0:
+            continue
+        scores = rng.random(n).astype(np.float32)
+        row = np.asarray(O.select_row_blocks(scores, pos, k, window, block))
+        N = max(0, pos - window + 1)
+        nb = -(-N // block)
+        assert row.size == k + window
+        cnt = int((row >= 0).sum())
+        sel = row[:cnt]
+        assert (row[cnt:] == -1).all() and (np.diff(sel) > 0).all() and (sel <= pos).all()
+        win = set(range(max(0, pos - window + 1), pos + 1))
+        assert win <= set(sel.tolist())
+        picked = sorted({t // block for t in sel.tolist() if t < N})
+        assert len(picked) == min(k // block, nb)
+        for j in picked:  # whole blocks, cut only at N
+            assert set(range(j * block, min((j + 1) * block, N))) <= set(sel.tolist())
+        assert cnt == sum(min(block, N - j * block) for j in picked) + len(win)
+        sums = np.add.reduceat(scores[:N].astype(np.float64), np.arange(0, N, block)) if N else np.zeros(0)
+        rest = [j for j in range(nb) if j not in picked]
+        if picked and rest:
+            assert min(sums[picked]) >= max(sums[rest]) * (1 - 1e-6)
+
+
 # ---------------------------------------------------------------- sparse attention
 def pin_sparse(O):
     rng = np.random.default_rng(8)
@@ -397,4 +479,4 @@ def pin_needles(O):
 
 ALL_PINS = [pin_bf16_decode, pin_attend_vs_library, pin_attend_special_cases, pin_full_group,
             pin_head_mapping, pin_select_bruteforce, pin_select_golden, pin_select_invariants,
-            pin_sparse, pin_sparse_sink_gate, pin_fp8_cache, pin_needles]
+            pin_select_blocks, pin_sparse, pin_sparse_sink_gate, pin_fp8_cache, pin_needles]

@@ -57,6 +57,16 @@ MUTANTS = [
     ("e4m3_no_subnormals", "np.where(e == 0, m / 8.0 * 2.0 ** -6,", "np.where(e < 0, m / 8.0 * 2.0 ** -6,"),
     ("v_with_k_scale", "Vg = cache_rows(V, b, g, slice(0, L), v_scale)", "Vg = cache_rows(V, b, g, slice(0, L), k_scale)"),
     ("scale_of_head_0", "* float(scale[g])", "* float(scale[0])"),
+    ("block_score_max", "out[j] = np.float32(vals[j * block: min((j + 1) * block, N)].sum())",
+     "out[j] = np.float32(vals[j * block: min((j + 1) * block, N)].max())"),
+    ("block_ties_to_higher", "order = np.lexsort((j, -key))", "order = np.lexsort((-j, -key))"),
+    ("block_tokens_not_cut", "parts = [np.arange(j * block, min((j + 1) * block, N), dtype=np.int64)",
+     "parts = [np.arange(j * block, (j + 1) * block, dtype=np.int64)"),
+    ("block_budget_in_blocks", "kb = int(k) // int(block)", "kb = int(k)"),
+    ("block_scores_into_window", "key = rank_key(block_scores(P_row, N, block))",
+     "key = rank_key(block_scores(P_row, N + int(window), block))"),
+    ("block_denormals_counted", "vals = rank_key(P_row[:N]).astype(np.float64)",
+     "vals = P_row[:N].astype(np.float64)"),
 ]
 
 
