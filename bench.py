@@ -60,6 +60,8 @@ def parse():
                     help="sparse layers with per-head sink logits and sigmoid output gates (hs2_sparse_attn_ex)")
     ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
                     help="cache format: bf16, or OCP E4M3 bytes with one scale per KV head (the _fp8 entry points)")
+    ap.add_argument("--block", type=int, default=0,
+                    help="block-level selection with blocks of this many tokens (hs2_full_attn_score_select_blocks)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -173,7 +175,7 @@ def main():
         gates = [torch.randn((B, C, Hq, D), generator=g).to(torch.bfloat16).to(dev) for _ in q_sa]
 
     def step():
-        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream, kv_scales=kv_scales)
+        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream, kv_scales=kv_scales, block=args.block)
         for qs, o, sk, gt in zip(q_sa, sa_out, sinks, gates):
             blk.sparse(qs, K, V, lens, idx, out=o, stream=stream, sink=sk, gate=gt, kv_scales=kv_scales)
 
@@ -238,6 +240,7 @@ def main():
                       "queries_per_seq": C, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D, "k": w.k,
                       "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles,
                       "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
+                      "selection": f"block{args.block}" if args.block else "token",
                       **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),

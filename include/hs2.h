@@ -176,6 +176,37 @@ hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const ui
                                int32_t n_slots, const float* sink, const uint16_t* gate, uint16_t* out,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* Block-level selection: the granularity of the predecessor HySparse, which
+ * the paper compares against (Sec. "Ablation 1: Token-Level versus
+ * Block-Level Sparsity": blocks of 64 tokens, the same global budget and the
+ * same local window).  The same full-attention layer and pooled scores as
+ * hs2_full_attn_score_select; then the N candidates before the window are
+ * cut into blocks [j*block, (j+1)*block), the last one cut short at N; a
+ * block's score is the sum of its candidates' pooled scores (each below
+ * FLT_MIN counting as zero; the paper does not restate how a block is
+ * scored), summed in fp32; the k / block best blocks (score descending,
+ * lower block first among equal scores) are selected.  idx rows hold the
+ * tokens of the selected blocks, then the window: ascending, -1 padded to
+ * k + window.  The sparse layers take these rows unchanged.
+ *
+ *   block   a power of two in [16, 256], k a multiple of it (HS2_ERR_SHAPE);
+ *           ceil(max_len / block) <= 16384 (HS2_ERR_UNSUPPORTED)
+ * Other arguments, outputs, ownership and errors as for
+ * hs2_full_attn_score_select (bf16 cache).                                   */
+hs2_status hs2_full_attn_score_select_blocks(const hs2_dims* dims, const uint16_t* q, const uint16_t* K,
+                                             const uint16_t* V, const int32_t* len, int32_t k, int32_t window,
+                                             int32_t block, uint16_t* out, int32_t* idx, float* stats,
+                                             float* scores, void* workspace, size_t workspace_bytes,
+                                             void* stream);
+
+/* Block-level selection alone, from caller-given pooled scores
+ * [B, Hkv, C, max_len] float (device; entries [0, N) of each row are read,
+ * >= 0 and finite), exactly the selection kernels of
+ * hs2_full_attn_score_select_blocks (test and diagnostics).                  */
+hs2_status hs2_select_blocks_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
+                                         int32_t window, int32_t block, int32_t* idx, void* workspace,
+                                         size_t workspace_bytes, void* stream);
+
 /* Selection alone, from caller-given pooled scores (test and diagnostics).
  * Runs exactly the selection kernels of hs2_full_attn_score_select on
  * scores [B, Hkv, C, max_len] float (device; entries [0, N) of each row are

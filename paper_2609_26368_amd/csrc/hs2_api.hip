@@ -234,10 +234,10 @@ void make_sa_plan(const Plan& p, int n_slots, SaPlan& s) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // ---------------------------------------------------------------- timing
-enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_POOL_LOGITS, KK_SEL_INIT, KK_SEL_HIST, KK_SELECT, KK_SA,
-                  KK_SA_COMBINE, KK_COUNT };
+enum KernelKind { KK_FA = 0, KK_COMBINE, KK_POOL, KK_POOL_LOGITS, KK_SEL_INIT, KK_SEL_HIST, KK_SELECT,
+                  KK_BLOCK_SELECT, KK_SA, KK_SA_COMBINE, KK_COUNT };
 const char* kKindNames[KK_COUNT] = {"fa_split", "fa_combine", "pool_scores", "pool_logits", "sel_init", "sel_hist",
-                                    "select", "sa_split", "sa_combine"};
+                                    "select", "block_select", "sa_split", "sa_combine"};
 constexpr int kMaxTimed = 16384;
 struct Timing {
   bool on = false;
@@ -397,15 +397,50 @@ hs2_status check_fp8(const hs2_dims* dims, const float* k_scale, const float* v_
   return HS2_OK;
 }
 
+// block-level selection: blocks of a power-of-two size in [16, 256], k a
+// whole number of blocks, at most 16384 blocks per row (their keys sit in LDS)
+hs2_status check_block(const hs2_dims* d, int32_t k, int32_t block) {
+  if (block < 16 || block > 256 || (block & (block - 1)))
+    return fail(HS2_ERR_SHAPE, "block must be a power of two in [16, 256] (got %d)", block);
+  if (k % block) return fail(HS2_ERR_SHAPE, "k (%d) must be a multiple of block (%d)", k, block);
+  if (((int64_t)d->max_len + block - 1) / block > 16384)
+    return fail(HS2_ERR_UNSUPPORTED, "max_len / block exceeds 16384 blocks");
+  return HS2_OK;
+}
+
+// block keys go to the token candidates' region of the workspace (unused by
+// block-level selection; rows x max_len keys >= rows x blocks)
+BlockSelArgs block_sel_args(const Plan& p, char* ws, const float* scores, int64_t score_stride, const int32_t* len,
+                            int32_t* idx, int block) {
+  BlockSelArgs a{};
+  a.scores = scores;
+  a.len = len;
+  a.idx = idx;
+  a.keys = (uint32_t*)(ws + p.off_ckey);
+  a.key_stride = ((int64_t)p.Lmax + block - 1) / block;
+  a.rows = p.rows;
+  a.score_stride = score_stride;
+  a.C = p.C;
+  a.Hkv = p.Hkv;
+  a.max_len = p.Lmax;
+  a.k = p.k;
+  a.W = p.W;
+  a.S = p.S;
+  a.block = block;
+  return a;
+}
+
+// block == 0: token-level selection
 hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K, const void* V, const float* k_scale,
-                          const float* v_scale, const int32_t* len, int32_t k, int32_t window, uint16_t* out,
-                          int32_t* idx, float* stats, float* scores, void* workspace, size_t workspace_bytes,
-                          void* stream) {
+                          const float* v_scale, const int32_t* len, int32_t k, int32_t window, int32_t block,
+                          uint16_t* out, int32_t* idx, float* stats, float* scores, void* workspace,
+                          size_t workspace_bytes, void* stream) {
   const bool kv8 = k_scale != nullptr;
   hs2_status st = check_dims(dims);
   if (st != HS2_OK) return st;
   if ((st = check_budget(k, window)) != HS2_OK) return st;
   if (kv8 && (st = check_fp8(dims, k_scale, v_scale)) != HS2_OK) return st;
+  if (block && (st = check_block(dims, k, block)) != HS2_OK) return st;
   if (!q || !K || !V || !len || !out || !idx || !workspace)
     return fail(HS2_ERR_NULL, "q, K, V, len, out, idx and workspace are required");
   if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16) || !aligned(idx, 4) ||
@@ -472,7 +507,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   // the histogram and the per-row counters (contiguous) start at zero
   ca.v_scale = v_scale;
   ca.hd = p.D;
-  ca.clear = (uint4*)(ws + p.off_hist);
+  ca.clear = block ? nullptr : (uint4*)(ws + p.off_hist);
   ca.n_clear = (int64_t)(p.off_state - p.off_hist + sizeof(int32_t) * p.rows * 8) / 16;
   HS2_TRY_LAUNCH(KK_COMBINE, s, launch_combine(ca, std::min(16 * p.RT, p.C * p.Gp), p.units, s));
 
@@ -484,7 +519,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   pa.len = len;
   pa.stats_log2 = stats_log2;
   pa.scores = sc;
-  pa.hist = sa.hist;
+  pa.hist = block ? nullptr : sa.hist;  // block selection needs no histogram
   pa.stride_b = dims->kv_stride_b;
   pa.stride_h = dims->kv_stride_h;
   pa.stride_t = dims->kv_stride_t;
@@ -506,6 +541,11 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
     HS2_TRY_LAUNCH(KK_POOL_LOGITS, s, launch_pool_logits(pa, s));
   else
     HS2_TRY_LAUNCH(KK_POOL, s, launch_pool(pa, p.RT, s));
+  if (block) {
+    const BlockSelArgs ba = block_sel_args(p, ws, sc, sc_stride, len, idx, block);
+    HS2_TRY_LAUNCH(KK_BLOCK_SELECT, s, launch_block_select(ba, s));
+    return HS2_OK;
+  }
   return run_selection_tail(p, sa, s);
 }
 
@@ -517,7 +557,17 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
                                       const int32_t* len, int32_t k, int32_t window, uint16_t* out, int32_t* idx,
                                       float* stats, float* scores, void* workspace, size_t workspace_bytes,
                                       void* stream) {
-  return full_attn_impl(dims, q, K, V, nullptr, nullptr, len, k, window, out, idx, stats, scores, workspace,
+  return full_attn_impl(dims, q, K, V, nullptr, nullptr, len, k, window, 0, out, idx, stats, scores, workspace,
+                        workspace_bytes, stream);
+}
+
+hs2_status hs2_full_attn_score_select_blocks(const hs2_dims* dims, const uint16_t* q, const uint16_t* K,
+                                             const uint16_t* V, const int32_t* len, int32_t k, int32_t window,
+                                             int32_t block, uint16_t* out, int32_t* idx, float* stats,
+                                             float* scores, void* workspace, size_t workspace_bytes,
+                                             void* stream) {
+  if (block == 0) return fail(HS2_ERR_SHAPE, "block must be a power of two in [16, 256] (got 0)");
+  return full_attn_impl(dims, q, K, V, nullptr, nullptr, len, k, window, block, out, idx, stats, scores, workspace,
                         workspace_bytes, stream);
 }
 
@@ -527,7 +577,7 @@ hs2_status hs2_full_attn_score_select_fp8(const hs2_dims* dims, const uint16_t* 
                                           int32_t* idx, float* stats, float* scores, void* workspace,
                                           size_t workspace_bytes, void* stream) {
   if (!k_scale || !v_scale) return fail(HS2_ERR_NULL, "k_scale and v_scale are required for an FP8 cache");
-  return full_attn_impl(dims, q, K, V, k_scale, v_scale, len, k, window, out, idx, stats, scores, workspace,
+  return full_attn_impl(dims, q, K, V, k_scale, v_scale, len, k, window, 0, out, idx, stats, scores, workspace,
                         workspace_bytes, stream);
 }
 
@@ -550,6 +600,28 @@ hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, con
   HS2_TRY_LAUNCH(KK_SEL_INIT, s, launch_sel_init(sa, s));
   HS2_TRY_LAUNCH(KK_SEL_HIST, s, launch_sel_hist(sa, p.sel_nchunks, s));
   return run_selection_tail(p, sa, s);
+}
+
+hs2_status hs2_select_blocks_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
+                                         int32_t window, int32_t block, int32_t* idx, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
+  hs2_status st = check_dims(dims);
+  if (st != HS2_OK) return st;
+  if ((st = check_budget(k, window)) != HS2_OK) return st;
+  if ((st = check_block(dims, k, block)) != HS2_OK) return st;
+  if (!scores || !len || !idx || !workspace) return fail(HS2_ERR_NULL, "scores, len, idx and workspace are required");
+  if (!aligned(scores, 4) || !aligned(len, 4) || !aligned(idx, 4) || !aligned(workspace, kAlign))
+    return fail(HS2_ERR_ALIGN, "scores/len/idx need 4-byte, workspace 256-byte alignment");
+  const DeviceInfo* di = try_device_info();
+  Plan p;
+  make_plan(dims, k, window, p, di);
+  if (workspace_bytes < p.fa_bytes)
+    return fail(HS2_ERR_WORKSPACE, "workspace %zu bytes < %zu required", workspace_bytes, p.fa_bytes);
+  if ((st = ensure_device_init(&di)) != HS2_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const BlockSelArgs ba = block_sel_args(p, (char*)workspace, scores, p.Lmax, len, idx, block);
+  HS2_TRY_LAUNCH(KK_BLOCK_SELECT, s, launch_block_select(ba, s));
+  return HS2_OK;
 }
 
 hs2_status hs2_sparse_attn(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,

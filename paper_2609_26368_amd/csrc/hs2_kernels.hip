@@ -776,12 +776,15 @@ __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
       for (int j = 0; j < 4; ++j)
         if (t + j < nc) {
           sr[j] = v[j];
-          const int dg = score_digit(score_key(v[j]));
-          atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+          if (a.hist) {
+            const int dg = score_digit(score_key(v[j]));
+            atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
+          }
         }
     }
   }
   __syncthreads();
+  if (!a.hist) return;
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) {
     const uint32_t v = hist[i];
     if (!v) continue;
@@ -1108,6 +1111,167 @@ __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
   if (th.mode == 2) resolve_row(a, row, th.need, min(a.state[row * 8 + 3], (int)a.cand_cap), sh);
   __syncthreads();
   emit_row(a, row, ri, sh);
+}
+
+// ---------------------------------------------------------------------------- block-level selection
+// The candidates [0, N) of a selection row (b, g, c) are cut into blocks of
+// `block` tokens (the last one cut short at N); a block's score is the fp32
+// sum of its candidates' scores (scores below FLT_MIN count as zero; fixed
+// summation order).  k_block_sums writes every block's score key; then one
+// workgroup per row finds the k / block best blocks (score descending, lower
+// block first among equal scores) by an 8-bit radix select on the keys held
+// in LDS and emits them in ascending order as their tokens, then the window,
+// then -1 padding.  Every selected block but the last one in ascending order
+// is whole, so block r of the ascending list starts at output slot r * block.
+constexpr int BSEL_MAX_BLOCKS = 16384;  // block keys per row in LDS (64 KB)
+constexpr int BSUM_TOKENS = 8192;       // tokens per workgroup of k_block_sums
+
+__device__ inline bool block_row(const BlockSelArgs& a, int64_t row, int& pos, int& N) {
+  const int c = (int)(row % a.C);
+  const int b = (int)(row / ((int64_t)a.C * a.Hkv));
+  pos = clamp_len(a.len, b, a.max_len) - a.C + c;
+  N = max(0, pos - a.W + 1);
+  return pos >= 0;
+}
+
+// grid (ceil(max_len / BSUM_TOKENS), rows), 256 threads: each thread sums 4
+// consecutive tokens, block / 4 lanes butterfly-sum one block (block is a
+// power of two in [16, 256], so blocks never straddle lanes of two waves).
+__global__ __launch_bounds__(256) void k_block_sums(BlockSelArgs a) {
+  const int64_t row = blockIdx.y;
+  int pos, N;
+  if (!block_row(a, row, pos, N)) return;
+  const int t0 = blockIdx.x * BSUM_TOKENS;
+  if (t0 >= N) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int B = a.block, gl = B / 4;  // lanes per block
+  const float* P = a.scores + row * a.score_stride;
+  uint32_t* keys = a.keys + row * a.key_stride;
+  constexpr int U = BSUM_TOKENS / 1024;
+  float v[U][4];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = t0 + 1024 * u + 4 * tid;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[u][i] = t + i < N ? P[t + i] : 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = t0 + 1024 * u + 4 * tid;
+    float x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = v[u][i] < 1.17549435e-38f ? 0.f : v[u][i];
+    float sum = (x[0] + x[1]) + (x[2] + x[3]);
+    for (int o = 1; o < gl; o <<= 1) sum += __shfl_xor(sum, o);
+    if ((lane & (gl - 1)) == 0 && t < N) keys[t / B] = score_key(sum);
+  }
+}
+
+// grid (rows), 1024 threads; dynamic LDS: 4 bytes per block of the longest row
+__global__ __launch_bounds__(SELB) void k_block_select(BlockSelArgs a) {
+  extern __shared__ uint32_t bkey[];  // [nb] score keys, then [kb] selected blocks ascending
+  __shared__ uint32_t hist[256];
+  __shared__ int lds16[16];
+  __shared__ int s_dig[2];
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  int pos, N;
+  int32_t* out = a.idx + row * a.S;
+  if (!block_row(a, row, pos, N)) {
+    for (int i = tid; i < a.S; i += SELB) out[i] = -1;
+    return;
+  }
+  const int B = a.block;  // power of two
+  const int nb = (N + B - 1) / B;
+  const int kb = min(a.k / B, nb);
+
+  // 1. the row's block keys
+  const uint32_t* keys = a.keys + row * a.key_stride;
+  for (int j = tid; j < nb; j += SELB) bkey[j] = keys[j];
+  __syncthreads();
+
+  // 2. threshold key T: fewer than kb keys above it, at least kb at or above
+  uint32_t prefix = 0, mask = 0;
+  int need = kb;  // blocks still to take among those matching the prefix
+  if (kb > 0 && kb < nb) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      if (tid < 256) hist[tid] = 0;
+      __syncthreads();
+      for (int j = tid; j < nb; j += SELB) {
+        const uint32_t key = bkey[j];
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (wave == 0) {  // lane l holds digits 255 - 4 l .. 252 - 4 l (from the top)
+        int cnt[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cnt[i] = (int)hist[255 - 4 * lane - i];
+          sum += cnt[i];
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o);
+          if (lane >= o) incl += y;
+        }
+        int above = incl - sum;
+        if (above < need && incl >= need) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (above + cnt[i] >= need) {
+              s_dig[0] = 255 - 4 * lane - i;
+              s_dig[1] = need - above;
+              break;
+            }
+            above += cnt[i];
+          }
+        }
+      }
+      __syncthreads();
+      prefix |= (uint32_t)s_dig[0] << shift;
+      mask |= 255u << shift;
+      need = s_dig[1];
+      __syncthreads();
+    }
+  }
+  const uint32_t T = prefix;  // with kb == nb every block is taken (need stays nb)
+
+  // 3. selection flags of this thread's contiguous blocks, ranks, emission
+  const int per = (nb + SELB - 1) / SELB;
+  const int j0 = tid * per, j1 = min(nb, j0 + per);
+  uint32_t sel = 0;
+  if (kb > 0) {
+    int eq = 0;
+    if (kb < nb)
+      for (int j = j0; j < j1; ++j) eq += bkey[j] == T;
+    int total;
+    int eq_before = block_scan_1024(eq, lds16, total);
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t key = bkey[j];
+      bool take = kb == nb || key > T;
+      if (kb < nb && key == T) take = eq_before++ < need;
+      if (take) sel |= 1u << (j - j0);
+    }
+  }
+  int before_total;
+  const int sel_before = block_scan_1024(__popc(sel), lds16, before_total);  // barriers: keys read
+  uint32_t* list = bkey;  // the keys are no longer needed
+  {
+    int r = sel_before;
+    for (int j = j0; j < j1; ++j)
+      if (sel >> (j - j0) & 1u) list[r++] = (uint32_t)j;
+  }
+  __syncthreads();
+  const int blk_tokens = kb == 0 ? 0 : (kb - 1) * B + min(B, N - (int)list[kb - 1] * B);
+  for (int e = tid; e < kb * B; e += SELB) {
+    const int t = (int)list[e / B] * B + (e & (B - 1));
+    if (t < N) out[e] = t;
+  }
+  const int wlo = max(0, pos - a.W + 1);
+  const int nwin = pos - wlo + 1;
+  for (int i = tid; i < a.S - blk_tokens; i += SELB) out[blk_tokens + i] = i < nwin ? wlo + i : -1;
 }
 
 // ============================================================================ sparse attention
@@ -1453,6 +1617,7 @@ hipError_t set_pool_smem_limits() {
 #define HS2_POOL_ATTR(rt, gp) allow((const void*)k_pool<rt, gp, false, 128>);
   HS2_POOL_CASES_128(HS2_POOL_ATTR)
 #undef HS2_POOL_ATTR
+  allow((const void*)k_block_select);
   allow((const void*)k_fa_split<1>);
   allow((const void*)k_fa_split<2>);
   allow((const void*)k_fa_split<4>);
@@ -1488,6 +1653,19 @@ hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s) {
   HS2_LAUNCH(k_sel_hist, dim3(nchunks, (unsigned)a.rows), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
+hipError_t launch_block_select(const BlockSelArgs& a, hipStream_t s) {
+  const size_t nb_max = ((size_t)a.max_len + a.block - 1) / a.block;
+  if (nb_max > (size_t)BSEL_MAX_BLOCKS || a.key_stride < (int64_t)nb_max || a.block < 16 || a.block > 256 ||
+      (a.block & (a.block - 1)))
+    return hipErrorInvalidValue;
+  const unsigned chunks = (unsigned)(((int64_t)a.max_len + BSUM_TOKENS - 1) / BSUM_TOKENS);
+  HS2_LAUNCH(k_block_sums, dim3(chunks, (unsigned)a.rows), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  HS2_LAUNCH(k_block_select, dim3((unsigned)a.rows), dim3(SELB), nb_max * sizeof(uint32_t), s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const SelArgs& a, hipStream_t s) {
   const int64_t chunks = ((int64_t)a.max_len + SEL_TOKENS - 1) / SEL_TOKENS;
   HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELB), 0, s, a);

@@ -75,6 +75,16 @@ struct SelArgs {
   int chunk;
 };
 
+struct BlockSelArgs {
+  const float* scores;  // [rows][score_stride]
+  const int32_t* len;
+  int32_t* idx;         // [rows][S]
+  uint32_t* keys;       // [rows][key_stride] block score keys (workspace)
+  int64_t rows, score_stride, key_stride;
+  int C, Hkv, max_len, k, W, S;
+  int block;            // tokens per block, a power of two in [16, 256]; ceil(max_len / block) <= 16384
+};
+
 struct SaArgs {
   const uint16_t* q;
   const uint16_t* K;
@@ -109,6 +119,7 @@ hipError_t set_pool_smem_limits();
 hipError_t launch_sel_init(const SelArgs& a, hipStream_t s);
 hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
 hipError_t launch_select(const SelArgs& a, hipStream_t s);
+hipError_t launch_block_select(const BlockSelArgs& a, hipStream_t s);  // block sums + selection
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s);
 
 }  // namespace hs2

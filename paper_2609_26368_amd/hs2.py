@@ -27,7 +27,8 @@ HS2_ERR_ALIGN = -5
 HS2_ERR_HIP = -6
 
 EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_sparse_attn_ex",
-            "hs2_full_attn_score_select_fp8", "hs2_sparse_attn_fp8", "hs2_select_from_scores",
+            "hs2_full_attn_score_select_fp8", "hs2_sparse_attn_fp8", "hs2_full_attn_score_select_blocks",
+            "hs2_select_from_scores", "hs2_select_blocks_from_scores",
             "hs2_status_string", "hs2_last_error", "hs2_timing_enable", "hs2_timing_reset", "hs2_timing_read"]
 
 
@@ -69,6 +70,10 @@ def load() -> ctypes.CDLL:
     lib.hs2_full_attn_score_select_fp8.restype = I32
     lib.hs2_sparse_attn_fp8.argtypes = [D, P, P, P, P, P, P, P, I32, P, P, P, P, SZ, P]
     lib.hs2_sparse_attn_fp8.restype = I32
+    lib.hs2_full_attn_score_select_blocks.argtypes = [D, P, P, P, P, I32, I32, I32, P, P, P, P, P, SZ, P]
+    lib.hs2_full_attn_score_select_blocks.restype = I32
+    lib.hs2_select_blocks_from_scores.argtypes = [D, P, P, I32, I32, I32, P, P, SZ, P]
+    lib.hs2_select_blocks_from_scores.restype = I32
     lib.hs2_select_from_scores.argtypes = [D, P, P, I32, I32, P, P, SZ, P]
     lib.hs2_select_from_scores.restype = I32
     lib.hs2_status_string.argtypes = [I32]
@@ -251,6 +256,44 @@ def hs2_sparse_attn_fp8(dims, q, K8, V8, k_scale, v_scale, len, idx, n_slots, si
                                       _stream(stream)))
 
 
+def hs2_full_attn_score_select_blocks(dims, q, K, V, len, k, window, block, out, idx, stats=None, scores=None,
+                                      workspace=None, stream=None):
+    """hs2_full_attn_score_select with block-level selection (blocks of `block` tokens)."""
+    dev = q.device
+    B, C, Hq, Hkv, D, L = dims.batch, dims.n_queries, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.max_len
+    _expect(q, "q", (B, C, Hq, D), _BF16, dev)
+    _check_kv(dims, K, V, dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(out, "out", (B, C, Hq, D), _BF16, dev)
+    _expect(idx, "idx", (B, Hkv, C, k + window), (torch.int32,), dev)
+    if stats is not None:
+        _expect(stats, "stats", (B, C, Hq, 2), (torch.float32,), dev)
+    if scores is not None:
+        _expect(scores, "scores", (B, Hkv, C, L), (torch.float32,), dev)
+    need = hs2_workspace_bytes(dims, k, window)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace of {need} bytes required")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(load().hs2_full_attn_score_select_blocks(ctypes.byref(dims), _ptr(q), _ptr(K), _ptr(V), _ptr(len), int(k),
+                                                    int(window), int(block), _ptr(out), _ptr(idx), _ptr(stats),
+                                                    _ptr(scores), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def hs2_select_blocks_from_scores(dims, scores, len, k, window, block, idx, workspace, stream=None):
+    """Block-level selection alone from given pooled scores [B, Hkv, C, max_len] float32."""
+    dev = scores.device
+    B, C, Hkv, L = dims.batch, dims.n_queries, dims.n_kv_heads, dims.max_len
+    _expect(scores, "scores", (B, Hkv, C, L), (torch.float32,), dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(idx, "idx", (B, Hkv, C, k + window), (torch.int32,), dev)
+    need = hs2_workspace_bytes(dims, k, window)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace of {need} bytes required")
+    _check(load().hs2_select_blocks_from_scores(ctypes.byref(dims), _ptr(scores), _ptr(len), int(k), int(window),
+                                                int(block), _ptr(idx), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
 def hs2_select_from_scores(dims, scores, len, k, window, idx, workspace, stream=None):
     """Selection alone from given pooled scores [B, Hkv, C, max_len] float32."""
     dev = scores.device
@@ -301,7 +344,8 @@ class HybridBlock:
 
     ``full(q, K, V, lens)`` runs the full-attention layer and selection and
     returns (out, idx); ``sparse(q, K, V, lens, idx)`` runs one sparse layer.
-    With ``kv_scales=(k_scale, v_scale)`` K and V are an E4M3 (uint8) cache.
+    With ``kv_scales=(k_scale, v_scale)`` K and V are an E4M3 (uint8) cache;
+    ``full(..., block=64)`` selects blocks of 64 tokens instead of tokens.
     """
 
     def __init__(self, batch, n_queries, n_q_heads, n_kv_heads, head_dim, max_len, k, window, device="cuda",
@@ -314,14 +358,20 @@ class HybridBlock:
         self.workspace = torch.empty(need, dtype=torch.uint8, device=device)
         self.device = torch.device(device)
 
-    def full(self, q, K, V, lens, stats=None, scores=None, out=None, idx=None, stream=None, kv_scales=None):
+    def full(self, q, K, V, lens, stats=None, scores=None, out=None, idx=None, stream=None, kv_scales=None,
+             block=None):
         d = self.dims
         if out is None:
             out = torch.empty((d.batch, d.n_queries, d.n_q_heads, d.head_dim), dtype=torch.bfloat16, device=q.device)
         if idx is None:
             idx = torch.empty((d.batch, d.n_kv_heads, d.n_queries, self.k + self.window), dtype=torch.int32,
                               device=q.device)
-        if kv_scales is None:
+        if block:
+            if kv_scales is not None:
+                raise ValueError("block-level selection is served for bf16 caches")
+            hs2_full_attn_score_select_blocks(d, q, K, V, lens, self.k, self.window, block, out, idx, stats, scores,
+                                              self.workspace, stream)
+        elif kv_scales is None:
             hs2_full_attn_score_select(d, q, K, V, lens, self.k, self.window, out, idx, stats, scores,
                                        self.workspace, stream)
         else:

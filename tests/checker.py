@@ -110,3 +110,45 @@ def boundary_gap(ref_P_row, pos: int, k: int, window: int) -> float:
         return float("inf")
     s = np.sort(ref_P_row[:N].astype(np.float64))[::-1]
     return float((s[k - 1] - s[k]) / max(s[k - 1], 1e-300))
+
+
+# block-level selection: the GPU sums a block's fp32 scores in its own order
+# from its own scores (each within ~2e-7 of the oracle's): up to 256 terms
+BLOCK_TIE_RTOL = 1e-5
+
+
+def check_block_idx(gpu_idx, ref_idx, ref_P, lens, C: int, window: int, block: int) -> dict:
+    """Block-level selection rows [B, Hkv, C, S]: the window part exact, the
+    selected blocks whole (cut only at the window) and equal to the oracle's
+    except swaps of blocks whose oracle block scores differ by less than
+    BLOCK_TIE_RTOL relative."""
+    B, Hkv = ref_idx.shape[:2]
+    swaps = 0
+    for b in range(B):
+        L = int(lens[b])
+        for g in range(Hkv):
+            for c in range(C):
+                pos = L - C + c
+                N = max(0, pos - window + 1)
+                gr, rr = np.asarray(gpu_idx[b, g, c]), np.asarray(ref_idx[b, g, c])
+                ng, nr = int((gr >= 0).sum()), int((rr >= 0).sum())
+                assert (gr[ng:] == -1).all(), "gpu row: -1 padding not contiguous"
+                gs, rs = gr[:ng].astype(np.int64), rr[:nr].astype(np.int64)
+                assert (np.diff(gs) > 0).all(), "gpu row not strictly ascending"
+                assert np.array_equal(gs[gs >= N], rs[rs >= N]), "window part differs"
+                gb = sorted(set((gs[gs < N] // block).tolist()))
+                rb = sorted(set((rs[rs < N] // block).tolist()))
+                assert len(gb) == len(rb), f"gpu selects {len(gb)} blocks, oracle {len(rb)}"
+                whole = [np.arange(j * block, min((j + 1) * block, N)) for j in gb]
+                assert np.array_equal(gs[gs < N], np.concatenate(whole) if whole else gs[:0]), "partial block"
+                only_g, only_r = sorted(set(gb) - set(rb)), sorted(set(rb) - set(gb))
+                if not only_g:
+                    continue
+                P = np.asarray(ref_P[b, g, c, :N], dtype=np.float32)
+                P = np.where(P < np.finfo(np.float32).tiny, 0.0, P.astype(np.float64))
+                sums = np.add.reduceat(P, np.arange(0, N, block))
+                pg, pr = sums[only_g], sums[only_r]
+                gap = np.abs(pr[:, None] - pg[None, :]) / np.maximum(np.maximum(pr[:, None], pg[None, :]), 1e-300)
+                assert gap.max() < BLOCK_TIE_RTOL, f"swap of blocks whose oracle scores differ by {gap.max():.3g}"
+                swaps += len(only_g)
+    return {"block_swaps": swaps}

@@ -189,6 +189,34 @@ def test_fp8_binding_checks_dtypes_before_calling():
         hs2.hs2_sparse_attn(d, q, K8, K8, lens, idx, 8, out, ws)
 
 
+def test_block_selection_rejects_before_launch(lib):
+    vp = ctypes.c_void_p
+
+    def full(d, k=128, w=16, block=64, ws_bytes=1 << 40):
+        return lib.hs2_full_attn_score_select_blocks(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), k, w,
+                                                     block, vp(FAKE), vp(FAKE), None, None, vp(FAKE), ws_bytes, None)
+
+    def sel(d, k=128, w=16, block=64, scores=FAKE, ws_bytes=1 << 40):
+        return lib.hs2_select_blocks_from_scores(ctypes.byref(d), vp(scores), vp(FAKE), k, w, block, vp(FAKE),
+                                                 vp(FAKE), ws_bytes, None)
+
+    d = dims()
+    for call in (full, sel):
+        assert call(d, block=0) == hs2.HS2_ERR_SHAPE
+        assert call(d, block=48) == hs2.HS2_ERR_SHAPE      # not a power of two
+        assert call(d, block=8) == hs2.HS2_ERR_SHAPE       # below 16
+        assert call(d, block=512) == hs2.HS2_ERR_SHAPE     # above 256
+        assert call(d, k=100) == hs2.HS2_ERR_SHAPE         # k not a whole number of blocks
+        assert "multiple" in hs2.hs2_last_error()
+        # more than 16384 blocks per row
+        assert call(dims(max_len=16384 * 16 + 1), block=16) == hs2.HS2_ERR_UNSUPPORTED
+    assert sel(d, scores=FAKE + 2) == hs2.HS2_ERR_ALIGN
+    assert sel(d, scores=None) == hs2.HS2_ERR_NULL
+    need = hs2.hs2_workspace_bytes(d, 128, 16)
+    assert full(d, ws_bytes=need - 256) == hs2.HS2_ERR_WORKSPACE
+    assert sel(d, ws_bytes=need - 256) == hs2.HS2_ERR_WORKSPACE
+
+
 def test_status_strings(lib):
     for code in (hs2.HS2_OK, hs2.HS2_ERR_NULL, hs2.HS2_ERR_SHAPE, hs2.HS2_ERR_UNSUPPORTED, hs2.HS2_ERR_WORKSPACE,
                  hs2.HS2_ERR_ALIGN, hs2.HS2_ERR_HIP):
