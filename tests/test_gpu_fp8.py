@@ -80,20 +80,23 @@ def test_fp8_sparse_sink_and_gate():
     CK.check_out(CK.bf16_bits_to_f64(host_bits(got)), want, "FP8 sparse layer with sink and gate")
 
 
-SAME = [  # (workload, FA split, score split): one row tile, two, and four
-    (SMALL[0], 512, 1024),
-    (SMALL[3], 1024, 1024),
-    (W.Workload("fp8_same_32q1kv", 2, 3000, 2, 32, 1, 128, 300, 40, 1, ctx_min=1200), 768, 512),
+SAME = [  # (workload, FA split, score split, FA kernel variant): one row tile (two shapes), four row tiles (two)
+    (SMALL[0], 512, 1024, 3),
+    (SMALL[0], 512, 1024, 2),
+    (SMALL[3], 1024, 1024, 5),
+    (W.Workload("fp8_same_32q1kv", 2, 3000, 2, 32, 1, 128, 300, 40, 1, ctx_min=1200), 768, 512, 0),
 ]
 
 
-@pytest.mark.parametrize("w,fa_split,pool_split", SAME, ids=[s[0].name for s in SAME])
-def test_fp8_equals_bf16_on_the_dequantised_cache(w, fa_split, pool_split, monkeypatch):
+@pytest.mark.parametrize("w,fa_split,pool_split,variant", SAME, ids=[f"{s[0].name}-v{s[3]}" for s in SAME])
+def test_fp8_equals_bf16_on_the_dequantised_cache(w, fa_split, pool_split, variant, monkeypatch):
     """Power-of-two scales: the bf16 cache of the dequantised values is
-    exactly the same cache, so both entry points give identical bits."""
+    exactly the same cache, so both entry points give identical bits when
+    they use the same kernel shape and splits."""
     from paper_2609_26368_amd import hs2
     monkeypatch.setenv("HS2_FA_SPLIT", str(fa_split))
     monkeypatch.setenv("HS2_POOL_SPLIT", str(pool_split))
+    monkeypatch.setenv("HS2_FA_VARIANT", str(variant))
     inp = W.make_inputs(w, seed=13, kv="fp8")
     B, C, Hq, Hkv, D, L = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim, inp.K.shape[2]
     ks = np.array([2.0 ** -(3 + g % 3) for g in range(Hkv)], dtype=np.float32)
