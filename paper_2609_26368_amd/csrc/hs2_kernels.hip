@@ -432,10 +432,12 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   float z = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (M != -INFINITY) {
+    // branch-free so that several slots' loads are in flight: an empty
+    // partial (m = -inf, O = 0) gets weight exp2(-inf) = 0
+#pragma unroll 4
     for (int s = sg; s < nvalid; s += SG) {
       const int64_t pr = base + (int64_t)s * a.rows;
       const float m = a.part_ml[pr * 4];
-      if (m == -INFINITY) continue;
       const float w = fast_exp2(m - M);
       z += a.part_ml[pr * 4 + 1] * w;
       const float4 o = *(const float4*)(a.part_o + pr * HDIM + 4 * dq);
