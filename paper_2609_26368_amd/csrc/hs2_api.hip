@@ -192,9 +192,6 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int pool_cu = di && p.C <= 16 ? di->pool_wgs[p.D == 256][kv8][lrt][ilog2(p.Gp)][p.C] : 0;
   const int64_t pslots = (int64_t)(di ? di->cus : 256) * (pool_cu > 0 ? pool_cu : 4);
   int psplit = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, std::max<int64_t>(1, pslots / p.units)), 64));
-  // the full-attention splits when they also fit in one round: the score
-  // pass then walks each split backwards from the rows the FA kernel read last
-  psplit = std::max(psplit, p.fa_split);
   psplit = env_int("HS2_POOL_SPLIT", psplit);
   psplit = (int)std::max<int64_t>(64, round_up(std::min<int64_t>(std::min(psplit, 32768), p.Lmax), 64));
   p.pool_split = psplit;

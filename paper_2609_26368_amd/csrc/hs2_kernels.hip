@@ -654,10 +654,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     const int row = RPL * (wave * LPM + u) + lane / CPR;
     lane_off[u] = lane_offset(row, row);
   }
-  // the split is walked from its end: the full-attention kernel read the
-  // ends of its splits last, so those rows are the likeliest to be cached
-  auto issue = [&](int tile) {  // tile-th in walking order
-    const int t0 = t_begin + (ntiles - 1 - tile) * TW;
+  auto issue = [&](int tile) {
+    const int t0 = t_begin + tile * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
     const int64_t tile_off = (int64_t)t0 * stride_t;
@@ -698,7 +696,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
       if (NWV > 1) __syncthreads();
       stg = tile_p;
     }
-    const int t0 = t_begin + (ntiles - 1 - i) * TW;
+    const int t0 = t_begin + i * TW;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
       const int row = 16 * bi + (lane & 15);
