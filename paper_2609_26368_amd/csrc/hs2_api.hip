@@ -137,15 +137,18 @@ int ilog2(int v) {
 
 // Measured on MI355X with one-round splits: 32-token tiles in 3 stages for
 // one row tile; 16-token tiles in 3 stages and two token groups merged in
-// LDS (half the split partials) for two and four; the workgroup kernel for
-// eight.  Head dim 256: one row tile per wave, 16-token tiles in 3 stages.
-// E4M3 cache with one row tile: 16-token tiles (the smaller ring and
-// converted tile keep twice as many one-wave workgroups resident, which the
-// per-tile conversion needs; 32-token tiles run at half the speed).
+// LDS (half the split partials) for two; for four, one row tile per wave
+// (four waves), 32-token tiles in 2 stages and two token groups; the
+// workgroup kernel for eight.  Head dim 256: one row tile per wave,
+// 16-token tiles in 3 stages.  E4M3 cache with one row tile: 16-token tiles
+// (the smaller ring and converted tile keep twice as many one-wave
+// workgroups resident, which the per-tile conversion needs; 32-token tiles
+// run at half the speed).
 int default_fa_variant(int RT, int hd, bool kv8) {
   if (hd == 256) return 6;
   if (RT >= 8) return 1;
   if (RT == 1) return kv8 ? 3 : 2;
+  if (RT == 4) return 7;
   return 5;
 }
 
@@ -168,8 +171,7 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   const int rows16 = (int)cdiv(p.C * p.Gp, 16);
   p.RT = next_pow2(rows16);
   p.fa_variant = env_int("HS2_FA_VARIANT", default_fa_variant(p.RT, p.D, kv8));
-  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || fa_variant_head_dim(p.RT, p.fa_variant) != p.D ||
-      (kv8 && p.fa_variant == 1))
+  if (p.fa_variant < 0 || p.fa_variant >= kFaVariants || fa_variant_head_dim(p.RT, p.fa_variant, kv8) != p.D)
     p.fa_variant = default_fa_variant(p.RT, p.D, kv8);
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;

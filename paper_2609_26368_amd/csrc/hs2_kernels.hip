@@ -1426,9 +1426,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
 // Full attention kernel variants (the planner's defaults: head dim 128 with
-// RT = 1 -> 2, RT = 2 or 4 -> 5, RT = 8 -> 1; head dim 256 -> 6):
+// RT = 1 -> 2 (E4M3: 3), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1; head dim
+// 256 -> 6):
 //   1: workgroup kernel (64-row stages shared by 4 or 8 waves), head dim 128
-//   0, 2, 3, 5: ring kernels of head dim 128; 6: ring kernels of head dim 256
+//   0, 2, 3, 5, 7: ring kernels of head dim 128; 6: ring kernels of head dim 256
 // Columns: variant, RT, waves per token group, stage rows, stages, token
 // groups, head dim.
 #define HS2_RING_VARIANTS(X)                                                        \
@@ -1436,12 +1437,17 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   X(2, 1, 1, 32, 3, 1, 128) X(2, 2, 1, 32, 3, 1, 128) X(2, 4, 2, 32, 3, 1, 128)     \
   X(3, 1, 1, 16, 3, 1, 128) X(3, 2, 1, 16, 3, 1, 128) X(3, 4, 2, 16, 3, 1, 128)     \
   X(5, 1, 1, 32, 3, 1, 128) X(5, 2, 1, 16, 3, 2, 128) X(5, 4, 2, 16, 3, 2, 128)     \
-  X(6, 1, 1, 16, 3, 1, 256) X(6, 2, 2, 16, 3, 1, 256) X(6, 4, 4, 16, 3, 1, 256)
+  X(6, 1, 1, 16, 3, 1, 256) X(6, 2, 2, 16, 3, 1, 256) X(6, 4, 4, 16, 3, 1, 256)     \
+  X(7, 2, 2, 32, 2, 2, 128) X(7, 4, 4, 32, 2, 2, 128)
 
-int fa_variant_head_dim(int RT, int variant) {
-  if (variant == 1) return RT == 1 || RT == 2 || RT == 4 || RT == 8 ? 128 : 0;  // workgroup kernel
+// a ring shape serves a cache format only if every wave loads whole 1 KB
+// pieces of each stage (the kernel asserts it; other shapes are never built)
+constexpr bool fa_ring_ok(int nwv, int tw, bool kv8, int hd) { return tw * (kv8 ? hd : 2 * hd) / 1024 / nwv >= 1; }
+
+int fa_variant_head_dim(int RT, int variant, bool kv8) {
+  if (variant == 1) return !kv8 && (RT == 1 || RT == 2 || RT == 4 || RT == 8) ? 128 : 0;  // workgroup kernel
 #define HS2_RING_HD(v, rt, nwv, tw, ns, tgw, hd) \
-  if (variant == v && RT == rt) return hd;
+  if (variant == v && RT == rt) return fa_ring_ok(nwv, tw, kv8, hd) ? hd : 0;
   HS2_RING_VARIANTS(HS2_RING_HD)
 #undef HS2_RING_HD
   return 0;
@@ -1480,14 +1486,44 @@ constexpr size_t fa_ring_lds(int tw, int ns, int tgw, bool kv8, int hd) {
   return (size_t)tgw * ((size_t)ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? 2 * tw * 2 * hd : 0));
 }
 
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+hipError_t fa_ring_occupancy(int* wgs) {
+  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
+    *wgs = 0;
+    return hipSuccess;
+  } else {
+    return occupancy_capped(wgs, (const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>, 64 * NWV * TGW,
+                            fa_ring_lds(TW, NS, TGW, KV8, HDIM));
+  }
+}
+
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+hipError_t fa_ring_launch(const FaArgs& a, dim3 grid, hipStream_t s) {
+  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
+    return hipErrorInvalidValue;
+  } else {
+    HS2_LAUNCH((k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>), grid, dim3(64 * NWV * TGW),
+               fa_ring_lds(TW, NS, TGW, KV8, HDIM), s, a);
+    return hipGetLastError();
+  }
+}
+
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+hipError_t fa_ring_allow_lds(int bytes) {
+  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
+    return hipSuccess;
+  } else {
+    return hipFuncSetAttribute((const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  }
+}
+
 hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
   *wgs = 0;
-#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw, hd)                                                                  \
-  if (variant == v && RT == rt)                                                                                   \
-    return kv8 ? occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>, 64 * nwv * tgw,     \
-                                  fa_ring_lds(tw, ns, tgw, true, hd))                                             \
-               : occupancy_capped(wgs, (const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>, 64 * nwv * tgw,    \
-                                  fa_ring_lds(tw, ns, tgw, false, hd));
+#define HS2_RING_OCC(v, rt, nwv, tw, ns, tgw, hd)                                                      \
+  if (variant == v && RT == rt)                                                                       \
+    return kv8 ? fa_ring_occupancy<rt, nwv, tw, ns, tgw, true, hd>(wgs)                               \
+               : fa_ring_occupancy<rt, nwv, tw, ns, tgw, false, hd>(wgs);
   HS2_RING_VARIANTS(HS2_RING_OCC)
 #undef HS2_RING_OCC
   if (kv8 || variant != 1) return hipSuccess;  // E4M3 only through the ring kernels
@@ -1503,16 +1539,10 @@ hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd)                                                   \
-  if (variant == v && RT == rt) {                                                                       \
-    if (a.k_scale)                                                                                      \
-      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>), grid, dim3(64 * nwv * tgw),              \
-                 fa_ring_lds(tw, ns, tgw, true, hd), s, a);                                             \
-    else                                                                                                \
-      HS2_LAUNCH((k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>), grid, dim3(64 * nwv * tgw),             \
-                 fa_ring_lds(tw, ns, tgw, false, hd), s, a);                                            \
-    return hipGetLastError();                                                                          \
-  }
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd)                                              \
+  if (variant == v && RT == rt)                                                                    \
+    return a.k_scale ? fa_ring_launch<rt, nwv, tw, ns, tgw, true, hd>(a, grid, s)                   \
+                     : fa_ring_launch<rt, nwv, tw, ns, tgw, false, hd>(a, grid, s);
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
 #undef HS2_RING_LAUNCH
   if (a.k_scale || variant != 1) return hipErrorInvalidValue;  // E4M3 only through the ring kernels
@@ -1624,9 +1654,9 @@ hipError_t set_pool_smem_limits() {
   allow((const void*)k_fa_split<2>);
   allow((const void*)k_fa_split<4>);
   allow((const void*)k_fa_split<8>);
-#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw, hd)               \
-  allow((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, false, hd>); \
-  allow((const void*)k_fa_ring<rt, nwv, tw, ns, tgw, true, hd>);
+#define HS2_RING_ATTR(v, rt, nwv, tw, ns, tgw, hd)                                          \
+  if (e == hipSuccess) e = fa_ring_allow_lds<rt, nwv, tw, ns, tgw, false, hd>(big);         \
+  if (e == hipSuccess) e = fa_ring_allow_lds<rt, nwv, tw, ns, tgw, true, hd>(big);
   HS2_RING_VARIANTS(HS2_RING_ATTR)
 #undef HS2_RING_ATTR
 #define HS2_SA_ATTR(rt, nwv, hd)                                          \

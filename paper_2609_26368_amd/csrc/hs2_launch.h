@@ -101,11 +101,11 @@ struct SaArgs {
   int hd;                // head dim (128 or 256)
 };
 
-constexpr int kFaVariants = 7;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
+constexpr int kFaVariants = 8;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
 int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
-// head dim served by full-attention kernel (RT, variant), 0 if there is none
-int fa_variant_head_dim(int RT, int variant);
+// head dim served by full-attention kernel (RT, variant) for the cache format, 0 if there is none
+int fa_variant_head_dim(int RT, int variant, bool kv8);
 // workgroups of the full-attention kernel (RT, variant) resident per compute
 // unit on the current device (0 if that kernel does not exist)
 hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs);
