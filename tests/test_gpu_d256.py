@@ -99,3 +99,11 @@ def test_d256_strided_cache_layout():
     CK.check_out(CK.bf16_bits_to_f64(host_bits(out)), ref["out"])
     CK.check_idx(idx.cpu().numpy(), ref["idx"], ref["P"], inp.lens, C, w.window)
     CK.check_out(CK.bf16_bits_to_f64(host_bits(sa)), O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"]))
+
+
+@pytest.mark.parametrize("variant", [6, 8])
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_d256_both_kernel_shapes(variant, kv, monkeypatch):
+    """Four row tiles: the 16-token / 3-stage and the 32-token / 2-stage kernels."""
+    monkeypatch.setenv("HS2_FA_VARIANT", str(variant))
+    parity_case(SMALL[0], seed=27, kv=kv)
