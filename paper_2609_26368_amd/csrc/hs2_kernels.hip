@@ -595,14 +595,17 @@ __device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g,
 template <int RT, int GP, bool KV8 = false, int HDIM = HD>
 struct PoolShape {
   static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
-  static constexpr int RPW = RT == 1 ? 1 : (TPQ > 2 ? TPQ : 2);  // row tiles per wave
+  // row tiles per wave: a query's tiles stay in one wave (its heads are
+  // summed in registers); one tile per wave otherwise (more waves per
+  // workgroup share each staged tile: 134 -> 126 us at 64 rows per KV head)
+  static constexpr int RPW = RT == 1 ? 1 : TPQ;
   static constexpr int NWV = RT / RPW;
   static constexpr int SRB = 2 * HDIM;                        // bytes of a bf16 stage row
   static constexpr int RB = KV8 ? HDIM : SRB;                 // bytes of a staged row
   static constexpr int RPL = 1024 / RB;                       // rows per 1 KB load
   // whole 1 KB loads for every wave: at least 16 rows, RPL NWV when more
   static constexpr int TW = RPL * NWV > 16 ? RPL * NWV : 16;
-  static constexpr int NS = HDIM > 128 ? 3 : 4;
+  static constexpr int NS = 3;
   static constexpr int SB = TW * RB;                          // ring stage
   static constexpr int TB = KV8 ? TW * SRB : 0;               // converted tile
   static constexpr int LDS = NS * SB + TB;                    // before the histograms
