@@ -1632,8 +1632,8 @@ hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// sparse-attention ring kernels: (RT, waves) per head dim; 16-row stages x 4
-constexpr int SAR_TW = 16, SAR_NS = 4;
+// sparse-attention ring kernels: (RT, waves) per head dim; 16-row stages x 2
+constexpr int SAR_TW = 16, SAR_NS = 2;
 #define HS2_SA_SHAPES(X) X(1, 1, 128) X(2, 1, 128) X(4, 2, 128) X(1, 1, 256) X(2, 2, 256) X(4, 4, 256)
 
 hipError_t set_pool_smem_limits() {
