@@ -1,16 +1,23 @@
 // HIP kernels of the hybrid-block decode path (gfx950).
 //
-//   k_fa_split   full attention, split-KV flash decode: per (sequence, KV head,
-//                token split) partial (m, l, O) of every query row of the group
-//   k_combine    merge of the partials -> bf16 output and (M, Z) per query row
-//   k_pool       re-reads K, recomputes the same logits, turns them into exact
-//                probabilities with the merged (M, Z) and sums them over the
-//                query heads of the KV head -> pooled score per candidate token;
-//                builds the first-level radix histogram of the scores
-//   k_sel_*      top-k outside the window (radix select on the score keys,
-//                ties to the lower index) + window union + ascending emission
-//   k_sa_split   sparse attention over gathered selected rows (same partial
-//                format, merged by k_combine)
+//   k_fa_ring     full attention, split-KV flash decode through per-token-group
+//                 LDS rings (bf16 or E4M3 cache, head dim 128 or 256): per
+//                 (sequence, KV head, token split) a partial (m, l, O) of every
+//                 query row of the group; optionally each row's logits
+//   k_fa_split    the same with 64-row stages shared by 4 or 8 waves (up to
+//                 128 query rows per KV head, bf16, head dim 128)
+//   k_combine     merge of the partials -> bf16 output and (M, Z) per query
+//                 row (sparse layers: sink logits, output gates)
+//   k_pool        re-reads K, recomputes the same logits, turns them into exact
+//                 probabilities with the merged (M, Z) and sums them over the
+//                 query heads of the KV head -> pooled score per candidate
+//                 token; builds the first-level radix histogram of the scores
+//   k_pool_logits the same scores from the stored logits (few query rows)
+//   k_sel_*       top-k outside the window (radix select on the score keys,
+//                 ties to the lower index) + window union + ascending emission
+//   k_block_*     block-level selection (block score keys, top blocks, emission)
+//   k_sa_ring     sparse attention over gathered selected rows (same partial
+//                 format, merged by k_combine)
 //
 // Query rows of one (sequence, KV head) group are laid out query-major:
 // row r = c * Gp + h with Gp = G rounded up to a power of two; rows with
