@@ -68,6 +68,8 @@ def parse():
                     help="cache format: bf16, or OCP E4M3 bytes with one scale per KV head (the _fp8 entry points)")
     ap.add_argument("--block", type=int, default=0,
                     help="block-level selection with blocks of this many tokens (hs2_full_attn_score_select_blocks)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time its replays (no per-kernel host launches)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -180,21 +182,32 @@ def main():
         sinks = [torch.randn(Hq, generator=g).to(dev) for _ in q_sa]
         gates = [torch.randn((B, C, Hq, D), generator=g).to(torch.bfloat16).to(dev) for _ in q_sa]
 
-    def step():
-        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=stream, kv_scales=kv_scales, block=args.block)
+    def step_on(st):
+        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=st, kv_scales=kv_scales, block=args.block)
         for qs, o, sk, gt in zip(q_sa, sa_out, sinks, gates):
-            blk.sparse(qs, K, V, lens, idx, out=o, stream=stream, sink=sk, gate=gt, kv_scales=kv_scales)
+            blk.sparse(qs, K, V, lens, idx, out=o, stream=st, sink=sk, gate=gt, kv_scales=kv_scales)
+
+    def step():
+        step_on(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done")
+    run_step = step
+    if args.graph:  # one step captured after the warmup (the library's set-up is done by then)
+        graph, cap = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.graph(graph, stream=cap):
+            step_on(cap)
+        torch.cuda.synchronize()
+        run_step = graph.replay
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        step()
+        run_step()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -247,6 +260,7 @@ def main():
                       "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles,
                       "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
                       "selection": f"block{args.block}" if args.block else "token",
+                      "launch": "graph" if args.graph else "eager",
                       **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
