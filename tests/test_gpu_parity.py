@@ -164,6 +164,22 @@ def test_parity_edges(name, B, ctx, ctx_min, C, k, win):
     parity_case(w, seed=7)
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_parity_len_below_chunk(kv):
+    """Outside the precondition len >= C: queries at negative positions get an
+    all -1 row, a zero output and (M, Z) = (-inf, 0); len = 0 sequences too."""
+    w = W.Workload("len_below_chunk", 3, 300, 4, 16, 2, 128, 16, 8, 1, ctx_min=100)
+    inp = W.make_inputs(w, seed=13, kv=kv)
+    inp.lens[:] = [2, 0, 300]
+    note(f"[parity] len_below_chunk kv={kv} lens={inp.lens.tolist()}")
+    ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, k_scale=inp.k_scale,
+                                   v_scale=inp.v_scale)
+    gpu = run_gpu(inp, oracle_idx=ref["idx"])
+    compare(inp, ref, gpu)
+    assert (gpu["idx"][1] == -1).all() and (gpu["out"][1] == 0).all()
+    assert (gpu["idx"][0, :, :2] == -1).all() and (gpu["out"][0, :2] == 0).all()
+
+
 def test_parity_padded_capacity():
     """Cache capacity larger than every length (rows past len are never read)."""
     w = W.Workload("capacity", 3, 1000, 2, 16, 4, 128, 96, 32, 1, ctx_min=300)
