@@ -70,6 +70,8 @@ def parse():
                     help="block-level selection with blocks of this many tokens (hs2_full_attn_score_select_blocks)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time its replays (no per-kernel host launches)")
+    ap.add_argument("--cold", action="store_true",
+                    help="evict the caches (read a 1 GiB buffer) before every step; steps timed one by one")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -202,20 +204,42 @@ def main():
             step_on(cap)
         torch.cuda.synchronize()
         run_step = graph.replay
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        run_step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ev_ms = e0.elapsed_time(e1)
-    ms_per_step = ev_ms / args.steps
     tokens = B * C
-    value = tokens * args.steps / wall
-    log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms")
+    # evicting by reading 1 GiB (a write would leave dirty lines whose
+    # write-back then overlaps the timed step)
+    flush = torch.ones(1 << 28, dtype=torch.int32, device=dev) if args.cold else None
+    if not args.cold:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev_ms = e0.elapsed_time(e1)
+        ms_per_step = ev_ms / args.steps
+        value = tokens * args.steps / wall
+        log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms")
+
+    # one event pair per step: percentiles (and, cold, the timing itself: the
+    # cache-evicting write before each step stays outside its events)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for a_, b_ in ev:
+        if flush is not None:
+            flush.amax()
+        a_.record(stream)
+        run_step()
+        b_.record(stream)
+    torch.cuda.synchronize()
+    per_step = np.array([a_.elapsed_time(b_) for a_, b_ in ev])
+    if args.cold:
+        ms_per_step = float(per_step.mean())
+        value = tokens / (ms_per_step * 1e-3)
+        log(f"[bench] timed {args.steps} cold steps: {ms_per_step:.4f} ms mean")
+    pct = {f"p{q}": round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)}
 
     # per-kernel durations (HIP events recorded by the library around each launch, same stream)
     hs2.hs2_timing_enable(True)
@@ -261,10 +285,12 @@ def main():
                       "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
                       "selection": f"block{args.block}" if args.block else "token",
                       "launch": "graph" if args.graph else "eager",
+                      "caches": "evicted before every step" if args.cold else "as left by the previous step",
                       **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
            "roofline": roofline,
+           "step_ms_percentiles": pct,
            "kernels_avg_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
            "cpu_baseline": cpu}
     print(json.dumps(rec), flush=True)
