@@ -436,6 +436,25 @@ __device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char
   }
 }
 
+// Raw E4M3 rows of RB bytes are staged swizzled too (chunk c of row r at
+// position c ^ raw_swz<RB>(r)) so that the 8-byte K-operand reads of 16 rows
+// hit distinct banks: two 128-byte rows share a 256-byte bank line.
+template <int RB>
+__device__ __host__ constexpr int raw_swz(int r) {
+  return RB == 128 ? (r >> 1) & 7 : r & 15;
+}
+
+// K operand of the logits MFMA (16x16x32: row `row`, the 8 values d =
+// 8 (lane / 16) + 32 kk .. + 7) straight from a raw E4M3 stage, converted to
+// bf16 in registers.
+template <int RB>
+__device__ inline uint4 k_operand_e4m3(const unsigned char* raw, int row, int kk, int lane) {
+  const int c = (lane >> 5) + 2 * kk;  // 16-byte chunk
+  const uint2 v = *(const uint2*)(raw + row * RB + 16 * (c ^ raw_swz<RB>(row)) + 8 * ((lane >> 4) & 1));
+  const uint2 lo = e4m3x4_to_bf16x4(v.x), hi = e4m3x4_to_bf16x4(v.y);
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
 // s_waitcnt vmcnt(per_stage * stages) for stages in [0, 5] (larger values
 // wait as for 5; counts above the 6-bit field wait for 63: both only wait
 // longer than needed)

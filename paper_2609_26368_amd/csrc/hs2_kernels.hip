@@ -597,8 +597,8 @@ __device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g,
 // own query row tiles held in registers.  Dynamic LDS: ring + C packed
 // first-level histograms (16-bit counters; a split has < 65536 tokens).
 // KV8: E4M3 cache with one K scale per KV head (folded into the logit
-// scale); raw rows are staged and converted like in k_fa_ring.  HDIM: head
-// dim (128 or 256).
+// scale); raw rows are staged (swizzled by raw_swz) and each wave converts
+// its K operands in registers.  HDIM: head dim (128 or 256).
 template <int RT, int GP, bool KV8 = false, int HDIM = HD>
 struct PoolShape {
   static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
@@ -614,8 +614,7 @@ struct PoolShape {
   static constexpr int TW = RPL * NWV > 16 ? RPL * NWV : 16;
   static constexpr int NS = 3;
   static constexpr int SB = TW * RB;                          // ring stage
-  static constexpr int TB = KV8 ? TW * SRB : 0;               // converted tile
-  static constexpr int LDS = NS * SB + TB;                    // before the histograms
+  static constexpr int LDS = NS * SB;                         // before the histograms
 };
 template <int RT, int GP, bool KV8, int HDIM>
 __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
@@ -627,7 +626,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   constexpr int LPM = TW * RB / 1024 / NWV;  // 1 KB loads per stage per wave
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* tile_p = smem + NS * SB;            // KV8: the converted tile
   uint32_t* hist = (uint32_t*)(smem + PS::LDS);       // [C][NBINS/2]
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -655,7 +653,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   const uint32_t ring = lds_addr(smem);
   constexpr int RPL = PS::RPL;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * (lane % CPR)
+    return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
                : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
   };
   int64_t lane_off[LPM];
@@ -701,19 +699,20 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     if (NWV > 1) __syncthreads();
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = smem + (i % NS) * SB;
-    if constexpr (KV8) {
-      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_p, tid);
-      if (NWV > 1) __syncthreads();
-      stg = tile_p;
-    }
     const int t0 = t_begin + i * TW;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
       const int row = 16 * bi + (lane & 15);
-      const unsigned char* rp = stg + row * SRB;
       uint4 k4[NKK];
+      if constexpr (KV8) {
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+        for (int kk = 0; kk < NKK; ++kk) k4[kk] = k_operand_e4m3<RB>(stg, row, kk, lane);
+      } else {
+        const unsigned char* rp = stg + row * SRB;
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+          k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+      }
       f32x4 acc[RPW];
 #pragma unroll
       for (int rr = 0; rr < RPW; ++rr) {
