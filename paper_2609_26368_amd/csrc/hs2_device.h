@@ -414,28 +414,6 @@ __device__ inline uint2 e4m3x4_to_bf16x4(uint32_t w) {
   return make_uint2(lo, hi);
 }
 
-// Convert NR staged E4M3 rows (raw, HDIM bytes each) into bf16 stage rows at
-// stg (2 HDIM bytes; chunk c of row r at position c ^ (r & 15)); threads tid
-// of NTHR.  A job is one 16-byte raw piece: 16 values, two bf16 chunks.
-template <int NR, int NTHR, int HDIM = HD>
-__device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
-  constexpr int PPR = HDIM / 16;  // raw pieces per row
-  constexpr int JOBS = NR * PPR;
-#pragma unroll
-  for (int k = 0; k < (JOBS + NTHR - 1) / NTHR; ++k) {
-    const int j = tid + k * NTHR;
-    if (JOBS % NTHR == 0 || j < JOBS) {
-      const int r = j / PPR, p = j % PPR;
-      const uint4 v = *(const uint4*)(raw + r * HDIM + 16 * p);
-      const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
-      const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
-      unsigned char* rp = stg + r * (2 * HDIM);
-      *(uint4*)(rp + 16 * ((2 * p) ^ (r & 15))) = make_uint4(a.x, a.y, b.x, b.y);
-      *(uint4*)(rp + 16 * ((2 * p + 1) ^ (r & 15))) = make_uint4(c.x, c.y, d.x, d.y);
-    }
-  }
-}
-
 // Raw E4M3 rows of RB bytes are staged swizzled too (chunk c of row r at
 // position c ^ raw_swz<RB>(r)) so that the 8-byte K-operand reads of 16 rows
 // hit distinct banks: two 128-byte rows share a 256-byte bank line.
@@ -453,6 +431,62 @@ __device__ inline uint4 k_operand_e4m3(const unsigned char* raw, int row, int kk
   const uint2 v = *(const uint2*)(raw + row * RB + 16 * (c ^ raw_swz<RB>(row)) + 8 * ((lane >> 4) & 1));
   const uint2 lo = e4m3x4_to_bf16x4(v.x), hi = e4m3x4_to_bf16x4(v.y);
   return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+// Logits of the 16 rows of block blk of a raw E4M3 stage against RPW row
+// tiles of queries (as qk_block_swz, K converted in registers).
+template <int RPW, int RB, int NKK>
+__device__ inline void qk_block_e4m3(const unsigned char* raw, int blk, const uint4 (&q)[RPW][NKK], f32x4 (&S)[RPW],
+                                     int lane) {
+  const int row = 16 * blk + (lane & 15);
+  uint4 a4[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) a4[kk] = k_operand_e4m3<RB>(raw, row, kk, lane);
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) acc = mfma_k32(a4[kk], q[rr][kk], acc);
+    S[rr] = acc;
+  }
+}
+
+// LDS of a full-attention ring kernel: per token group an NS-stage ring of
+// TW K rows and TW V rows (bf16: 2 hd bytes a row; E4M3: hd bytes, plus one
+// converted bf16 V tile); at least the end-of-split merge of TGW groups.
+__device__ __host__ constexpr int fa_ring_group_bytes(int tw, int ns, bool kv8, int hd) {
+  return ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? tw * 2 * hd : 0);
+}
+__device__ __host__ constexpr int fa_ring_merge_bytes(int rt, int tgw, int hd) {
+  return tgw > 1 ? tgw * 16 * rt * 16 + (tgw - 1) * 16 * rt * hd * 4 : 0;
+}
+__device__ __host__ constexpr int fa_ring_lds_bytes(int rt, int tw, int ns, int tgw, bool kv8, int hd) {
+  return tgw * fa_ring_group_bytes(tw, ns, kv8, hd) > fa_ring_merge_bytes(rt, tgw, hd)
+             ? tgw * fa_ring_group_bytes(tw, ns, kv8, hd)
+             : fa_ring_merge_bytes(rt, tgw, hd);
+}
+
+// Convert NR staged E4M3 rows (raw, HDIM bytes each, chunk c of row r at
+// position c ^ raw_swz(r)) into bf16 stage rows at stg (2 HDIM bytes; chunk c
+// of row r at position c ^ (r & 15)); threads tid of NTHR.  A job is one
+// 16-byte raw piece: 16 values, two bf16 chunks.
+template <int NR, int NTHR, int HDIM = HD>
+__device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
+  constexpr int PPR = HDIM / 16;  // raw pieces per row
+  constexpr int JOBS = NR * PPR;
+#pragma unroll
+  for (int k = 0; k < (JOBS + NTHR - 1) / NTHR; ++k) {
+    const int j = tid + k * NTHR;
+    if (JOBS % NTHR == 0 || j < JOBS) {
+      const int r = j / PPR, p = j % PPR;
+      const uint4 v = *(const uint4*)(raw + r * HDIM + 16 * (p ^ raw_swz<HDIM>(r)));
+      const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
+      const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
+      unsigned char* rp = stg + r * (2 * HDIM);
+      *(uint4*)(rp + 16 * ((2 * p) ^ (r & 15))) = make_uint4(a.x, a.y, b.x, b.y);
+      *(uint4*)(rp + 16 * ((2 * p + 1) ^ (r & 15))) = make_uint4(c.x, c.y, d.x, d.y);
+    }
+  }
 }
 
 // s_waitcnt vmcnt(per_stage * stages) for stages in [0, 5] (larger values

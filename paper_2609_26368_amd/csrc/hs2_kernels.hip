@@ -160,8 +160,11 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // partial (m, l, O) per split.
 // KV8: the cache is E4M3 bytes with one scale per KV head (k_scale folds
 // into the logit scale, v_scale is applied by the merge); each token group
-// stages raw rows in its ring and converts the current tile into one bf16
-// tile before computing on it.  HDIM: head dim (128 or 256).
+// stages raw rows in its ring (swizzled by raw_swz), reads the K operands
+// raw and converts them in registers, and converts the V rows of the
+// current tile into one bf16 tile (before the logits, so that the
+// conversion overlaps them; one barrier before P.V).  HDIM: head dim (128
+// or 256).
 template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
@@ -172,12 +175,9 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int CPR = RB / 16;                             // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;                // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * RB;                          // ring stage: K rows then V rows
-  constexpr int TB = KV8 ? 2 * TW * SRB : 0;               // converted bf16 tile
-  constexpr int GB = NS * SB + TB;                         // LDS of one token group
+  constexpr int GB = fa_ring_group_bytes(TW, NS, KV8, HDIM);  // LDS of one token group: ring + V tile
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads for every wave and stage");
   static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
-  static_assert(TGW == 1 || TGW * 16 * RT * 16 + (TGW - 1) * 16 * RT * HDIM * 4 <= TGW * GB,
-                "the merge fits in the rings");
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
@@ -210,7 +210,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * GB);
   unsigned char* ring_p = smem + tg * GB;
-  unsigned char* tile_p = ring_p + NS * SB;  // KV8: the converted tile
+  unsigned char* tile_p = ring_p + NS * SB;  // KV8: the converted V tile
   // logits output of a single row tile (C G <= 16 query rows): this lane's
   // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
   float* lrow = nullptr;
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   // swizzled, E4M3 rows raw
   constexpr int RPL = 1024 / RB;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * (lane % CPR)
+    return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
                : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
   };
   int64_t lane_off[LPM];
@@ -266,16 +266,20 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     if (NWV * TGW > 1) __syncthreads();
     if (i < ntiles && i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = ring_p + (i % NS) * SB;
-    if constexpr (KV8) {
-      if (i < ntiles) convert_rows_e4m3<2 * TW, 64 * NWV, HDIM>(stg, tile_p, 64 * wave + lane);
-      if (NWV * TGW > 1) __syncthreads();  // every group's tile converted
-      stg = tile_p;
+    if (i >= ntiles) {
+      if (KV8 && NWV * TGW > 1) __syncthreads();  // the other groups' V-tile barrier
+      continue;
     }
-    if (i >= ntiles) continue;
+    if constexpr (KV8) convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_p, 64 * wave + lane);
     const int t0 = t_begin + i * TW;
     f32x4 S[NB][RPW];
 #pragma unroll
-    for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    for (int bi = 0; bi < NB; ++bi) {
+      if constexpr (KV8)
+        qk_block_e4m3<RPW, RB>(stg, bi, q, S[bi], lane);
+      else
+        qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    }
     if constexpr (RT == 1) {  // the lane's 4 consecutive tokens; the row stride covers whole tiles
       if (lrow)
 #pragma unroll
@@ -297,7 +301,8 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         }
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
-    const unsigned char* vbase = stg + TW * SRB;
+    if (KV8 && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
+    const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
@@ -1303,10 +1308,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   constexpr int CPR = RB / 16;                  // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;
   constexpr int SB = 2 * TW * RB;
-  constexpr int TB = KV8 ? 2 * TW * SRB : 0;    // converted tile
+  constexpr int TB = KV8 ? TW * SRB : 0;        // converted V tile
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* tile_p = smem + NS * SB;                  // KV8: the converted tile
+  unsigned char* tile_p = smem + NS * SB;                  // KV8: the converted V tile
   int32_t* sidx = (int32_t*)(smem + NS * SB + TB);        // [split_slots]
 
   const int split = blockIdx.x;
@@ -1361,7 +1366,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
       const int row = RPL * n + lane / CPR;
       const int t = sidx[tile * TW + row];
       const int64_t off = (int64_t)(t < 0 ? 0 : t) * stride_t +
-                          (KV8 ? 16 * (lane % CPR) : 16 * ((lane % CPR) ^ (row & 15)));
+                          (KV8 ? 16 * ((lane % CPR) ^ raw_swz<RB>(row)) : 16 * ((lane % CPR) ^ (row & 15)));
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
       dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
       const uint64_t bal = __ballot(t >= 0);  // lanes CPR j .. hold row RPL n + j
@@ -1390,10 +1395,8 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
         if (k == (i + NS - 1) % NS) vmask[k] = mnew;
     }
     const unsigned char* stg = smem + (i % NS) * SB;
-    if constexpr (KV8) {  // converted tile complete at the barrier below (one wave: in order)
-      convert_rows_e4m3<2 * TW, 64 * NWV, HDIM>(stg, tile_p, threadIdx.x);
-      stg = tile_p;
-    }
+    if constexpr (KV8)  // V tile complete at the barrier below (one wave: in order); K is read raw
+      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_p, threadIdx.x);
     if (NWV > 1) {  // every wave's row bits
       __shared__ uint32_t s_mask[NWV];
       if (lane == 0) s_mask[wave] = m_i;
@@ -1404,7 +1407,12 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
     }
     f32x4 S[NB][RPW];
 #pragma unroll
-    for (int bi = 0; bi < NB; ++bi) qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    for (int bi = 0; bi < NB; ++bi) {
+      if constexpr (KV8)
+        qk_block_e4m3<RPW, RB>(stg, bi, q, S[bi], lane);
+      else
+        qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
+    }
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
@@ -1416,7 +1424,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
         }
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
-    const unsigned char* vbase = stg + TW * SRB;
+    const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
@@ -1490,10 +1498,8 @@ static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t
   return e;
 }
 
-// LDS of a full-attention ring kernel: per token group the ring of raw rows
-// (bf16 2 hd bytes or E4M3 hd bytes) and, for E4M3, one converted bf16 tile
-constexpr size_t fa_ring_lds(int tw, int ns, int tgw, bool kv8, int hd) {
-  return (size_t)tgw * ((size_t)ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? 2 * tw * 2 * hd : 0));
+constexpr size_t fa_ring_lds(int rt, int tw, int ns, int tgw, bool kv8, int hd) {
+  return (size_t)fa_ring_lds_bytes(rt, tw, ns, tgw, kv8, hd);
 }
 
 template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
@@ -1503,7 +1509,7 @@ hipError_t fa_ring_occupancy(int* wgs) {
     return hipSuccess;
   } else {
     return occupancy_capped(wgs, (const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>, 64 * NWV * TGW,
-                            fa_ring_lds(TW, NS, TGW, KV8, HDIM));
+                            fa_ring_lds(RT, TW, NS, TGW, KV8, HDIM));
   }
 }
 
@@ -1513,7 +1519,7 @@ hipError_t fa_ring_launch(const FaArgs& a, dim3 grid, hipStream_t s) {
     return hipErrorInvalidValue;
   } else {
     HS2_LAUNCH((k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>), grid, dim3(64 * NWV * TGW),
-               fa_ring_lds(TW, NS, TGW, KV8, HDIM), s, a);
+               fa_ring_lds(RT, TW, NS, TGW, KV8, HDIM), s, a);
     return hipGetLastError();
   }
 }
@@ -1718,7 +1724,7 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
 }
 
 size_t sa_smem_bytes(int split_slots, bool kv8, int hd) {
-  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? hd : 2 * hd) + (kv8 ? 2 * SAR_TW * 2 * hd : 0) +
+  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? hd : 2 * hd) + (kv8 ? SAR_TW * 2 * hd : 0) +
          sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
 }
 
