@@ -1443,10 +1443,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
 // Full attention kernel variants (the planner's defaults: head dim 128 with
-// RT = 1 -> 2 (E4M3: 9), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1; head dim
+// RT = 1 -> 2 (E4M3: 3), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1; head dim
 // 256 with RT = 4 -> 8, else 6):
 //   1: workgroup kernel (64-row stages shared by 4 or 8 waves), head dim 128
-//   0, 2, 3, 5, 7, 9: ring kernels of head dim 128; 6, 8: head dim 256
+//   0, 2, 3, 5, 7: ring kernels of head dim 128; 6, 8: head dim 256
 // Columns: variant, RT, waves per token group, stage rows, stages, token
 // groups, head dim.
 #define HS2_RING_VARIANTS(X)                                                        \
@@ -1455,8 +1455,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   X(3, 1, 1, 16, 3, 1, 128) X(3, 2, 1, 16, 3, 1, 128) X(3, 4, 2, 16, 3, 1, 128)     \
   X(5, 1, 1, 32, 3, 1, 128) X(5, 2, 1, 16, 3, 2, 128) X(5, 4, 2, 16, 3, 2, 128)     \
   X(6, 1, 1, 16, 3, 1, 256) X(6, 2, 2, 16, 3, 1, 256) X(6, 4, 4, 16, 3, 1, 256)     \
-  X(7, 2, 2, 32, 2, 2, 128) X(7, 4, 4, 32, 2, 2, 128) X(8, 4, 4, 32, 2, 1, 256)     \
-  X(9, 1, 1, 16, 2, 1, 128)
+  X(7, 2, 2, 32, 2, 2, 128) X(7, 4, 4, 32, 2, 2, 128) X(8, 4, 4, 32, 2, 1, 256)
 
 // a ring shape serves a cache format only if every wave loads whole 1 KB
 // pieces of each stage (the kernel asserts it; other shapes are never built)

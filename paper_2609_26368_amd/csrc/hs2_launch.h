@@ -101,7 +101,7 @@ struct SaArgs {
   int hd;                // head dim (128 or 256)
 };
 
-constexpr int kFaVariants = 10;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
+constexpr int kFaVariants = 9;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
 int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
 // head dim served by full-attention kernel (RT, variant) for the cache format, 0 if there is none
