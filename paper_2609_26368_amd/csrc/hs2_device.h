@@ -1,8 +1,9 @@
 // Device-side building blocks shared by the hybrid-block kernels (gfx950 only).
 //
-// Tile scheme: a workgroup of 256 threads (4 waves of 64) stages 64 cache rows
-// at a time in LDS: K row-major (padded rows) and V transposed (Vt[d][row]),
-// so that both MFMA operands of P.V can be read with plain LDS loads.
+// Staging: cache rows go global -> LDS by 16-byte direct-to-LDS loads (no
+// register staging), row-major, 16-byte chunks swizzled by the row index so
+// that the MFMA K-operand reads and the transposing V reads
+// (ds_read_b64_tr_b16) need no padding; E4M3 rows are staged raw.
 //
 // MFMA lane layouts used (checked on gfx950):
 //   16x16x32 bf16: lane l supplies A[l%16][8(l/16)+j] and B[8(l/16)+j][l%16],
@@ -22,22 +23,13 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int HD = 128;         // head dim of the workgroup kernel; the ring kernels take theirs as a parameter
-constexpr int TILE = 64;        // cache rows per LDS stage
-constexpr int NT = 256;         // threads per workgroup
-constexpr int KPAD = HD + 8;    // K / Q row stride in LDS (bf16): 272 B, conflict-free 16-B reads
-constexpr int VPAD = TILE + 4;  // Vt row stride in LDS (bf16): 136 B
+constexpr int TILE = 64;        // cache rows per LDS stage of the workgroup kernel
+constexpr int NT = 256;         // threads per workgroup of the score and histogram kernels
 constexpr int SEL_CHUNK = 4096;  // tokens per workgroup of the selection scans
 constexpr int NBINS = 1024;     // first-level radix bins of the pooled-score keys
 constexpr int DIGIT_SHIFT = 19; // key >> 19 = 8 exponent bits + 4 mantissa bits (1/16 binade)
 constexpr int DIGIT_BASE = 1120;// (exp 133, mant 15) -> bin 1023: 64 binades below 128 > P;
                                 // P < 2^-56 all fall into bin 0
-
-struct TileLds {
-  uint16_t k[TILE * KPAD];
-  uint16_t vt[HD * VPAD];
-  int32_t tok[TILE];  // token held by each tile row, -1 if none (gathered tiles)
-};
-constexpr size_t KTILE_BYTES = sizeof(uint16_t) * TILE * KPAD;  // the K part alone
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
@@ -74,59 +66,6 @@ __device__ inline uint32_t score_key(float p) {
 __device__ inline int score_digit(uint32_t key) {
   int d = (int)(key >> DIGIT_SHIFT) - DIGIT_BASE;
   return d < 0 ? 0 : (d >= NBINS ? NBINS - 1 : d);
-}
-
-// ---------------------------------------------------------------- tile staging
-// Thread tid owns four 16-byte chunks of the 64 x 16 chunk grid of a tile:
-// column group cg = tid & 15, rows row_of(tid, u), u = 0..3.  Rows come in
-// adjacent pairs (u = 0, 1 and u = 2, 3) so V can be stored transposed two
-// tokens (one 32-bit word) at a time.  Every 16 lanes read one full 256-byte
-// cache row: loads are fully coalesced.
-__device__ inline int row_of(int tid, int u) { return 2 * (tid >> 4) + (u & 1) + 32 * (u >> 1); }
-
-struct TileRegs {
-  uint4 k[4];
-  uint4 v[4];
-};
-
-// Load the K and V rows of tokens tok[u] (tok < 0: zeros) of one (b, g) cache.
-template <bool WITH_V>
-__device__ inline void load_tile(TileRegs& r, const uint16_t* __restrict__ Kbg, const uint16_t* __restrict__ Vbg,
-                                 int64_t stride_t, const int (&tok)[4], int cg) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    if (tok[u] >= 0) {
-      const int64_t off = (int64_t)tok[u] * stride_t + cg * 8;
-      r.k[u] = *(const uint4*)(Kbg + off);
-      if (WITH_V) r.v[u] = *(const uint4*)(Vbg + off);
-    } else {
-      r.k[u] = make_uint4(0, 0, 0, 0);
-      if (WITH_V) r.v[u] = make_uint4(0, 0, 0, 0);
-    }
-  }
-}
-
-template <bool WITH_V>
-__device__ inline void store_tile(TileLds& s, const TileRegs& r, int tid) {
-  const int cg = tid & 15;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) *(uint4*)&s.k[row_of(tid, u) * KPAD + cg * 8] = r.k[u];
-  if (WITH_V) {
-#pragma unroll
-    for (int pr = 0; pr < 2; ++pr) {
-      const int row = row_of(tid, 2 * pr);  // even row; row + 1 is its pair
-      const uint32_t* a = (const uint32_t*)&r.v[2 * pr];
-      const uint32_t* b = (const uint32_t*)&r.v[2 * pr + 1];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // word w of a chunk holds elements d = cg*8 + 2w (low half) and +1 (high half)
-        const uint32_t lo = (a[w] & 0xFFFFu) | (b[w] << 16);
-        const uint32_t hi = (a[w] >> 16) | (b[w] & 0xFFFF0000u);
-        *(uint32_t*)&s.vt[(cg * 8 + 2 * w) * VPAD + row] = lo;
-        *(uint32_t*)&s.vt[(cg * 8 + 2 * w + 1) * VPAD + row] = hi;
-      }
-    }
-  }
 }
 
 // ---------------------------------------------------------------- wave-level attention state
@@ -170,23 +109,6 @@ struct WaveState {
     }
   }
 };
-
-// Logits of the 16 tile rows of block `blk` against RPW row tiles of queries
-// (B operands in registers): S[rr][i] = <K[16 blk + 4(lane/16) + i], Q[row lane&15]>.
-template <int RPW>
-__device__ inline void qk_block(const TileLds& s, int blk, const uint4 (&q)[RPW][4], f32x4 (&S)[RPW], int lane) {
-  const uint16_t* kp = &s.k[(16 * blk + (lane & 15)) * KPAD + 8 * (lane >> 4)];
-  uint4 a[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) a[kk] = *(const uint4*)(kp + 32 * kk);
-#pragma unroll
-  for (int rr = 0; rr < RPW; ++rr) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) acc = mfma_k32(a[kk], q[rr][kk], acc);
-    S[rr] = acc;
-  }
-}
 
 // Online-softmax update of a wave's state with BPW blocks of log2-domain
 // logits (masked = -inf); returns the bf16 probabilities as P.V A operands.
@@ -236,24 +158,6 @@ __device__ inline void online_softmax(WaveState<RPW, HDIM>& st, f32x4 (&S)[BPW][
   }
 }
 
-// Online softmax + O += P . V with V transposed in LDS (Vt[d][row]).
-template <int RPW, int BPW>
-__device__ inline void softmax_pv(WaveState<RPW>& st, const TileLds& s, const int (&blk)[BPW],
-                                  f32x4 (&S)[BPW][RPW], int lane) {
-  uint2 pa[BPW][RPW];
-  online_softmax<RPW, BPW>(st, S, pa, lane);
-#pragma unroll
-  for (int bi = 0; bi < BPW; ++bi) {
-    const uint16_t* vp = &s.vt[(lane & 15) * VPAD + 16 * blk[bi] + 4 * (lane >> 4)];
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      const uint2 vb = *(const uint2*)(vp + 16 * nb * VPAD);
-#pragma unroll
-      for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
-    }
-  }
-}
-
 // Write one wave's partial for its RPW row tiles: (m ref, l, m true, 0) and O
 // (rows of HDIM floats).
 template <int RPW, int HDIM>
@@ -287,8 +191,6 @@ constexpr int STAGE_KV_BYTES = TILE * STAGE_ROW_BYTES;  // 16 KB
 constexpr int STAGE_BYTES = 2 * STAGE_KV_BYTES;         // K + V
 constexpr int FA_STAGES = 4;
 
-typedef __attribute__((address_space(3))) void* lds_void_ptr;
-typedef __attribute__((address_space(1))) const void* global_cvoid_ptr;
 typedef short i16x4_lds __attribute__((ext_vector_type(4)));
 
 // NW waves share the loads of a stage: LPW = 16 / NW loads of 1 KB per
