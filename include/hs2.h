@@ -42,6 +42,14 @@
  *     n_queries <= len[b] <= max_len.  The kernels clamp len[b] to
  *     [0, max_len]; a query whose position is negative gets an all -1 index
  *     row and a zero output.
+ *
+ * Planner overrides (environment, read on every call; for tests and tuning,
+ * invalid values fall back to the planner's choice): HS2_FA_VARIANT
+ * (full-attention kernel shape), HS2_FA_SPLIT / HS2_POOL_SPLIT /
+ * HS2_SA_SPLIT (tokens or slots per workgroup), HS2_FA_ROUNDS (workgroup
+ * rounds the full-attention splits are sized for), HS2_POOL_FROM_K=1
+ * (recompute the scores from K even where the stored logits would serve).
+ * None changes a result beyond floating-point summation order.
  */
 #ifndef HS2_H
 #define HS2_H
