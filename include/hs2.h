@@ -83,8 +83,7 @@ typedef struct hs2_dims {
   int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, G = Hq / Hkv <= 64,            */
                        /*   C * (G rounded up to a power of two) <= 128           */
   int32_t head_dim;    /* D: 128, or 256 (the paper's head dim, Sec. "Experimental */
-                       /*   Setup") with C * pow2(G) <= 64; other values and      */
-                       /*   larger groups: HS2_ERR_UNSUPPORTED                     */
+                       /*   Setup"); other values: HS2_ERR_UNSUPPORTED            */
   int32_t max_len;     /* Lmax: cache capacity per sequence, 1 .. 2^27 tokens     */
   int64_t kv_stride_b; /* elements; multiple of 8                                 */
   int64_t kv_stride_h; /* elements; multiple of 8                                 */
@@ -169,8 +168,6 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
  *            (HS2_ERR_ALIGN), K8 and V8 16-byte aligned
  *   k_scale, v_scale  [Hkv] float (device, 4-byte aligned), both required
  *            (HS2_ERR_NULL); finite and > 0 for meaningful results
- *   n_queries * (G rounded up to a power of two) must be <= 64
- *            (HS2_ERR_UNSUPPORTED above that)
  * Other arguments, outputs, ownership and errors as for
  * hs2_full_attn_score_select and hs2_sparse_attn_ex respectively; the same
  * hs2_workspace_bytes() covers both cache formats.                            */

@@ -96,9 +96,6 @@ hs2_status check_dims(const hs2_dims* d) {
   if (d->n_queries * next_pow2(G) > kMaxRows)
     return fail(HS2_ERR_UNSUPPORTED, "n_queries * pow2(G) = %d exceeds %d query rows per KV head",
                 d->n_queries * next_pow2(G), kMaxRows);
-  if (d->head_dim == 256 && d->n_queries * next_pow2(G) > 64)
-    return fail(HS2_ERR_UNSUPPORTED, "head_dim 256: n_queries * pow2(G) = %d exceeds 64 query rows per KV head",
-                d->n_queries * next_pow2(G));
   if (d->kv_stride_t < d->head_dim || d->kv_stride_t % 8 || d->kv_stride_h < 0 || d->kv_stride_h % 8 ||
       d->kv_stride_b < 0 || d->kv_stride_b % 8)
     return fail(HS2_ERR_ALIGN, "KV strides must be non-negative multiples of 8 elements, kv_stride_t >= head_dim");
@@ -146,8 +143,8 @@ int ilog2(int v) {
 // which the per-tile conversion needs: 125 us against 218 us with the bf16
 // shape on the ragged 128K workload).
 int default_fa_variant(int RT, int hd, bool kv8) {
-  if (hd == 256) return RT == 4 ? 8 : 6;
-  if (RT >= 8) return 1;
+  if (hd == 256) return RT >= 4 ? 8 : 6;
+  if (RT >= 8) return kv8 ? 7 : 1;
   if (RT == 1) return kv8 ? 3 : 2;
   if (RT == 4) return 7;
   return 5;
@@ -402,9 +399,6 @@ hs2_status check_fp8(const hs2_dims* dims, const float* k_scale, const float* v_
   if (!aligned(k_scale, 4) || !aligned(v_scale, 4)) return fail(HS2_ERR_ALIGN, "scales need 4-byte alignment");
   if (dims->kv_stride_t % 16 || dims->kv_stride_h % 16 || dims->kv_stride_b % 16)
     return fail(HS2_ERR_ALIGN, "FP8 cache strides must be multiples of 16 elements");
-  const int rows = dims->n_queries * next_pow2(dims->n_q_heads / dims->n_kv_heads);
-  if (rows > 64)
-    return fail(HS2_ERR_UNSUPPORTED, "FP8 cache: n_queries * pow2(G) = %d exceeds 64 query rows per KV head", rows);
   return HS2_OK;
 }
 

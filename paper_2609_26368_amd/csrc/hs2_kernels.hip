@@ -1443,8 +1443,8 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
 // Full attention kernel variants (the planner's defaults: head dim 128 with
-// RT = 1 -> 2 (E4M3: 3), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1; head dim
-// 256 with RT = 4 -> 8, else 6):
+// RT = 1 -> 2 (E4M3: 3), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1 (E4M3: 7);
+// head dim 256 with RT = 4, 8 -> 8, else 6):
 //   1: workgroup kernel (64-row stages shared by 4 or 8 waves), head dim 128
 //   0, 2, 3, 5, 7: ring kernels of head dim 128; 6, 8: head dim 256
 // Columns: variant, RT, waves per token group, stage rows, stages, token
@@ -1455,7 +1455,8 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   X(3, 1, 1, 16, 3, 1, 128) X(3, 2, 1, 16, 3, 1, 128) X(3, 4, 2, 16, 3, 1, 128)     \
   X(5, 1, 1, 32, 3, 1, 128) X(5, 2, 1, 16, 3, 2, 128) X(5, 4, 2, 16, 3, 2, 128)     \
   X(6, 1, 1, 16, 3, 1, 256) X(6, 2, 2, 16, 3, 1, 256) X(6, 4, 4, 16, 3, 1, 256)     \
-  X(7, 2, 2, 32, 2, 2, 128) X(7, 4, 4, 32, 2, 2, 128) X(8, 4, 4, 32, 2, 1, 256)
+  X(7, 2, 2, 32, 2, 2, 128) X(7, 4, 4, 32, 2, 2, 128) X(7, 8, 8, 64, 2, 1, 128)     \
+  X(8, 4, 4, 32, 2, 1, 256) X(8, 8, 8, 32, 2, 1, 256)
 
 // a ring shape serves a cache format only if every wave loads whole 1 KB
 // pieces of each stage (the kernel asserts it; other shapes are never built)
@@ -1578,13 +1579,12 @@ size_t pool_smem_bytes(int C) {
 }
 
 // pool kernels for every (row tiles, padded group) pair the planner can produce:
-// RT = pow2(ceil(C * GP / 16)) with C <= 16 and C * GP <= 128; the E4M3 and
-// head-dim-256 kernels serve at most 64 query rows (RT <= 4)
-#define HS2_POOL_CASES_64(X)                                  \
+// RT = pow2(ceil(C * GP / 16)) with C <= 16 and C * GP <= 128
+#define HS2_POOL_CASES(X)                                     \
   X(1, 1) X(1, 2) X(1, 4) X(1, 8) X(1, 16)                    \
   X(2, 1) X(2, 2) X(2, 4) X(2, 8) X(2, 16) X(2, 32)           \
-  X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)
-#define HS2_POOL_CASES_128(X) X(8, 8) X(8, 16) X(8, 32) X(8, 64)
+  X(4, 4) X(4, 8) X(4, 16) X(4, 32) X(4, 64)                  \
+  X(8, 8) X(8, 16) X(8, 32) X(8, 64)
 
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
   const int64_t chunks = ((int64_t)a.max_len + LOGIT_CHUNK - 1) / LOGIT_CHUNK;
@@ -1607,11 +1607,7 @@ hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int hd, int* wgs) {
                               : pool_occupancy<rt, gp, false, 256>(wgs, C);               \
     return kv8 ? pool_occupancy<rt, gp, true, 128>(wgs, C) : pool_occupancy<rt, gp, false, 128>(wgs, C); \
   }
-  HS2_POOL_CASES_64(HS2_POOL_OCC)
-#undef HS2_POOL_OCC
-#define HS2_POOL_OCC(rt, gp) \
-  if (RT == rt && Gp == gp && hd == 128 && !kv8) return pool_occupancy<rt, gp, false, 128>(wgs, C);
-  HS2_POOL_CASES_128(HS2_POOL_OCC)
+  HS2_POOL_CASES(HS2_POOL_OCC)
 #undef HS2_POOL_OCC
   return hipSuccess;
 }
@@ -1634,11 +1630,7 @@ hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
     return kv8 ? launch_pool_one<rt, gp, true, 128>(a, grid, hc, s)                           \
                : launch_pool_one<rt, gp, false, 128>(a, grid, hc, s);                         \
   }
-  HS2_POOL_CASES_64(HS2_POOL_LAUNCH)
-#undef HS2_POOL_LAUNCH
-#define HS2_POOL_LAUNCH(rt, gp) \
-  if (RT == rt && a.Gp == gp && a.hd == 128 && !kv8) return launch_pool_one<rt, gp, false, 128>(a, grid, hc, s);
-  HS2_POOL_CASES_128(HS2_POOL_LAUNCH)
+  HS2_POOL_CASES(HS2_POOL_LAUNCH)
 #undef HS2_POOL_LAUNCH
   return hipErrorInvalidValue;
 }
@@ -1659,10 +1651,7 @@ hipError_t set_pool_smem_limits() {
   allow((const void*)k_pool<rt, gp, true, 128>);        \
   allow((const void*)k_pool<rt, gp, false, 256>);       \
   allow((const void*)k_pool<rt, gp, true, 256>);
-  HS2_POOL_CASES_64(HS2_POOL_ATTR)
-#undef HS2_POOL_ATTR
-#define HS2_POOL_ATTR(rt, gp) allow((const void*)k_pool<rt, gp, false, 128>);
-  HS2_POOL_CASES_128(HS2_POOL_ATTR)
+  HS2_POOL_CASES(HS2_POOL_ATTR)
 #undef HS2_POOL_ATTR
   allow((const void*)k_block_select);
   allow((const void*)k_fa_split<1>);

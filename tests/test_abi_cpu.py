@@ -59,7 +59,8 @@ def test_workspace_bytes(lib):
     # head dim 256: partials twice as wide; at most 64 query rows per KV head
     assert hs2.hs2_workspace_bytes(dims(head_dim=256), 256, 64) > n
     assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_q_heads=64, n_kv_heads=1), 1024, 128) > 0
-    assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1), 16, 8) == 0
+    assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1), 16, 8) > 0
+    assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=4, n_q_heads=64, n_kv_heads=1), 16, 8) == 0
 
 
 FAKE = 1 << 20  # a 256-byte aligned non-null address; never dereferenced on the error paths
@@ -82,8 +83,8 @@ def test_full_attn_rejects_before_launch(lib):
     assert call_full(lib, dims(n_queries=17)) == hs2.HS2_ERR_SHAPE
     assert call_full(lib, dims(head_dim=64)) == hs2.HS2_ERR_UNSUPPORTED
     assert call_full(lib, dims(head_dim=192)) == hs2.HS2_ERR_UNSUPPORTED
-    assert call_full(lib, dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
-    assert "256" in hs2.hs2_last_error()
+    assert call_full(lib, dims(head_dim=256, n_queries=4, n_q_heads=64, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
+    assert "256" in hs2.hs2_last_error()  # 4 * 64 query rows
     # kv_stride_t must cover the head dim
     assert call_full(lib, dims(head_dim=256, kv_strides=(4096 * 128 * 4, 4096 * 128, 128))) == hs2.HS2_ERR_ALIGN
     assert call_full(lib, dims(n_q_heads=128, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED  # G = 128
@@ -159,8 +160,8 @@ def test_fp8_entry_points_reject_before_launch(lib):
         assert call(d, ks=FAKE + 2) == hs2.HS2_ERR_ALIGN
         # one byte per element: strides must keep 16-byte loads aligned
         assert call(dims(kv_strides=(4096 * 136 * 4, 4096 * 136, 136))) == hs2.HS2_ERR_ALIGN
-        # at most 64 query rows per KV head (C * pow2(G))
-        assert call(dims(n_queries=4, n_q_heads=32, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
+        # at most 128 query rows per KV head (C * pow2(G))
+        assert call(dims(n_queries=8, n_q_heads=32, n_kv_heads=1)) == hs2.HS2_ERR_UNSUPPORTED
         assert call(dims(head_dim=64)) == hs2.HS2_ERR_UNSUPPORTED
     assert full(d, K=FAKE + 8) == hs2.HS2_ERR_ALIGN
     assert sparse(d, n_slots=0) == hs2.HS2_ERR_SHAPE

@@ -26,6 +26,8 @@ SMALL = [
     W.Workload("d256_32q2kv_C2", 1, 2200, 2, 32, 2, 256, 150, 40, 1),
     W.Workload("d256_8q2kv_C3", 2, 1700, 3, 8, 2, 256, 120, 32, 1, ctx_min=700),
     W.Workload("d256_12q4kv_C5", 1, 1400, 5, 12, 4, 256, 100, 24, 1),
+    # the paper's MQA 64/1 with a 2-token verify chunk: 128 query rows per KV head
+    W.Workload("mqa64_d256_C2", 2, 2200, 2, 64, 1, 256, 200, 48, 1, ctx_min=1100),
 ]
 
 
@@ -34,7 +36,10 @@ def test_d256_parity(w):
     parity_case(w, seed=21)
 
 
-@pytest.mark.parametrize("w", SMALL[:2], ids=[w.name for w in SMALL[:2]])
+FP8 = [SMALL[0], SMALL[1], SMALL[5]]
+
+
+@pytest.mark.parametrize("w", FP8, ids=[w.name for w in FP8])
 def test_d256_parity_fp8(w):
     parity_case(w, seed=22, kv="fp8")
 

@@ -26,8 +26,8 @@ def test_fp8_parity_small(w):
     parity_case(w, kv="fp8")
 
 
-HEADS = [  # (Hq, Hkv, C) with C * pow2(G) <= 64 query rows per KV head
-    (12, 4, 1), (8, 8, 3), (16, 1, 2), (32, 1, 2), (6, 2, 5), (8, 2, 16),
+HEADS = [  # (Hq, Hkv, C): group sizes incl. non-powers of two, up to the 128-row maximum
+    (12, 4, 1), (8, 8, 3), (16, 1, 2), (32, 1, 2), (6, 2, 5), (8, 2, 16), (32, 1, 4), (64, 1, 2), (8, 1, 16),
 ]
 
 

@@ -15,10 +15,11 @@ BY_RT = {  # a reduced workload per number of 16-row query tiles per KV head
     1: SMALL[0],                                                                  # 16q/2kv, C = 1: 8 rows
     2: W.Workload("rt2_16q1kv_C2", 2, 3000, 2, 16, 1, 128, 200, 48, 1, ctx_min=1500),  # 32 rows
     4: SMALL[3],                                                                  # 32q/4kv, C = 8: 64 rows
+    8: W.Workload("rt8_32q1kv_C4", 2, 2500, 4, 32, 1, 128, 200, 48, 1, ctx_min=1200),  # 128 rows
 }
 # (row tiles, variant) pairs of the head-dim-128 table: ring kernels 0, 2, 3,
-# 5 (RT 1, 2, 4) and 7 (RT 2, 4); the workgroup kernel 1 (bf16 only)
-SHAPES = [(rt, v) for rt in (1, 2, 4) for v in (0, 1, 2, 3, 5, 7) if not (v == 7 and rt == 1)]
+# 5 (RT 1, 2, 4) and 7 (RT 2, 4, 8); the workgroup kernel 1 (bf16 only)
+SHAPES = [(rt, v) for rt in (1, 2, 4) for v in (0, 1, 2, 3, 5, 7) if not (v == 7 and rt == 1)] + [(8, 1), (8, 7)]
 
 
 @pytest.mark.parametrize("rt,variant", SHAPES, ids=[f"rt{rt}-v{v}" for rt, v in SHAPES])
