@@ -303,14 +303,33 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     online_softmax<RPW, NB>(st, S, pa, lane);
     if (KV8 && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
+    if constexpr (NB % 2 == 0) {
+      // two 16-token blocks per 16x16x32 product: k slots 8 (lane / 16) + j
+      // hold the lane group's 4 tokens of block 2 bp, then its 4 of block
+      // 2 bp + 1, in the P fragments and the transposed V reads alike
 #pragma unroll
-    for (int bi = 0; bi < NB; ++bi)
+      for (int bp = 0; bp < NB / 2; ++bp)
 #pragma unroll
-      for (int nb = 0; nb < HDIM / 16; ++nb) {
-        const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
+        for (int nb = 0; nb < HDIM / 16; ++nb) {
+          const uint2 v0 = v_operand_tr_at<HDIM>(vbase, 2 * bp, nb, lane);
+          const uint2 v1 = v_operand_tr_at<HDIM>(vbase, 2 * bp + 1, nb, lane);
+          const uint4 vb = make_uint4(v0.x, v0.y, v1.x, v1.y);
 #pragma unroll
-        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
-      }
+          for (int rr = 0; rr < RPW; ++rr) {
+            const uint4 pp = make_uint4(pa[2 * bp][rr].x, pa[2 * bp][rr].y, pa[2 * bp + 1][rr].x, pa[2 * bp + 1][rr].y);
+            st.o[rr][nb] = mfma_k32(pp, vb, st.o[rr][nb]);
+          }
+        }
+    } else {
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+        for (int nb = 0; nb < HDIM / 16; ++nb) {
+          const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
+#pragma unroll
+          for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+        }
+    }
   }
   const int64_t unit = (int64_t)b * a.Hkv + g;
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);

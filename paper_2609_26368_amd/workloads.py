@@ -73,6 +73,9 @@ WORKLOADS = {
     # one KV head and head dim 256 (Sec. "Experimental Setup", table of the
     # attention configurations), 1024 global + 128 local tokens (same section)
     "paper_mqa64_d256_128k_b8": Workload("paper_mqa64_d256_128k_b8", 8, 131072, 1, 64, 1, 256, 1024, 128, 3),
+    # the same with a 2-token verify chunk per sequence (128 query rows on the KV head), batch 4
+    "paper_mqa64_d256_128k_b4_chunk2": Workload("paper_mqa64_d256_128k_b4_chunk2", 4, 131072, 2, 64, 1, 256, 1024, 128,
+                                                3),
 }
 
 
