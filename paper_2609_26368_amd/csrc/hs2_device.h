@@ -421,4 +421,37 @@ __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int
 }
 
 
+// O += P . V for the NB 16-token blocks of a staged tile (V rows swizzled at
+// vbase).  With an even NB two blocks share one 16x16x32 product: k slots
+// 8 (lane / 16) + j hold the lane group's 4 tokens of block 2 bp, then its 4
+// of block 2 bp + 1, in the P fragments and the transposed V reads alike.
+template <int RPW, int NB, int HDIM>
+__device__ inline void pv_tile(WaveState<RPW, HDIM>& st, const uint2 (&pa)[NB][RPW], const unsigned char* vbase,
+                               int lane) {
+  if constexpr (NB % 2 == 0) {
+#pragma unroll
+    for (int bp = 0; bp < NB / 2; ++bp)
+#pragma unroll
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint2 v0 = v_operand_tr_at<HDIM>(vbase, 2 * bp, nb, lane);
+        const uint2 v1 = v_operand_tr_at<HDIM>(vbase, 2 * bp + 1, nb, lane);
+        const uint4 vb = make_uint4(v0.x, v0.y, v1.x, v1.y);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) {
+          const uint4 pp = make_uint4(pa[2 * bp][rr].x, pa[2 * bp][rr].y, pa[2 * bp + 1][rr].x, pa[2 * bp + 1][rr].y);
+          st.o[rr][nb] = mfma_k32(pp, vb, st.o[rr][nb]);
+        }
+      }
+  } else {
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+      }
+  }
+}
+
 }  // namespace hs2

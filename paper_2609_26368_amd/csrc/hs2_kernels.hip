@@ -303,33 +303,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     online_softmax<RPW, NB>(st, S, pa, lane);
     if (KV8 && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-    if constexpr (NB % 2 == 0) {
-      // two 16-token blocks per 16x16x32 product: k slots 8 (lane / 16) + j
-      // hold the lane group's 4 tokens of block 2 bp, then its 4 of block
-      // 2 bp + 1, in the P fragments and the transposed V reads alike
-#pragma unroll
-      for (int bp = 0; bp < NB / 2; ++bp)
-#pragma unroll
-        for (int nb = 0; nb < HDIM / 16; ++nb) {
-          const uint2 v0 = v_operand_tr_at<HDIM>(vbase, 2 * bp, nb, lane);
-          const uint2 v1 = v_operand_tr_at<HDIM>(vbase, 2 * bp + 1, nb, lane);
-          const uint4 vb = make_uint4(v0.x, v0.y, v1.x, v1.y);
-#pragma unroll
-          for (int rr = 0; rr < RPW; ++rr) {
-            const uint4 pp = make_uint4(pa[2 * bp][rr].x, pa[2 * bp][rr].y, pa[2 * bp + 1][rr].x, pa[2 * bp + 1][rr].y);
-            st.o[rr][nb] = mfma_k32(pp, vb, st.o[rr][nb]);
-          }
-        }
-    } else {
-#pragma unroll
-      for (int bi = 0; bi < NB; ++bi)
-#pragma unroll
-        for (int nb = 0; nb < HDIM / 16; ++nb) {
-          const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
-#pragma unroll
-          for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
-        }
-    }
+    pv_tile<RPW, NB, HDIM>(st, pa, vbase, lane);
   }
   const int64_t unit = (int64_t)b * a.Hkv + g;
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
@@ -1444,14 +1418,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
     uint2 pa[NB][RPW];
     online_softmax<RPW, NB>(st, S, pa, lane);
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-#pragma unroll
-    for (int bi = 0; bi < NB; ++bi)
-#pragma unroll
-      for (int nb = 0; nb < HDIM / 16; ++nb) {
-        const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
-#pragma unroll
-        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
-      }
+    pv_tile<RPW, NB, HDIM>(st, pa, vbase, lane);
   }
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
@@ -1654,8 +1621,8 @@ hipError_t launch_pool(const PoolArgs& a, int RT, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// sparse-attention ring kernels: (RT, waves) per head dim; 16-row stages x 2
-constexpr int SAR_TW = 16, SAR_NS = 2;
+// sparse-attention ring kernels: (RT, waves) per head dim; 32-row stages x 2
+constexpr int SAR_TW = 32, SAR_NS = 2;
 #define HS2_SA_SHAPES(X) X(1, 1, 128) X(2, 1, 128) X(4, 2, 128) X(1, 1, 256) X(2, 2, 256) X(4, 4, 256)
 
 hipError_t set_pool_smem_limits() {
