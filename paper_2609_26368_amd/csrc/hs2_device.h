@@ -117,8 +117,33 @@ struct WaveState {
 // accumulators are rescaled rarely; the true maximum is tracked in mt.
 constexpr float LAZY_MARGIN = 8.f;
 
-template <int RPW, int BPW, int HDIM>
-__device__ inline void online_softmax(WaveState<RPW, HDIM>& st, f32x4 (&S)[BPW][RPW], uint2 (&pa)[BPW][RPW],
+// bf16 probabilities of BPW 16-token blocks x RPW row tiles in the layout of
+// the P.V A operands: with K32, blocks 2 bp and 2 bp + 1 share one 16x16x32
+// operand w[bp] (x, y: block 2 bp; z, w: block 2 bp + 1); otherwise block bi
+// is the 16x16x16 operand h[bi].  Written straight into this layout, the
+// fragments stay in registers.
+template <int BPW, int RPW, bool K32 = BPW % 2 == 0>
+struct PFrags {
+  static_assert(!K32 || BPW % 2 == 0, "paired blocks");
+  uint4 w[K32 ? BPW / 2 : 1][RPW];
+  uint2 h[K32 ? 1 : BPW][RPW];
+  __device__ inline void set(int bi, int rr, uint32_t lo, uint32_t hi) {
+    if constexpr (K32) {
+      if (bi & 1) {
+        w[bi >> 1][rr].z = lo;
+        w[bi >> 1][rr].w = hi;
+      } else {
+        w[bi >> 1][rr].x = lo;
+        w[bi >> 1][rr].y = hi;
+      }
+    } else {
+      h[bi][rr] = make_uint2(lo, hi);
+    }
+  }
+};
+
+template <int RPW, int BPW, int HDIM, bool K32>
+__device__ inline void online_softmax(WaveState<RPW, HDIM>& st, f32x4 (&S)[BPW][RPW], PFrags<BPW, RPW, K32>& pf,
                                       int lane) {
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
@@ -151,8 +176,7 @@ __device__ inline void online_softmax(WaveState<RPW, HDIM>& st, f32x4 (&S)[BPW][
         p[i] = fast_exp2(S[bi][rr][i] - msub);
         psum += p[i];
       }
-      pa[bi][rr].x = pack_bf16x2(p[0], p[1]);
-      pa[bi][rr].y = pack_bf16x2(p[2], p[3]);
+      pf.set(bi, rr, pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]));
     }
     st.l[rr] += psum;
   }
@@ -181,11 +205,19 @@ __device__ inline void store_partial(const WaveState<RPW, HDIM>& st, float* __re
 
 // ---------------------------------------------------------------- direct-to-LDS staging (swizzled)
 // One stage holds TILE cache rows of K then TILE rows of V, 256 bytes each,
-// row-major; the 16-byte chunk c of row r sits at position c ^ (r & 15) of
-// the row, which makes both the MFMA K-operand reads and the transposing V
-// reads free of bank conflicts.  A wave's 16-byte direct LDS load writes
-// 64 consecutive 16-byte slots (lane order): load n = 4 * wave + u fills
-// slots 64 n + lane, i.e. row 4 n + lane / 16, position lane % 16.
+// row-major; the 16-byte chunk c of row r sits at position c ^ stage_swz(r)
+// of the row.  stage_swz(r) mod 8 is a permutation of rows 0-7 and of rows
+// 8-15, so one chunk of 8 consecutive rows (the MFMA K-operand reads) lands
+// in 8 distinct slots of a 128-byte window; its bits 1-2 are r & 3, so the
+// transposing V reads (4 rows x chunks 2m, 2m + 1) land in 8 distinct slots
+// as well; and it is a permutation of all 16 rows.  With it both reads were
+// measured free of bank conflicts (with c ^ (r & 15) the V reads were
+// 2-way).  A wave's 16-byte direct LDS load writes 64 consecutive 16-byte
+// slots (lane order): load n = 4 * wave + u fills slots 64 n + lane, i.e.
+// row 4 n + lane / 16, position lane % 16.
+__device__ __host__ constexpr int stage_swz(int r) {
+  return ((r & 3) << 1) | (((r >> 2) & 1) << 3) | (((r >> 2) ^ (r >> 3)) & 1);
+}
 constexpr int STAGE_ROW_BYTES = HD * 2;
 constexpr int STAGE_KV_BYTES = TILE * STAGE_ROW_BYTES;  // 16 KB
 constexpr int STAGE_BYTES = 2 * STAGE_KV_BYTES;         // K + V
@@ -223,7 +255,7 @@ __device__ inline void issue_stage_loads(unsigned char* stage, const uint16_t* K
   for (int u = 0; u < LPW; ++u) {
     const int n = LPW * wave + u;
     const int r = stage_row<NW>(wave, u, lane);
-    const int c = (lane & 15) ^ (r & 15);
+    const int c = (lane & 15) ^ stage_swz(r);
     const int64_t off = (int64_t)tok[u] * stride_t + 8 * c;
     dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
     dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + STAGE_KV_BYTES + 1024 * n));
@@ -246,6 +278,14 @@ __device__ inline void wait_stage_loads(int tiles) {
   }
 }
 
+// The k order of the logits MFMAs (16x16x32): for MFMA kk, lane group
+// j = lane / 16 holds the 8 head dims 64 (kk / 2) + 16 j + 8 (kk % 2) .. + 7,
+// in the K operands and the query operands alike.  So MFMAs 2 i and 2 i + 1
+// of a lane together cover one 16-dim run, which one 16-byte read of an
+// E4M3 row supplies; a bf16 row supplies it as two 16-byte chunks.
+__device__ inline int q_koff(int kk, int lane) { return 64 * (kk >> 1) + 16 * (lane >> 4) + 8 * (kk & 1); }
+__device__ inline int k_chunk(int kk, int lane) { return 8 * (kk >> 1) + 2 * (lane >> 4) + (kk & 1); }
+
 // Logits S^T = K . Q^T of the 16 staged rows of block blk; rows of 64 NKK
 // bytes (head dim 32 NKK), swizzled chunks.
 template <int RPW, int NKK>
@@ -255,7 +295,7 @@ __device__ inline void qk_block_swz(const unsigned char* stg, int blk, const uin
   const unsigned char* rp = stg + row * (64 * NKK);
   uint4 a4[NKK];
 #pragma unroll
-  for (int kk = 0; kk < NKK; ++kk) a4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+  for (int kk = 0; kk < NKK; ++kk) a4[kk] = *(const uint4*)(rp + 16 * (k_chunk(kk, lane) ^ stage_swz(row)));
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -271,7 +311,7 @@ __device__ inline uint2 v_operand_tr(const unsigned char* stg, int blk, int nb, 
   const int kq = lane & 15;
   const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
   const int col = 16 * nb + 4 * (kq & 3);
-  const int pos = (col >> 3) ^ (row & 15);
+  const int pos = (col >> 3) ^ stage_swz(row);
   const unsigned char* p = stg + STAGE_KV_BYTES + row * STAGE_ROW_BYTES + 16 * pos + 2 * (col & 7);
   const i16x4_lds v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_lds*)(p));
   return __builtin_bit_cast(uint2, v);
@@ -280,15 +320,15 @@ __device__ inline uint2 v_operand_tr(const unsigned char* stg, int blk, int nb, 
 template <int RPW, int BPW>
 __device__ inline void softmax_pv_swz(WaveState<RPW>& st, const unsigned char* stg, const int (&blk)[BPW],
                                       f32x4 (&S)[BPW][RPW], int lane) {
-  uint2 pa[BPW][RPW];
-  online_softmax<RPW, BPW>(st, S, pa, lane);
+  PFrags<BPW, RPW, false> pf;
+  online_softmax(st, S, pf, lane);
 #pragma unroll
   for (int bi = 0; bi < BPW; ++bi) {
 #pragma unroll
     for (int nb = 0; nb < 8; ++nb) {
       const uint2 vb = v_operand_tr(stg, blk[bi], nb, lane);
 #pragma unroll
-      for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+      for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pf.h[bi][rr], vb, st.o[rr][nb]);
     }
   }
 }
@@ -316,23 +356,28 @@ __device__ inline uint2 e4m3x4_to_bf16x4(uint32_t w) {
   return make_uint2(lo, hi);
 }
 
-// Raw E4M3 rows of RB bytes are staged swizzled too (chunk c of row r at
-// position c ^ raw_swz<RB>(r)) so that the 8-byte K-operand reads of 16 rows
-// hit distinct banks: two 128-byte rows share a 256-byte bank line.
+// Raw E4M3 rows of RB bytes are staged swizzled too: chunk c of row r at
+// position c ^ raw_swz<RB>(r), r modulo the chunks of a row, so that the
+// 16-byte K-operand reads (one chunk of each of 16 rows) spread over all
+// chunk slots (measured free of bank conflicts, as are the row-contiguous
+// conversion reads).
 template <int RB>
 __device__ __host__ constexpr int raw_swz(int r) {
-  return RB == 128 ? (r >> 1) & 7 : r & 15;
+  return r & (RB / 16 - 1);
 }
 
-// K operand of the logits MFMA (16x16x32: row `row`, the 8 values d =
-// 8 (lane / 16) + 32 kk .. + 7) straight from a raw E4M3 stage, converted to
-// bf16 in registers.
+// Operands of the logits MFMAs 2 i and 2 i + 1 (16x16x32, row `row`) from a
+// raw E4M3 stage, converted to bf16 in registers: one 16-byte chunk
+// c = lane / 16 + 4 i (head dims 16 c .. 16 c + 15), its first 8 values for
+// MFMA 2 i and its last 8 for MFMA 2 i + 1 (the order of q_koff).
 template <int RB>
-__device__ inline uint4 k_operand_e4m3(const unsigned char* raw, int row, int kk, int lane) {
-  const int c = (lane >> 5) + 2 * kk;  // 16-byte chunk
-  const uint2 v = *(const uint2*)(raw + row * RB + 16 * (c ^ raw_swz<RB>(row)) + 8 * ((lane >> 4) & 1));
-  const uint2 lo = e4m3x4_to_bf16x4(v.x), hi = e4m3x4_to_bf16x4(v.y);
-  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+__device__ inline void k_operands_e4m3(const unsigned char* raw, int row, int i, int lane, uint4& a0, uint4& a1) {
+  const int c = (lane >> 4) + 4 * i;
+  const uint4 v = *(const uint4*)(raw + row * RB + 16 * (c ^ raw_swz<RB>(row)));
+  const uint2 x = e4m3x4_to_bf16x4(v.x), y = e4m3x4_to_bf16x4(v.y);
+  const uint2 z = e4m3x4_to_bf16x4(v.z), w = e4m3x4_to_bf16x4(v.w);
+  a0 = make_uint4(x.x, x.y, y.x, y.y);
+  a1 = make_uint4(z.x, z.y, w.x, w.y);
 }
 
 // Logits of the 16 rows of block blk of a raw E4M3 stage against RPW row
@@ -343,7 +388,7 @@ __device__ inline void qk_block_e4m3(const unsigned char* raw, int blk, const ui
   const int row = 16 * blk + (lane & 15);
   uint4 a4[NKK];
 #pragma unroll
-  for (int kk = 0; kk < NKK; ++kk) a4[kk] = k_operand_e4m3<RB>(raw, row, kk, lane);
+  for (int i = 0; i < NKK / 2; ++i) k_operands_e4m3<RB>(raw, row, i, lane, a4[2 * i], a4[2 * i + 1]);
 #pragma unroll
   for (int rr = 0; rr < RPW; ++rr) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -370,23 +415,30 @@ __device__ __host__ constexpr int fa_ring_lds_bytes(int rt, int tw, int ns, int 
 
 // Convert NR staged E4M3 rows (raw, HDIM bytes each, chunk c of row r at
 // position c ^ raw_swz(r)) into bf16 stage rows at stg (2 HDIM bytes; chunk c
-// of row r at position c ^ (r & 15)); threads tid of NTHR.  A job is one
-// 16-byte raw piece: 16 values, two bf16 chunks.
+// of row r at position c ^ stage_swz(r)); threads tid of NTHR.  A job is one
+// 16-byte raw piece p of row r: 16 values, bf16 chunks 2 p and 2 p + 1.
+// Eight consecutive jobs take pieces 4 m' .. 4 m' + 3 of rows r and r + 4 of
+// an 8-row block (r < 4 within it): those rows' stage_swz differ in bit 0,
+// so each of the two stores of 8 lanes covers 8 distinct 16-byte slots of a
+// 128-byte window, and so does the raw read.
 template <int NR, int NTHR, int HDIM = HD>
 __device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
   constexpr int PPR = HDIM / 16;  // raw pieces per row
   constexpr int JOBS = NR * PPR;
+  static_assert(NR % 8 == 0 && PPR % 4 == 0, "8-row blocks, 4-piece quads");
 #pragma unroll
   for (int k = 0; k < (JOBS + NTHR - 1) / NTHR; ++k) {
     const int j = tid + k * NTHR;
     if (JOBS % NTHR == 0 || j < JOBS) {
-      const int r = j / PPR, p = j % PPR;
+      const int jb = j % (8 * PPR), m = jb >> 3;
+      const int r = 8 * (j / (8 * PPR)) + (m & 3) + 4 * ((jb >> 2) & 1);
+      const int p = 4 * (m >> 2) + (jb & 3);
       const uint4 v = *(const uint4*)(raw + r * HDIM + 16 * (p ^ raw_swz<HDIM>(r)));
       const uint2 a = e4m3x4_to_bf16x4(v.x), b = e4m3x4_to_bf16x4(v.y);
       const uint2 c = e4m3x4_to_bf16x4(v.z), d = e4m3x4_to_bf16x4(v.w);
       unsigned char* rp = stg + r * (2 * HDIM);
-      *(uint4*)(rp + 16 * ((2 * p) ^ (r & 15))) = make_uint4(a.x, a.y, b.x, b.y);
-      *(uint4*)(rp + 16 * ((2 * p + 1) ^ (r & 15))) = make_uint4(c.x, c.y, d.x, d.y);
+      *(uint4*)(rp + 16 * ((2 * p) ^ stage_swz(r))) = make_uint4(a.x, a.y, b.x, b.y);
+      *(uint4*)(rp + 16 * ((2 * p + 1) ^ stage_swz(r))) = make_uint4(c.x, c.y, d.x, d.y);
     }
   }
 }
@@ -414,7 +466,7 @@ __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int
   const int kq = lane & 15;
   const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
   const int col = 16 * nb + 4 * (kq & 3);
-  const int pos = (col >> 3) ^ (row & 15);
+  const int pos = (col >> 3) ^ stage_swz(row);
   const unsigned char* p = vbase + row * (2 * HDIM) + 16 * pos + 2 * (col & 7);
   const i16x4_lds v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4_lds*)(p));
   return __builtin_bit_cast(uint2, v);
@@ -426,7 +478,7 @@ __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int
 // 8 (lane / 16) + j hold the lane group's 4 tokens of block 2 bp, then its 4
 // of block 2 bp + 1, in the P fragments and the transposed V reads alike.
 template <int RPW, int NB, int HDIM>
-__device__ inline void pv_tile(WaveState<RPW, HDIM>& st, const uint2 (&pa)[NB][RPW], const unsigned char* vbase,
+__device__ inline void pv_tile(WaveState<RPW, HDIM>& st, const PFrags<NB, RPW>& pf, const unsigned char* vbase,
                                int lane) {
   if constexpr (NB % 2 == 0) {
 #pragma unroll
@@ -437,10 +489,7 @@ __device__ inline void pv_tile(WaveState<RPW, HDIM>& st, const uint2 (&pa)[NB][R
         const uint2 v1 = v_operand_tr_at<HDIM>(vbase, 2 * bp + 1, nb, lane);
         const uint4 vb = make_uint4(v0.x, v0.y, v1.x, v1.y);
 #pragma unroll
-        for (int rr = 0; rr < RPW; ++rr) {
-          const uint4 pp = make_uint4(pa[2 * bp][rr].x, pa[2 * bp][rr].y, pa[2 * bp + 1][rr].x, pa[2 * bp + 1][rr].y);
-          st.o[rr][nb] = mfma_k32(pp, vb, st.o[rr][nb]);
-        }
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k32(pf.w[bp][rr], vb, st.o[rr][nb]);
       }
   } else {
 #pragma unroll
@@ -449,7 +498,7 @@ __device__ inline void pv_tile(WaveState<RPW, HDIM>& st, const uint2 (&pa)[NB][R
       for (int nb = 0; nb < HDIM / 16; ++nb) {
         const uint2 vb = v_operand_tr_at<HDIM>(vbase, bi, nb, lane);
 #pragma unroll
-        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pa[bi][rr], vb, st.o[rr][nb]);
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pf.h[bi][rr], vb, st.o[rr][nb]);
       }
   }
 }

@@ -34,16 +34,16 @@ __device__ inline int clamp_len(const int32_t* len, int b, int max_len) {
 }
 
 // Load B operands (Q^T) of query row tile rt for this lane: row 16 rt + (lane & 15)
-// (head dim 32 NKK).
+// (head dim 32 NKK), in the k order of q_koff.
 template <int NKK>
 __device__ inline void load_q_tile(uint4 (&q)[NKK], const uint16_t* __restrict__ qbase, int rt, int lane, int Gp,
                                    int G, int C, int Hq, int g, int b) {
   const int r = 16 * rt + (lane & 15);
   const int c = r / Gp, h = r % Gp;
   if (c < C && h < G) {
-    const uint16_t* p = qbase + (((int64_t)b * C + c) * Hq + g * G + h) * (32 * NKK) + 8 * (lane >> 4);
+    const uint16_t* p = qbase + (((int64_t)b * C + c) * Hq + g * G + h) * (32 * NKK);
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const uint4*)(p + 32 * kk);
+    for (int kk = 0; kk < NKK; ++kk) q[kk] = *(const uint4*)(p + q_koff(kk, lane));
   } else {
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) q[kk] = make_uint4(0, 0, 0, 0);
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPL = 1024 / RB;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
     return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
-               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
+               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ stage_swz(row));
   };
   int64_t lane_off[LPM];
 #pragma unroll
@@ -299,11 +299,11 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
           }
           S[bi][rr][ii] = v;
         }
-    uint2 pa[NB][RPW];
-    online_softmax<RPW, NB>(st, S, pa, lane);
+    PFrags<NB, RPW> pf;
+    online_softmax(st, S, pf, lane);
     if (KV8 && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-    pv_tile<RPW, NB, HDIM>(st, pa, vbase, lane);
+    pv_tile<RPW, NB, HDIM>(st, pf, vbase, lane);
   }
   const int64_t unit = (int64_t)b * a.Hkv + g;
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
@@ -652,7 +652,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
   constexpr int RPL = PS::RPL;  // rows per 1 KB load
   auto lane_offset = [&](int row, int t) -> int64_t {
     return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
-               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ (row & 15));
+               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ stage_swz(row));
   };
   int64_t lane_off[LPM];
 #pragma unroll
@@ -704,12 +704,12 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
       uint4 k4[NKK];
       if constexpr (KV8) {
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) k4[kk] = k_operand_e4m3<RB>(stg, row, kk, lane);
+        for (int i = 0; i < NKK / 2; ++i) k_operands_e4m3<RB>(stg, row, i, lane, k4[2 * i], k4[2 * i + 1]);
       } else {
         const unsigned char* rp = stg + row * SRB;
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk)
-          k4[kk] = *(const uint4*)(rp + 16 * (((lane >> 4) + 4 * kk) ^ (row & 15)));
+          k4[kk] = *(const uint4*)(rp + 16 * (k_chunk(kk, lane) ^ stage_swz(row)));
       }
       f32x4 acc[RPW];
 #pragma unroll
@@ -1330,9 +1330,9 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   for (int rr = 0; rr < RPW; ++rr) {
     const int h = 16 * (rt0 + rr) + (lane & 15);
     if (h < a.G) {
-      const uint16_t* p = a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HDIM + 8 * (lane >> 4);
+      const uint16_t* p = a.q + (((int64_t)b * a.C + c) * a.Hq + g * a.G + h) * HDIM;
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) q[rr][kk] = *(const uint4*)(p + 32 * kk);
+      for (int kk = 0; kk < NKK; ++kk) q[rr][kk] = *(const uint4*)(p + q_koff(kk, lane));
     } else {
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) q[rr][kk] = make_uint4(0, 0, 0, 0);
@@ -1359,7 +1359,7 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
       const int row = RPL * n + lane / CPR;
       const int t = sidx[tile * TW + row];
       const int64_t off = (int64_t)(t < 0 ? 0 : t) * stride_t +
-                          (KV8 ? 16 * ((lane % CPR) ^ raw_swz<RB>(row)) : 16 * ((lane % CPR) ^ (row & 15)));
+                          (KV8 ? 16 * ((lane % CPR) ^ raw_swz<RB>(row)) : 16 * ((lane % CPR) ^ stage_swz(row)));
       dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
       dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
       const uint64_t bal = __ballot(t >= 0);  // lanes CPR j .. hold row RPL n + j
@@ -1415,10 +1415,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
           const int row = 16 * bi + 4 * (lane >> 4) + ii;
           S[bi][rr][ii] = ((m_i >> row) & 1u) ? S[bi][rr][ii] * c2 : -INFINITY;
         }
-    uint2 pa[NB][RPW];
-    online_softmax<RPW, NB>(st, S, pa, lane);
+    PFrags<NB, RPW> pf;
+    online_softmax(st, S, pf, lane);
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-    pv_tile<RPW, NB, HDIM>(st, pa, vbase, lane);
+    pv_tile<RPW, NB, HDIM>(st, pf, vbase, lane);
   }
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
