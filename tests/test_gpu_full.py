@@ -1,0 +1,40 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (same workloads, same seeded inputs, the planner's default
+kernels and splits), checked on sampled (sequence, KV head) groups.
+
+The oracle computes only the sampled groups (each a whole context: up to
+524,288 tokens); every output row of those groups is held to the same bar
+as the small cases: full-attention output and statistics, pooled scores,
+index rows (block-tie aware as in tests/checker.py), and the sparse layers
+on the oracle's selection and, when it matches, on the GPU's own.
+"""
+from __future__ import annotations
+
+import pytest
+
+from paper_2609_26368_amd import workloads as W
+from tests.test_gpu_parity import parity_case
+
+pytestmark = pytest.mark.gpu
+
+WL = W.WORKLOADS
+# (workload, cache format, sampled groups): the first and the last
+# (sequence, KV head) of every workload; the ragged workload's last sequence
+# has its own length
+FULL = [
+    ("decode_4k_16q2kv", "bf16", [(0, 0), (0, 1)]),
+    ("block_32k_32q4kv", "bf16", [(0, 0), (0, 3)]),
+    ("ragged_16k_128k_b8_needles", "bf16", [(0, 0), (7, 3)]),
+    ("ragged_16k_128k_b8_needles", "fp8", [(3, 1)]),
+    ("chunk8_128k_b4", "bf16", [(0, 0), (3, 3)]),
+    ("chunk8_128k_b4", "fp8", [(1, 2)]),
+    ("stress_512k_b2_64q8kv", "bf16", [(1, 7)]),
+    ("paper_mqa64_d256_128k_b8", "bf16", [(0, 0), (7, 0)]),
+    ("paper_mqa64_d256_128k_b8", "fp8", [(4, 0)]),
+    ("paper_mqa64_d256_128k_b4_chunk2", "bf16", [(3, 0)]),
+]
+
+
+@pytest.mark.parametrize("name,kv,groups", FULL, ids=[f"{n}-{kv}" for n, kv, _ in FULL])
+def test_full_size_sampled_groups(name, kv, groups):
+    parity_case(WL[name], groups=groups, kv=kv)
