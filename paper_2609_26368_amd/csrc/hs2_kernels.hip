@@ -381,12 +381,11 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
 template <int HDIM>
 __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   constexpr int NQ = HDIM / 4, SG = 256 / NQ;
-  __shared__ float s_wmax[8];
-  __shared__ float s_z[SG];
+  __shared__ float s_m[SG], s_mt[SG], s_z[SG];
   __shared__ float4 s_o[SG][NQ];
   const int r = blockIdx.x;
   const int64_t unit = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x;
   const int sg = tid / NQ, dq = tid % NQ;
   if (a.clear) {  // zero the selection histogram and counters for the kernels that follow
     const int64_t nb = (int64_t)gridDim.x * gridDim.y, bid = unit * gridDim.x + r;
@@ -411,49 +410,46 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
     nvalid = ((Lv + a.split_tokens - 1) / a.split_tokens) * a.tg;
   }
   const int64_t base = unit * a.nslot * a.rows + r;
-  // largest reference maximum and largest true maximum of the partials
-  float M = -INFINITY, Mt = -INFINITY;
-  for (int s = tid; s < nvalid; s += 256) {
-    const float4 ml = *(const float4*)(a.part_ml + (base + (int64_t)s * a.rows) * 4);
-    M = fmaxf(M, ml.x);
-    Mt = fmaxf(Mt, ml.z);
+  // one pass over the partials: each slot group merges its slots online
+  // (reference maximum m, sum l, output row, rescaled when m rises) with
+  // every slot's loads issued together, then the groups are merged in LDS
+  float m = -INFINITY, mt = -INFINITY, z = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int s = sg; s < nvalid; s += SG) {
+    const int64_t pr = base + (int64_t)s * a.rows;
+    const float4 ml = *(const float4*)(a.part_ml + pr * 4);
+    const float4 o = *(const float4*)(a.part_o + pr * HDIM + 4 * dq);
+    mt = fmaxf(mt, ml.z);
+    const float mn = fmaxf(m, ml.x);
+    // an empty partial (m = -inf, O = 0) adds nothing; exp2(-inf) = 0
+    const float keep = mn == -INFINITY ? 1.f : fast_exp2(m - mn);
+    const float w = mn == -INFINITY ? 0.f : fast_exp2(ml.x - mn);
+    z = z * keep + ml.y * w;
+    acc.x = acc.x * keep + o.x * w;
+    acc.y = acc.y * keep + o.y * w;
+    acc.z = acc.z * keep + o.z * w;
+    acc.w = acc.w * keep + o.w * w;
+    m = mn;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    M = fmaxf(M, __shfl_xor(M, o));
-    Mt = fmaxf(Mt, __shfl_xor(Mt, o));
-  }
-  if (lane == 0) {
-    s_wmax[wave] = M;
-    s_wmax[4 + wave] = Mt;
+  if (dq == 0) {
+    s_m[sg] = m;
+    s_mt[sg] = mt;
   }
   __syncthreads();
-  M = fmaxf(fmaxf(s_wmax[0], s_wmax[1]), fmaxf(s_wmax[2], s_wmax[3]));
-  Mt = fmaxf(fmaxf(s_wmax[4], s_wmax[5]), fmaxf(s_wmax[6], s_wmax[7]));
+  float M = -INFINITY, Mt = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < SG; ++j) {
+    M = fmaxf(M, s_m[j]);
+    Mt = fmaxf(Mt, s_mt[j]);
+  }
   const int64_t orow = ((int64_t)b * a.C + c) * a.Hq + (int64_t)g * a.G + h;
   // sink logit of this head in log2 units: joins the normaliser, no value row
   const float sink2 = a.sink ? a.sink[g * a.G + h] * 1.4426950408889634f : -INFINITY;
   M = fmaxf(M, sink2);
-  float z = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (M != -INFINITY) {
-    // branch-free so that several slots' loads are in flight: an empty
-    // partial (m = -inf, O = 0) gets weight exp2(-inf) = 0
-#pragma unroll 4
-    for (int s = sg; s < nvalid; s += SG) {
-      const int64_t pr = base + (int64_t)s * a.rows;
-      const float m = a.part_ml[pr * 4];
-      const float w = fast_exp2(m - M);
-      z += a.part_ml[pr * 4 + 1] * w;
-      const float4 o = *(const float4*)(a.part_o + pr * HDIM + 4 * dq);
-      acc.x += o.x * w;
-      acc.y += o.y * w;
-      acc.z += o.z * w;
-      acc.w += o.w * w;
-    }
-  }
-  s_o[sg][dq] = acc;
-  if (dq == 0) s_z[sg] = z;
+  const float f = M == -INFINITY ? 0.f : fast_exp2(m - M);  // this group's share
+  s_o[sg][dq] = make_float4(acc.x * f, acc.y * f, acc.z * f, acc.w * f);
+  if (dq == 0) s_z[sg] = z * f;
   __syncthreads();
   if (sg != 0) return;
   float Z = 0.f;
