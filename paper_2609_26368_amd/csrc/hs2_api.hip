@@ -62,6 +62,7 @@ struct Plan {
   int RT, TG;                 // full-attention / pooling row tiles
   int fa_variant;             // ring kernel shape (0, 2, 3, 4) for RT <= 4; 1: workgroup kernel
   int fa_split, fa_nsplit;
+  int logit_chunk;
   int pool_split, pool_nsplit;
   int64_t units;              // B * Hkv
   int64_t rows;               // selection rows B * Hkv * C
@@ -205,6 +206,10 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   // from them instead of re-reading K (256 bytes per token)
   p.pool_logits = p.RT == 1 && p.fa_variant != 1 && env_int("HS2_POOL_FROM_K", 0) == 0;
   p.logit_stride = round_up(p.Lmax, 64);
+  // score pass over stored logits: chunks of 1024-4096 tokens (whole float4
+  // steps of its 256 threads), about two workgroups per CU
+  p.logit_chunk = (int)std::min<int64_t>(
+      4096, std::max<int64_t>(1024, round_up(cdiv(p.Lmax * p.units, 2 * (int64_t)(di ? di->cus : 256)), 1024)));
 
   const int64_t prow = 16 * p.RT;
   const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
@@ -538,7 +543,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   pa.Gp = p.Gp;
   pa.max_len = p.Lmax;
   pa.W = p.W;
-  pa.split_tokens = p.pool_split;
+  pa.split_tokens = p.pool_logits ? p.logit_chunk : p.pool_split;
   pa.n_split = p.pool_nsplit;
   pa.logits = fa.logits;
   pa.logit_stride = p.logit_stride;

@@ -741,7 +741,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 // P = sum over h of exp2(s2_h - msub) * fac, the same constants as k_pool.
 // grid (chunks of LOGIT_CHUNK tokens, B * Hkv), 256 threads, 4 consecutive
 // tokens per thread; dynamic LDS: C packed histograms.
-constexpr int LOGIT_CHUNK = 4096;
 __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint32_t* hist = (uint32_t*)smem;  // [C][NBINS/2], 16-bit packed counters
@@ -751,9 +750,9 @@ __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
   const int tid = threadIdx.x;
   const int Lv = clamp_len(a.len, b, a.max_len);
   const int n_cand_max = Lv - a.W;  // union of the queries' candidates
-  const int t_begin = blockIdx.x * LOGIT_CHUNK;
+  const int t_begin = blockIdx.x * a.split_tokens;
   if (t_begin >= n_cand_max) return;
-  const int t_end = min(n_cand_max, t_begin + LOGIT_CHUNK);
+  const int t_end = min(n_cand_max, t_begin + a.split_tokens);
   const int CG = a.C * a.G;
   for (int i = tid; i < a.C * (NBINS / 2); i += NT) hist[i] = 0;
   if (tid < CG) {
@@ -772,6 +771,7 @@ __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
       const int nc = nc0 + c;
       if (t >= nc) continue;  // not a candidate of query c (later queries have more)
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
       for (int h = 0; h < a.G; ++h) {
         const int r = c * a.G + h;
         const float4 l = *(const float4*)(lg + r * a.logit_stride + t);
@@ -1575,7 +1575,7 @@ size_t pool_smem_bytes(int C) {
   X(8, 8) X(8, 16) X(8, 32) X(8, 64)
 
 hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
-  const int64_t chunks = ((int64_t)a.max_len + LOGIT_CHUNK - 1) / LOGIT_CHUNK;
+  const int64_t chunks = ((int64_t)a.max_len + a.split_tokens - 1) / a.split_tokens;
   HS2_LAUNCH(k_pool_logits, dim3((unsigned)chunks, (unsigned)(a.B * a.Hkv)), dim3(NT),
              (size_t)a.C * (NBINS / 2) * sizeof(uint32_t), s, a);
   return hipGetLastError();
