@@ -894,6 +894,7 @@ constexpr int SEL_PER = 16;             // tokens per thread
 constexpr int SEL_TOKENS = SELB * SEL_PER;
 constexpr int SEL_LDS_CAND = 2048;      // candidates a workgroup gathers in LDS
 constexpr int RESOLVE_LDS_CAP = 6144;   // candidates the resolver keeps in LDS
+constexpr size_t SEL_BM_LDS_MAX = 65536; // largest row bitmap kept in LDS (524288 tokens)
 static_assert(NBINS == SELB, "one histogram bin per thread");
 
 struct SelShared {
@@ -940,8 +941,10 @@ __device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const 
   return th;
 }
 
-// The need largest of the m candidates get their bitmap bits.
-__device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, SelShared& sh) {
+// The need largest of the m candidates get their bitmap bits (in the row's
+// LDS copy sbm when given, else in the global bitmap).
+__device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, SelShared& sh,
+                                   uint64_t* sbm) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const uint32_t* ck = a.cand_key + row * a.cand_cap;
   const int32_t* ci = a.cand_idx + row * a.cand_cap;
@@ -1005,16 +1008,21 @@ __device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int 
   for (int i = tid; i < m; i += SELB) {
     const uint64_t cv = composite(i);
     if (cv >= thresh) {
-      const int t = ci[i];
-      atomicOr(&bm32[t >> 5], 1u << (t & 31));
+      const int t = in_lds ? (int)~(uint32_t)cv : ci[i];
+      if (sbm)
+        atomicOr((unsigned long long*)&sbm[t >> 6], 1ull << (t & 63));
+      else
+        atomicOr(&bm32[t >> 5], 1u << (t & 31));
     }
   }
 }
 
-// Ascending emission into the row's index slots.  The bitmap words are read
-// with agent-scope atomic loads: this workgroup has just set bits in them
-// with device atomics (ordered before these loads by the block barrier).
-__device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh) {
+// Ascending emission into the row's index slots, from the row's LDS copy of
+// the bitmap when given; else the global words are read with agent-scope
+// atomic loads: this workgroup has just set bits in them with device atomics
+// (ordered before these loads by the block barrier).
+__device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh,
+                                const uint64_t* sbm) {
   int32_t* out = a.idx + row * a.S;
   uint64_t* bm = a.bitmap + row * a.bitmap_words;
   const int tid = threadIdx.x;
@@ -1022,7 +1030,9 @@ __device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri
   int base = 0;
   for (int w0 = 0; w0 < nwords; w0 += SELB) {
     const int w = w0 + tid;
-    uint64_t bits = w < nwords ? __hip_atomic_load(&bm[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    uint64_t bits = w >= nwords ? 0ull
+                    : sbm       ? sbm[w]
+                                : __hip_atomic_load(&bm[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (w == nwords - 1 && (ri.N & 63)) bits &= (1ull << (ri.N & 63)) - 1ull;  // tail bits are not maintained
     int total;
     int off = block_scan_1024(__popcll(bits), sh.lds16, total);
@@ -1061,6 +1071,10 @@ __global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
   if (tid == 0) sh.n = 0;
   const Threshold th = find_threshold(a, row, ri, sh);
   __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
+  // per mode: tokens with digit > sel_above are taken, those equal to
+  // cand_digit are candidates (mode 0: none; 1: every valid token)
+  const int sel_above = th.mode == 2 ? th.bstar : (th.mode == 1 ? -1 : NBINS);
+  const int cand_digit = th.mode == 2 ? th.bstar : -2;
 #pragma unroll
   for (int j = 0; j < SEL_PER; ++j) {
     const int tb = t0 + SELB * j + 64 * wave;  // this wave's 64 tokens: one bitmap word
@@ -1069,27 +1083,26 @@ __global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
     const bool valid = t < t1;
     const uint32_t key = score_key(v[j]);
     const int d = score_digit(key);
-    const bool sel = valid && (th.mode == 1 || (th.mode == 2 && d > th.bstar));
-    const bool cand = valid && th.mode == 2 && d == th.bstar;
-    const uint64_t sm = __ballot(sel);
+    const uint64_t sm = __ballot(valid && d > sel_above);
     if (lane == 0) bm[tb >> 6] = sm;
-    const uint64_t cm = __ballot(cand);
-    if (cm) {
+    const uint64_t cm = __ballot(valid && d == cand_digit);
+    if (cm) {  // wave-uniform: lane 0 claims the wave's slots
       // LDS slots [off, off + cnt) are claimed; those at or past the LDS
       // capacity go to global slots reserved here (LDS slots below the
       // capacity are then all written exactly once)
-      const int leader = __builtin_ctzll(cm);
       const int cnt = __popcll(cm);
-      int off = 0, gbase = 0;
-      if (lane == leader) {
-        off = atomicAdd(&sh.n, cnt);
-        const int excess = off + cnt - max(off, SEL_LDS_CAND);
-        if (excess > 0) gbase = atomicAdd(&st[3], excess);
+      int off = 0;
+      if (lane == 0) off = atomicAdd(&sh.n, cnt);
+      off = __builtin_amdgcn_readfirstlane(off);
+      const int excess = off + cnt - max(off, SEL_LDS_CAND);
+      int gbase = 0;
+      if (excess > 0) {
+        if (lane == 0) gbase = atomicAdd(&st[3], excess);
+        gbase = __builtin_amdgcn_readfirstlane(gbase);
       }
-      off = __shfl(off, leader);
-      gbase = __shfl(gbase, leader);
-      if (cand) {
-        const int slot = off + __popcll(cm & ((1ull << lane) - 1ull));
+      if ((cm >> lane) & 1ull) {
+        const int slot = off + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
         if (slot < SEL_LDS_CAND) {
           sh.u.cand.key[slot] = key;
           sh.u.cand.idx[slot] = t;
@@ -1114,14 +1127,26 @@ __global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
   }
 }
 
+// BM_LDS: the row's bitmap is copied into dynamic LDS at the start (its
+// loads overlap the histogram's) and completed and emitted there; otherwise
+// (rows of more than 512K tokens) the global bitmap is used throughout.
+template <bool BM_LDS>
 __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
   __shared__ SelShared sh;
+  extern __shared__ __align__(16) uint64_t sbm[];
   const int64_t row = blockIdx.x;
   const RowInfo ri = row_info(a, row);
+  const int m = min(a.state[row * 8 + 3], (int)a.cand_cap);
+  if constexpr (BM_LDS) {
+    const uint64_t* bm = a.bitmap + row * a.bitmap_words;
+    const int nwords = (ri.N + 63) >> 6;
+    for (int w = threadIdx.x; w < nwords; w += SELB) sbm[w] = bm[w];
+  }
   const Threshold th = find_threshold(a, row, ri, sh);
-  if (th.mode == 2) resolve_row(a, row, th.need, min(a.state[row * 8 + 3], (int)a.cand_cap), sh);
+  __syncthreads();  // the LDS bitmap complete (find_threshold may return before its barriers)
+  if (th.mode == 2) resolve_row(a, row, th.need, m, sh, BM_LDS ? sbm : nullptr);
   __syncthreads();
-  emit_row(a, row, ri, sh);
+  emit_row(a, row, ri, sh, BM_LDS ? sbm : nullptr);
 }
 
 // ---------------------------------------------------------------------------- block-level selection
@@ -1642,6 +1667,9 @@ hipError_t set_pool_smem_limits() {
   HS2_POOL_CASES(HS2_POOL_ATTR)
 #undef HS2_POOL_ATTR
   allow((const void*)k_block_select);
+  if (e == hipSuccess)  // its static LDS is large: only the bitmap's own limit
+    e = hipFuncSetAttribute((const void*)k_sel_finish<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)SEL_BM_LDS_MAX);
   allow((const void*)k_fa_split<1>);
   allow((const void*)k_fa_split<2>);
   allow((const void*)k_fa_split<4>);
@@ -1695,7 +1723,11 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
   HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELB), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  HS2_LAUNCH(k_sel_finish, dim3((unsigned)a.rows), dim3(SELB), 0, s, a);
+  const size_t bm_bytes = (size_t)a.bitmap_words * sizeof(uint64_t);
+  if (bm_bytes <= SEL_BM_LDS_MAX)
+    HS2_LAUNCH(k_sel_finish<true>, dim3((unsigned)a.rows), dim3(SELB), bm_bytes, s, a);
+  else
+    HS2_LAUNCH(k_sel_finish<false>, dim3((unsigned)a.rows), dim3(SELB), 0, s, a);
   return hipGetLastError();
 }
 
