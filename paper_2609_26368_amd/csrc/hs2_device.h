@@ -399,17 +399,18 @@ __device__ inline void qk_block_e4m3(const unsigned char* raw, int blk, const ui
 }
 
 // LDS of a full-attention ring kernel: per token group an NS-stage ring of
-// TW K rows and TW V rows (bf16: 2 hd bytes a row; E4M3: hd bytes, plus one
-// converted bf16 V tile); at least the end-of-split merge of TGW groups.
-__device__ __host__ constexpr int fa_ring_group_bytes(int tw, int ns, bool kv8, int hd) {
-  return ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? tw * 2 * hd : 0);
+// TW K rows and TW V rows (bf16: 2 hd bytes a row; E4M3: hd bytes, plus a
+// converted bf16 V tile, and a converted K tile when the group has several
+// waves); at least the end-of-split merge of TGW groups.
+__device__ __host__ constexpr int fa_ring_group_bytes(int nwv, int tw, int ns, bool kv8, int hd) {
+  return ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? (nwv > 1 ? 2 : 1) * tw * 2 * hd : 0);
 }
 __device__ __host__ constexpr int fa_ring_merge_bytes(int rt, int tgw, int hd) {
   return tgw > 1 ? tgw * 16 * rt * 16 + (tgw - 1) * 16 * rt * hd * 4 : 0;
 }
-__device__ __host__ constexpr int fa_ring_lds_bytes(int rt, int tw, int ns, int tgw, bool kv8, int hd) {
-  return tgw * fa_ring_group_bytes(tw, ns, kv8, hd) > fa_ring_merge_bytes(rt, tgw, hd)
-             ? tgw * fa_ring_group_bytes(tw, ns, kv8, hd)
+__device__ __host__ constexpr int fa_ring_lds_bytes(int rt, int nwv, int tw, int ns, int tgw, bool kv8, int hd) {
+  return tgw * fa_ring_group_bytes(nwv, tw, ns, kv8, hd) > fa_ring_merge_bytes(rt, tgw, hd)
+             ? tgw * fa_ring_group_bytes(nwv, tw, ns, kv8, hd)
              : fa_ring_merge_bytes(rt, tgw, hd);
 }
 

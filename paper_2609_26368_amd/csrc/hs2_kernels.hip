@@ -175,7 +175,11 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int CPR = RB / 16;                             // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;                // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * RB;                          // ring stage: K rows then V rows
-  constexpr int GB = fa_ring_group_bytes(TW, NS, KV8, HDIM);  // LDS of one token group: ring + V tile
+  constexpr int GB = fa_ring_group_bytes(NWV, TW, NS, KV8, HDIM);  // LDS of one token group: ring + tiles
+  // E4M3 with several waves per group: K is converted once into a shared
+  // bf16 tile too (each wave would otherwise convert the whole tile for its
+  // own row tiles)
+  constexpr bool KCONV = KV8 && NWV > 1;
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads for every wave and stage");
   static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
   extern __shared__ __align__(16) unsigned char smem[];
@@ -211,6 +215,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * GB);
   unsigned char* ring_p = smem + tg * GB;
   unsigned char* tile_p = ring_p + NS * SB;  // KV8: the converted V tile
+  unsigned char* tile_k = tile_p + TW * SRB;  // KCONV: the converted K tile
   // logits output of a single row tile (C G <= 16 query rows): this lane's
   // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
   float* lrow = nullptr;
@@ -271,11 +276,17 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       continue;
     }
     if constexpr (KV8) convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_p, 64 * wave + lane);
+    if constexpr (KCONV) {
+      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, 64 * wave + lane);
+      __syncthreads();  // both tiles converted by every wave of the group
+    }
     const int t0 = t_begin + i * TW;
     f32x4 S[NB][RPW];
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
-      if constexpr (KV8)
+      if constexpr (KCONV)
+        qk_block_swz<RPW>(tile_k, bi, q, S[bi], lane);
+      else if constexpr (KV8)
         qk_block_e4m3<RPW, RB>(stg, bi, q, S[bi], lane);
       else
         qk_block_swz<RPW>(stg, bi, q, S[bi], lane);
@@ -301,7 +312,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         }
     PFrags<NB, RPW> pf;
     online_softmax(st, S, pf, lane);
-    if (KV8 && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
+    if (KV8 && !KCONV && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
     const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
     pv_tile<RPW, NB, HDIM>(st, pf, vbase, lane);
   }
@@ -1511,8 +1522,8 @@ static hipError_t occupancy_capped(int* wgs, const void* fn, int threads, size_t
   return e;
 }
 
-constexpr size_t fa_ring_lds(int rt, int tw, int ns, int tgw, bool kv8, int hd) {
-  return (size_t)fa_ring_lds_bytes(rt, tw, ns, tgw, kv8, hd);
+constexpr size_t fa_ring_lds(int rt, int nwv, int tw, int ns, int tgw, bool kv8, int hd) {
+  return (size_t)fa_ring_lds_bytes(rt, nwv, tw, ns, tgw, kv8, hd);
 }
 
 template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
@@ -1522,7 +1533,7 @@ hipError_t fa_ring_occupancy(int* wgs) {
     return hipSuccess;
   } else {
     return occupancy_capped(wgs, (const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>, 64 * NWV * TGW,
-                            fa_ring_lds(RT, TW, NS, TGW, KV8, HDIM));
+                            fa_ring_lds(RT, NWV, TW, NS, TGW, KV8, HDIM));
   }
 }
 
@@ -1532,7 +1543,7 @@ hipError_t fa_ring_launch(const FaArgs& a, dim3 grid, hipStream_t s) {
     return hipErrorInvalidValue;
   } else {
     HS2_LAUNCH((k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>), grid, dim3(64 * NWV * TGW),
-               fa_ring_lds(RT, TW, NS, TGW, KV8, HDIM), s, a);
+               fa_ring_lds(RT, NWV, TW, NS, TGW, KV8, HDIM), s, a);
     return hipGetLastError();
   }
 }
