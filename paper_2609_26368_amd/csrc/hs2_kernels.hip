@@ -622,7 +622,9 @@ struct PoolShape {
   static constexpr int TW = RPL * NWV > TW_MIN ? RPL * NWV : TW_MIN;
   static constexpr int NS = 3;
   static constexpr int SB = TW * RB;                          // ring stage
-  static constexpr int LDS = NS * SB;                         // before the histograms
+  // E4M3 with several waves: K converted once into a shared bf16 tile
+  static constexpr bool KCONV = KV8 && NWV > 1;
+  static constexpr int LDS = NS * SB + (KCONV ? TW * SRB : 0);  // before the histograms
 };
 template <int RT, int GP, bool KV8, int HDIM>
 __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
@@ -711,11 +713,21 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = smem + (i % NS) * SB;
     const int t0 = t_begin + (ntiles - 1 - i) * TW;
+    unsigned char* tile_k = smem + NS * SB;
+    if constexpr (PS::KCONV) {
+      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, tid);
+      __syncthreads();  // the K tile converted by every wave
+    }
 #pragma unroll
     for (int bi = 0; bi < NB; ++bi) {
       const int row = 16 * bi + (lane & 15);
       uint4 k4[NKK];
-      if constexpr (KV8) {
+      if constexpr (PS::KCONV) {
+        const unsigned char* rp = tile_k + row * SRB;
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+          k4[kk] = *(const uint4*)(rp + 16 * (k_chunk(kk, lane) ^ stage_swz(row)));
+      } else if constexpr (KV8) {
 #pragma unroll
         for (int i = 0; i < NKK / 2; ++i) k_operands_e4m3<RB>(stg, row, i, lane, k4[2 * i], k4[2 * i + 1]);
       } else {
