@@ -3,7 +3,9 @@
 // Staging: cache rows go global -> LDS by 16-byte direct-to-LDS loads (no
 // register staging), row-major, 16-byte chunks swizzled by the row index so
 // that the MFMA K-operand reads and the transposing V reads
-// (ds_read_b64_tr_b16) need no padding; E4M3 rows are staged raw.
+// (ds_read_b64_tr_b16) are free of bank conflicts without padding; E4M3
+// rows are staged raw (swizzled too) and converted in registers (K) or into
+// a bf16 tile of the same layout (V; K as well when several waves share it).
 //
 // MFMA lane layouts used (checked on gfx950):
 //   16x16x32 bf16: lane l supplies A[l%16][8(l/16)+j] and B[8(l/16)+j][l%16],
@@ -11,7 +13,9 @@
 //   16x16x16 bf16: same with 4(l/16)+j, j = 0..3, for A and B.
 // Logits are computed as S^T = K . Q^T (tokens on MFMA rows, query rows on
 // MFMA columns): lane l then holds four tokens 4(l/16)+i of query row l%16,
-// which is exactly the A operand of the 16x16x16 product P . V.
+// which is exactly the A operand of the 16x16x16 product P . V (two such
+// blocks side by side: the A operand of a 16x16x32 product).  The logits'
+// k slots carry the head dims in the order of q_koff / k_chunk.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

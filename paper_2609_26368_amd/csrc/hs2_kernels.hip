@@ -762,8 +762,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 // Scores from the logits the full-attention ring kernel stored (small row
 // counts: C * G logits per token cost less traffic than re-reading K):
 // P = sum over h of exp2(s2_h - msub) * fac, the same constants as k_pool.
-// grid (chunks of LOGIT_CHUNK tokens, B * Hkv), 256 threads, 4 consecutive
-// tokens per thread; dynamic LDS: C packed histograms.
+// grid (chunks of split_tokens tokens, B * Hkv; the host sizes the chunks,
+// 1024-4096 tokens, for about two workgroups per CU), 256 threads, 4
+// consecutive tokens per thread; dynamic LDS: C packed histograms.
 __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint32_t* hist = (uint32_t*)smem;  // [C][NBINS/2], 16-bit packed counters
@@ -909,8 +910,9 @@ __device__ inline int block_scan_1024(int v, int* lds16, int& total) {
 //                 (key desc, index asc), i.e. by the 64-bit composite
 //                 (key << 32) | ~index, with an 8-bit radix select that stops
 //                 at the first digit whose keys are all taken, sets their
-//                 bits, then emits the bitmap's tokens in ascending order,
-//                 the window, and -1 padding.
+//                 bits (in an LDS copy of the row's bitmap, rows up to 512K
+//                 tokens), then emits the bitmap's tokens in ascending
+//                 order, the window, and -1 padding.
 // state: [3] candidates collected (starts at zero).
 constexpr int SELB = 1024;              // threads per selection workgroup
 constexpr int SEL_PER = 16;             // tokens per thread
