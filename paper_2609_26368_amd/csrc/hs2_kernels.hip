@@ -920,6 +920,9 @@ constexpr int SEL_TOKENS = SELB * SEL_PER;
 constexpr int SEL_LDS_CAND = 2048;      // candidates a workgroup gathers in LDS
 constexpr int RESOLVE_LDS_CAP = 6144;   // candidates the resolver keeps in LDS
 constexpr size_t SEL_BM_LDS_MAX = 65536; // largest row bitmap kept in LDS (524288 tokens)
+// longest rows selected by one workgroup (one chunk: with two, the 32K
+// decode's selection was 1.4 us slower than the two-kernel path)
+constexpr int SEL_FUSED_TOKENS = SEL_PER * SELB;
 static_assert(NBINS == SELB, "one histogram bin per thread");
 
 struct SelShared {
@@ -969,7 +972,7 @@ __device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const 
 // The need largest of the m candidates get their bitmap bits (in the row's
 // LDS copy sbm when given, else in the global bitmap).
 __device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, SelShared& sh,
-                                   uint64_t* sbm) {
+                                   uint64_t* sbm, bool comp_ready = false) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const uint32_t* ck = a.cand_key + row * a.cand_cap;
   const int32_t* ci = a.cand_idx + row * a.cand_cap;
@@ -979,7 +982,7 @@ __device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int 
   auto composite = [&](int i) -> uint64_t {
     return in_lds ? sh.u.comp[i] : (((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]));
   };
-  if (in_lds)
+  if (in_lds && !comp_ready)  // (comp_ready: the caller built them in LDS)
     for (int i = tid; i < m; i += SELB) sh.u.comp[i] = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
   uint64_t thresh = 0;  // composite of the need-th largest (0: take every candidate)
   if (need < m) {
@@ -1076,26 +1079,13 @@ __device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri
   for (int j = base + nw + tid; j < a.S; j += SELB) out[j] = -1;
 }
 
-__global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
-  __shared__ SelShared sh;
-  const int64_t row = blockIdx.y;
-  const RowInfo ri = row_info(a, row);
-  const int t0 = blockIdx.x * SEL_TOKENS;
-  if (t0 >= ri.N) return;
-  const int t1 = min(ri.N, t0 + SEL_TOKENS);
-  const float* P = a.scores + row * a.score_stride;
-  uint64_t* bm = a.bitmap + row * a.bitmap_words;
-  int* st = a.state + row * 8;
+// One chunk of a row's candidates [t0, t1) (the thread's SEL_PER scores in
+// v, token t0 + SELB j + threadIdx.x): sets the bitmap words of the tokens
+// above b* (bm: global or LDS) and appends the tokens of b* to the LDS list
+// (sh.n; past its capacity to global slots reserved in state[3]).
+__device__ inline void filter_chunk(const SelArgs& a, int64_t row, const Threshold& th, int t0, int t1,
+                                    const float (&v)[SEL_PER], SelShared& sh, int* st, uint64_t* bm) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float v[SEL_PER];
-#pragma unroll
-  for (int j = 0; j < SEL_PER; ++j) {
-    const int t = t0 + SELB * j + tid;
-    v[j] = t < t1 ? P[t] : 0.f;
-  }
-  if (tid == 0) sh.n = 0;
-  const Threshold th = find_threshold(a, row, ri, sh);
-  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
   // per mode: tokens with digit > sel_above are taken, those equal to
   // cand_digit are candidates (mode 0: none; 1: every valid token)
   const int sel_above = th.mode == 2 ? th.bstar : (th.mode == 1 ? -1 : NBINS);
@@ -1139,6 +1129,29 @@ __global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
       }
     }
   }
+}
+
+__global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
+  __shared__ SelShared sh;
+  const int64_t row = blockIdx.y;
+  const RowInfo ri = row_info(a, row);
+  const int t0 = blockIdx.x * SEL_TOKENS;
+  if (t0 >= ri.N) return;
+  const int t1 = min(ri.N, t0 + SEL_TOKENS);
+  const float* P = a.scores + row * a.score_stride;
+  uint64_t* bm = a.bitmap + row * a.bitmap_words;
+  int* st = a.state + row * 8;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float v[SEL_PER];
+#pragma unroll
+  for (int j = 0; j < SEL_PER; ++j) {
+    const int t = t0 + SELB * j + tid;
+    v[j] = t < t1 ? P[t] : 0.f;
+  }
+  if (tid == 0) sh.n = 0;
+  const Threshold th = find_threshold(a, row, ri, sh);
+  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
+  filter_chunk(a, row, th, t0, t1, v, sh, st, bm);
   __syncthreads();
   const int n = min(sh.n, SEL_LDS_CAND);
   if (n > 0) {
@@ -1172,6 +1185,64 @@ __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
   if (th.mode == 2) resolve_row(a, row, th.need, m, sh, BM_LDS ? sbm : nullptr);
   __syncthreads();
   emit_row(a, row, ri, sh, BM_LDS ? sbm : nullptr);
+}
+
+// Rows of at most SEL_FUSED_TOKENS candidates: one workgroup per row filters
+// every chunk into an LDS bitmap and LDS candidate list, then selects and
+// emits (one launch; the two-kernel path above serves longer rows, whose
+// chunks need more workgroups).
+__global__ __launch_bounds__(SELB) void k_sel_fused(SelArgs a) {
+  __shared__ SelShared sh;
+  extern __shared__ __align__(16) uint64_t sbm[];
+  const int64_t row = blockIdx.x;
+  const RowInfo ri = row_info(a, row);
+  const float* P = a.scores + row * a.score_stride;
+  int* st = a.state + row * 8;
+  const int tid = threadIdx.x;
+  if (tid == 0) sh.n = 0;
+  const Threshold th = find_threshold(a, row, ri, sh);
+  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
+  for (int t0 = 0; t0 < ri.N; t0 += SEL_TOKENS) {
+    const int t1 = min(ri.N, t0 + SEL_TOKENS);
+    float v[SEL_PER];
+#pragma unroll
+    for (int j = 0; j < SEL_PER; ++j) {
+      const int t = t0 + SELB * j + tid;
+      v[j] = t < t1 ? P[t] : 0.f;
+    }
+    filter_chunk(a, row, th, t0, t1, v, sh, st, sbm);
+  }
+  __syncthreads();
+  const int n = sh.n;
+  if (th.mode == 2 && n > 0) {
+    if (n <= SEL_LDS_CAND) {  // every candidate in LDS: composites in place, through registers
+      uint64_t cv[SEL_LDS_CAND / SELB];
+#pragma unroll
+      for (int r = 0; r < SEL_LDS_CAND / SELB; ++r) {
+        const int i = tid + SELB * r;
+        cv[r] = i < n ? ((uint64_t)sh.u.cand.key[i] << 32) | (uint32_t)(~sh.u.cand.idx[i]) : 0ull;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < SEL_LDS_CAND / SELB; ++r)
+        if (tid + SELB * r < n) sh.u.comp[tid + SELB * r] = cv[r];
+      __syncthreads();
+      resolve_row(a, row, th.need, n, sh, sbm, true);
+    } else {  // the LDS part joins the overflow in global memory
+      if (tid == 0) sh.base = atomicAdd(&st[3], SEL_LDS_CAND);
+      __syncthreads();
+      const int64_t dst = row * a.cand_cap + sh.base;
+      for (int i = tid; i < SEL_LDS_CAND; i += SELB) {
+        a.cand_key[dst + i] = sh.u.cand.key[i];
+        a.cand_idx[dst + i] = sh.u.cand.idx[i];
+      }
+      __threadfence_block();
+      __syncthreads();
+      resolve_row(a, row, th.need, min(n, (int)a.cand_cap), sh, sbm);
+    }
+  }
+  __syncthreads();
+  emit_row(a, row, ri, sh, sbm);
 }
 
 // ---------------------------------------------------------------------------- block-level selection
@@ -1744,6 +1815,10 @@ hipError_t launch_block_select(const BlockSelArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_select(const SelArgs& a, hipStream_t s) {
+  if (a.max_len <= SEL_FUSED_TOKENS) {
+    HS2_LAUNCH(k_sel_fused, dim3((unsigned)a.rows), dim3(SELB), (size_t)a.bitmap_words * sizeof(uint64_t), s, a);
+    return hipGetLastError();
+  }
   const int64_t chunks = ((int64_t)a.max_len + SEL_TOKENS - 1) / SEL_TOKENS;
   HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELB), 0, s, a);
   hipError_t e = hipGetLastError();

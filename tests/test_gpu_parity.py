@@ -268,6 +268,10 @@ SEL = [
     # every chunk overflows the filter's LDS candidate buffer; the row's
     # candidates exceed the resolver's LDS capacity
     ("all_equal_long", 1, 1, 2, 20000, 5000, 64, "const"),
+    # one-workgroup rows (at most 16384 tokens): candidates past the
+    # resolver's LDS capacity, and a row of exactly the limit
+    ("all_equal_one_chunk", 1, 1, 1, 16000, 3000, 32, "const"),
+    ("lognormal_16384", 2, 1, 1, 16384, 1024, 64, "lognormal"),
     ("denormals_and_zeros", 1, 1, 3, 2000, 100, 10, "tiny"),
     ("lognormal_long", 1, 2, 1, 200000, 4096, 256, "lognormal"),
     ("k_equals_N", 1, 1, 1, 1000, 990, 10, "uniform"),
