@@ -554,9 +554,8 @@ __device__ __forceinline__ void pool_emit_block(const f32x4 (&acc)[RPW], float c
       // rows 16 rt + 4 q4 .. belong to query (16 rt + 4 q4) / GP; one lane group per query emits
       if (((4 * q4) & (GP - 1)) == 0) emit(v, (16 * (rt0 + rr) + 4 * q4) / GP, t);
     }
-  } else {
+  } else if constexpr (RPW % (GP / 16) == 0) {
     constexpr int TPQ = GP / 16;  // row tiles per query, all in this wave
-    static_assert(RPW % TPQ == 0, "a query's row tiles must belong to one wave");
 #pragma unroll
     for (int cq = 0; cq < RPW / TPQ; ++cq) {
       float v = 0.f;
@@ -568,6 +567,13 @@ __device__ __forceinline__ void pool_emit_block(const f32x4 (&acc)[RPW], float c
       v = sum_xor32(sum_xor16(v));
       if (q4 == 0) emit(v, (16 * rt0) / GP + cq, t);
     }
+  } else {  // this wave holds RPW of the query's row tiles: emit its part of the sum
+    static_assert((GP / 16) % RPW == 0, "a query's row tiles split evenly over its waves");
+    float v = 0.f;
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) v += (e[rr][0] + e[rr][1]) + (e[rr][2] + e[rr][3]);
+    v = sum_xor32(sum_xor16(v));
+    if (q4 == 0) emit(v, (16 * rt0) / GP, t);
   }
 }
 
@@ -604,13 +610,17 @@ __device__ __forceinline__ void pool_row_consts(const PoolArgs& a, int b, int g,
 // KV8: E4M3 cache with one K scale per KV head (folded into the logit
 // scale); raw rows are staged (swizzled by raw_swz) and each wave converts
 // its K operands in registers.  HDIM: head dim (128 or 256).
-template <int RT, int GP, bool KV8 = false, int HDIM = HD>
+template <int RT, int GP, bool KV8, int HDIM>
 struct PoolShape {
   static constexpr int TPQ = GP > 16 ? GP / 16 : 1;           // row tiles per query
-  // row tiles per wave: a query's tiles stay in one wave (its heads are
-  // summed in registers); one tile per wave otherwise (more waves per
-  // workgroup share each staged tile: 134 -> 126 us at 64 rows per KV head)
-  static constexpr int RPW = RT == 1 ? 1 : TPQ;
+  // row tiles per wave: one tile per wave for queries of at most 16 heads
+  // (more waves share each staged tile: 134 -> 126 us at 64 rows per KV
+  // head); a query of 32 heads in one wave (its heads summed in registers);
+  // of 64 heads, with a bf16 cache, in two waves whose per-token sums meet
+  // in LDS (MQA 64/1: 106 -> 104 us at one query, 62 -> 54 us at two; with
+  // E4M3 one wave stays 8 % faster)
+  static constexpr int RPW = RT == 1 ? 1 : (TPQ > 2 && !KV8 ? TPQ / 2 : TPQ);
+  static constexpr int WPQ = TPQ / RPW > 1 ? TPQ / RPW : 1;  // waves per query
   static constexpr int NWV = RT / RPW;
   static constexpr int SRB = 2 * HDIM;                        // bytes of a bf16 stage row
   static constexpr int RB = KV8 ? HDIM : SRB;                 // bytes of a staged row
@@ -627,7 +637,7 @@ struct PoolShape {
   static constexpr int LDS = NS * SB + (KCONV ? TW * SRB : 0);  // before the histograms
 };
 template <int RT, int GP, bool KV8, int HDIM>
-__global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>::NWV))) void k_pool(PoolArgs a) {
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP, KV8, HDIM>::NWV))) void k_pool(PoolArgs a) {
   using PS = PoolShape<RT, GP, KV8, HDIM>;
   constexpr int RPW = PS::RPW, NWV = PS::NWV, TW = PS::TW, NS = PS::NS, SB = PS::SB, RB = PS::RB, SRB = PS::SRB;
   constexpr int NB = TW / 16;
@@ -695,6 +705,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 
   float* scores = a.scores + ((int64_t)b * a.Hkv + g) * a.C * a.score_stride;
   const int nc0 = Lv - a.C - a.W + 1;  // candidates of query 0 (query c: nc0 + c)
+  int t0_tile = 0;
+  __shared__ float s_part[PS::WPQ > 1 ? NWV * TW : 1];  // per-token parts of split queries
+  auto emit_part = [&](float v, int, int t) { s_part[wave * TW + (t - t0_tile)] = v; };
   auto emit = [&](float v, int c, int t) {
     if (c < a.C && t < nc0 + c) {
       scores[c * a.score_stride + t] = v;
@@ -713,6 +726,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
     if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = smem + (i % NS) * SB;
     const int t0 = t_begin + (ntiles - 1 - i) * TW;
+    t0_tile = t0;
     unsigned char* tile_k = smem + NS * SB;
     if constexpr (PS::KCONV) {
       convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, tid);
@@ -743,7 +757,19 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP>
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
       }
-      pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
+      if constexpr (PS::WPQ == 1)
+        pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
+      else
+        pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit_part);
+    }
+    if constexpr (PS::WPQ > 1) {  // the query's first wave adds its waves' parts and emits
+      __syncthreads();
+      if (wave % PS::WPQ == 0 && lane < TW) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < PS::WPQ; ++w) v += s_part[(wave + w) * TW + lane];
+        emit(v, wave / PS::WPQ, t0 + lane);
+      }
     }
   }
   __syncthreads();
@@ -1704,7 +1730,7 @@ hipError_t launch_pool_logits(const PoolArgs& a, hipStream_t s) {
 
 template <int RT, int GP, bool KV8, int HDIM>
 hipError_t pool_occupancy(int* wgs, int C) {
-  return occupancy_capped(wgs, (const void*)k_pool<RT, GP, KV8, HDIM>, 64 * PoolShape<RT, GP>::NWV,
+  return occupancy_capped(wgs, (const void*)k_pool<RT, GP, KV8, HDIM>, 64 * PoolShape<RT, GP, KV8, HDIM>::NWV,
                           pool_smem_bytes<RT, GP, KV8, HDIM>(C));
 }
 
@@ -1723,7 +1749,7 @@ hipError_t pool_wgs_per_cu(int RT, int Gp, int C, bool kv8, int hd, int* wgs) {
 
 template <int RT, int GP, bool KV8, int HDIM>
 hipError_t launch_pool_one(const PoolArgs& a, dim3 grid, int hc, hipStream_t s) {
-  HS2_LAUNCH((k_pool<RT, GP, KV8, HDIM>), grid, dim3(64 * PoolShape<RT, GP>::NWV),
+  HS2_LAUNCH((k_pool<RT, GP, KV8, HDIM>), grid, dim3(64 * PoolShape<RT, GP, KV8, HDIM>::NWV),
              (pool_smem_bytes<RT, GP, KV8, HDIM>(hc)), s, a);
   return hipGetLastError();
 }
