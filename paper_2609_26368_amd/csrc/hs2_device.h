@@ -426,7 +426,7 @@ __device__ __host__ constexpr int fa_ring_lds_bytes(int rt, int nwv, int tw, int
 // an 8-row block (r < 4 within it): those rows' stage_swz differ in bit 0,
 // so each of the two stores of 8 lanes covers 8 distinct 16-byte slots of a
 // 128-byte window, and so does the raw read.
-template <int NR, int NTHR, int HDIM = HD>
+template <int NR, int NTHR, int HDIM>
 __device__ inline void convert_rows_e4m3(const unsigned char* raw, unsigned char* stg, int tid) {
   constexpr int PPR = HDIM / 16;  // raw pieces per row
   constexpr int JOBS = NR * PPR;
@@ -466,7 +466,7 @@ __device__ inline void wait_ring(int stages) {
 
 // V operand of P.V for block blk, columns 16 nb .. 16 nb + 15, read
 // transposed from the row-major swizzled V rows (2 HDIM bytes) at `vbase`.
-template <int HDIM = HD>
+template <int HDIM>
 __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int nb, int lane) {
   const int kq = lane & 15;
   const int row = 16 * blk + 4 * (lane >> 4) + (kq >> 2);
