@@ -48,8 +48,13 @@
  * (full-attention kernel shape), HS2_FA_SPLIT / HS2_POOL_SPLIT /
  * HS2_SA_SPLIT (tokens or slots per workgroup), HS2_FA_ROUNDS (workgroup
  * rounds the full-attention splits are sized for), HS2_POOL_FROM_K=1
- * (recompute the scores from K even where the stored logits would serve).
- * None changes a result beyond floating-point summation order.
+ * (recompute the scores from K even where the stored logits would serve),
+ * HS2_FA_CACHE_POLICY (0: every full-attention load cacheable, 1: V rows
+ * non-temporal, 2: K and V non-temporal, 3: V and the leading K rows of
+ * each token group non-temporal; 1 and 2 exist for one query row tile, 3
+ * for more) and HS2_FA_K_KEEP (percent of each token group's K rows that
+ * policy 3 keeps cacheable).  None changes a result beyond floating-point
+ * summation order; the cache policies change none at all.
  */
 #ifndef HS2_H
 #define HS2_H

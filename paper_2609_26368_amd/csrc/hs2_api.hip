@@ -28,6 +28,10 @@ constexpr int32_t kMaxLen = 1 << 27;
 constexpr int kNBins = 1024;          // must match the kernels' first-level radix bins
 constexpr int kSelChunk = hs2::SEL_CHUNK;  // tokens per workgroup of the selection scans
 constexpr size_t kAlign = 256;
+// share of each full-attention token group whose K rows stay cacheable when
+// the score pass re-reads K (percent; the rest streams past the caches)
+constexpr int kFaKeepPercent = 75;
+constexpr int64_t kLastLevelCacheBytes = 256ll << 20;  // MI355X memory-side cache
 
 thread_local std::string g_last_error;
 
@@ -62,6 +66,8 @@ struct Plan {
   int RT, TG;                 // full-attention / pooling row tiles
   int fa_variant;             // ring kernel shape (0, 2, 3, 4) for RT <= 4; 1: workgroup kernel
   int fa_split, fa_nsplit;
+  int fa_cache_policy;  // FaCachePolicy of the full-attention ring kernel
+  int fa_k_stream;      // FA_STREAM_K_HEAD: leading K rows of each token group read non-temporal
   int logit_chunk;
   int pool_split, pool_nsplit;
   int64_t units;              // B * Hkv
@@ -206,6 +212,27 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   // from them instead of re-reading K (256 bytes per token)
   p.pool_logits = p.RT == 1 && p.fa_variant != 1 && env_int("HS2_POOL_FROM_K", 0) == 0;
   p.logit_stride = round_up(p.Lmax, 64);
+  // Cache policy of the full-attention ring kernel's loads.  A cache that
+  // fits the last-level cache keeps every row cacheable (a decode loop finds
+  // it there again).  A larger one streams V.  K streams too where the scores
+  // come from the stored logits; where the score pass re-reads K, the last
+  // kFaKeepPercent (HS2_FA_K_KEEP) percent of each token group's K rows stay
+  // cacheable for it (it walks each split from the end); one row tile keeps
+  // all of K then (no per-tile policy switch).
+  {
+    const int64_t kv_bytes = 2 * (int64_t)p.B * p.Hkv * p.Lmax * p.D * (kv8 ? 1 : 2);
+    const bool stream = kv_bytes > kLastLevelCacheBytes;
+    const int part = p.fa_split / std::max(1, p.TG);
+    int keep = kFaKeepPercent;
+    const int ek = env_int("HS2_FA_K_KEEP", -1);
+    if (ek >= 0 && ek <= 100) keep = ek;
+    p.fa_cache_policy = !stream ? FA_CACHE_DEFAULT
+                        : p.RT == 1 ? (p.pool_logits ? FA_STREAM_KV : FA_STREAM_V)
+                                    : FA_STREAM_K_HEAD;
+    p.fa_k_stream = part - (int)((int64_t)part * keep / 100);
+    const int ep = env_int("HS2_FA_CACHE_POLICY", -1);
+    if (ep >= 0 && fa_cache_policy_built(p.RT, ep)) p.fa_cache_policy = ep;
+  }
   // score pass over stored logits: chunks of 1024-4096 tokens (whole float4
   // steps of its 256 threads), about two workgroups per CU
   p.logit_chunk = (int)std::min<int64_t>(
@@ -493,6 +520,8 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   fa.n_split = p.fa_nsplit;
   fa.logits = p.pool_logits ? (float*)(ws + p.off_logits) : nullptr;
   fa.logit_stride = p.logit_stride;
+  fa.cache_policy = p.fa_cache_policy;
+  fa.k_stream_tokens = p.fa_k_stream;
   HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, p.fa_variant, s));
 
   CombineArgs ca{};
@@ -547,6 +576,7 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   pa.n_split = p.pool_nsplit;
   pa.logits = fa.logits;
   pa.logit_stride = p.logit_stride;
+  pa.k_stream = p.fa_cache_policy != FA_CACHE_DEFAULT;
   if (p.pool_logits)
     HS2_TRY_LAUNCH(KK_POOL_LOGITS, s, launch_pool_logits(pa, s));
   else

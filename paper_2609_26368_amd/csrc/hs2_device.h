@@ -245,6 +245,16 @@ __device__ inline void dma16(const void* src, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_base) : "memory");
 }
 
+// The same load with the non-temporal hint when NTH: for rows read once, they
+// stream past the caches instead of evicting lines a later pass reads again.
+template <bool NTH>
+__device__ inline void dma16_p(const void* src, uint32_t lds_base) {
+  if constexpr (NTH)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" : : "v"(src), "s"(lds_base) : "memory");
+  else
+    dma16(src, lds_base);
+}
+
 __device__ inline uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }

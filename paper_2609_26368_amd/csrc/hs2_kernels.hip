@@ -22,6 +22,8 @@
 // Query rows of one (sequence, KV head) group are laid out query-major:
 // row r = c * Gp + h with Gp = G rounded up to a power of two; rows with
 // h >= G or c >= C are padding (zero queries, never written out).
+#include <type_traits>
+
 #include "hs2_device.h"
 #include "hs2_launch.h"
 
@@ -164,8 +166,8 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // raw and converts them in registers, and converts the V rows of the
 // current tile into one bf16 tile (before the logits, so that the
 // conversion overlaps them; one barrier before P.V).  HDIM: head dim (128
-// or 256).
-template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+// or 256).  KP: cache policy of the stage loads (FaCachePolicy).
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM, int KP>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
   constexpr int NB = TW / 16;                              // 16-row blocks per stage
@@ -240,7 +242,9 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     const int row = RPL * (wave * LPM + u) + lane / CPR;
     lane_off[u] = lane_offset(row, row);
   }
-  auto issue = [&](int tile) {
+  // K_NT: this tile's K rows are loaded non-temporal (V rows: every policy
+  // but the default)
+  auto issue_as = [&](int tile, auto k_nt) __attribute__((always_inline)) {
     const int t0 = t_begin + tile * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
@@ -253,8 +257,18 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         const int row = RPL * n + lane / CPR;
         off = lane_offset(row, min(t0 + row, t_end - 1));
       }
-      dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
-      dma16(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
+      dma16_p<decltype(k_nt)::value>(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16_p<KP != FA_CACHE_DEFAULT>(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
+    }
+  };
+  auto issue = [&](int tile) __attribute__((always_inline)) {
+    if constexpr (KP == FA_STREAM_K_HEAD) {  // one scalar branch per tile
+      if (tile * TW < a.k_stream_tokens)
+        issue_as(tile, std::true_type{});
+      else
+        issue_as(tile, std::false_type{});
+    } else {
+      issue_as(tile, std::integral_constant<bool, KP == FA_STREAM_KV>{});
     }
   };
 
@@ -685,7 +699,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
   // tiles from the end of the split backwards: at equal split lengths the
   // full-attention pass read those rows last (2 % faster at 64 rows per KV
   // head, where the two passes' ranges coincide)
-  auto issue = [&](int tile) {
+  // the last pass over these K rows: a cache larger than the last-level
+  // cache streams them (non-temporal) past the caches
+  auto issue_as = [&](int tile, auto k_nt) __attribute__((always_inline)) {
     const int t0 = t_begin + (ntiles - 1 - tile) * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
@@ -698,8 +714,14 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
         const int row = RPL * n + lane / CPR;
         off = lane_offset(row, min(t0 + row, t_end - 1));
       }
-      dma16(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16_p<decltype(k_nt)::value>(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
     }
+  };
+  auto issue = [&](int tile) __attribute__((always_inline)) {  // one scalar branch per tile
+    if (a.k_stream)
+      issue_as(tile, std::true_type{});
+    else
+      issue_as(tile, std::false_type{});
   };
   __syncthreads();  // histogram cleared before any wave adds to it
 
@@ -1642,31 +1664,57 @@ hipError_t fa_ring_occupancy(int* wgs) {
   if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
     *wgs = 0;
     return hipSuccess;
-  } else {
-    return occupancy_capped(wgs, (const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>, 64 * NWV * TGW,
+  } else {  // the cache policy changes no resource
+    return occupancy_capped(wgs, (const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM, FA_CACHE_DEFAULT>, 64 * NWV * TGW,
                             fa_ring_lds(RT, NWV, TW, NS, TGW, KV8, HDIM));
   }
 }
 
-template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM, int KP>
 hipError_t fa_ring_launch(const FaArgs& a, dim3 grid, hipStream_t s) {
-  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
+  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM) || !fa_cache_policy_built(RT, KP)) {
     return hipErrorInvalidValue;
   } else {
-    HS2_LAUNCH((k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>), grid, dim3(64 * NWV * TGW),
+    HS2_LAUNCH((k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM, KP>), grid, dim3(64 * NWV * TGW),
                fa_ring_lds(RT, NWV, TW, NS, TGW, KV8, HDIM), s, a);
     return hipGetLastError();
   }
 }
 
-template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
-hipError_t fa_ring_allow_lds(int bytes) {
-  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM)) {
+template <int RT, int NWV, int TW, int NS, int TGW, int HDIM>
+hipError_t fa_ring_dispatch(const FaArgs& a, dim3 grid, hipStream_t s) {
+  const bool kv8 = a.k_scale != nullptr;
+  switch (a.cache_policy) {
+#define HS2_KP_CASE(kp)                                                                   \
+  case kp:                                                                                \
+    return kv8 ? fa_ring_launch<RT, NWV, TW, NS, TGW, true, HDIM, kp>(a, grid, s)         \
+               : fa_ring_launch<RT, NWV, TW, NS, TGW, false, HDIM, kp>(a, grid, s);
+    HS2_KP_CASE(FA_CACHE_DEFAULT)
+    HS2_KP_CASE(FA_STREAM_V)
+    HS2_KP_CASE(FA_STREAM_KV)
+    HS2_KP_CASE(FA_STREAM_K_HEAD)
+#undef HS2_KP_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM, int KP>
+hipError_t fa_ring_allow_lds_kp(int bytes) {
+  if constexpr (!fa_ring_ok(NWV, TW, KV8, HDIM) || !fa_cache_policy_built(RT, KP)) {
     return hipSuccess;
   } else {
-    return hipFuncSetAttribute((const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM>,
+    return hipFuncSetAttribute((const void*)k_fa_ring<RT, NWV, TW, NS, TGW, KV8, HDIM, KP>,
                                hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   }
+}
+
+template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM>
+hipError_t fa_ring_allow_lds(int bytes) {
+  hipError_t e = fa_ring_allow_lds_kp<RT, NWV, TW, NS, TGW, KV8, HDIM, FA_CACHE_DEFAULT>(bytes);
+  if (e == hipSuccess) e = fa_ring_allow_lds_kp<RT, NWV, TW, NS, TGW, KV8, HDIM, FA_STREAM_V>(bytes);
+  if (e == hipSuccess) e = fa_ring_allow_lds_kp<RT, NWV, TW, NS, TGW, KV8, HDIM, FA_STREAM_KV>(bytes);
+  if (e == hipSuccess) e = fa_ring_allow_lds_kp<RT, NWV, TW, NS, TGW, KV8, HDIM, FA_STREAM_K_HEAD>(bytes);
+  return e;
 }
 
 hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
@@ -1690,10 +1738,8 @@ hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
   dim3 grid(a.n_split, a.Hkv, a.B);
-#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd)                                              \
-  if (variant == v && RT == rt)                                                                    \
-    return a.k_scale ? fa_ring_launch<rt, nwv, tw, ns, tgw, true, hd>(a, grid, s)                   \
-                     : fa_ring_launch<rt, nwv, tw, ns, tgw, false, hd>(a, grid, s);
+#define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd) \
+  if (variant == v && RT == rt) return fa_ring_dispatch<rt, nwv, tw, ns, tgw, hd>(a, grid, s);
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
 #undef HS2_RING_LAUNCH
   if (a.k_scale || variant != 1) return hipErrorInvalidValue;  // E4M3 only through the ring kernels

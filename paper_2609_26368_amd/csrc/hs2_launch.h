@@ -20,7 +20,24 @@ struct FaArgs {
   float* logits;   // [B*Hkv][C*G][logit_stride] logits in log2 units (ring kernels), or null
   int64_t logit_stride;
   const float* k_scale;  // [Hkv] for an E4M3 cache (K, V are then byte arrays), else null
+  int cache_policy;      // ring kernels: FaCachePolicy of the stage loads
+  int k_stream_tokens;   // FA_STREAM_K_HEAD: K rows of a token group before this offset are non-temporal
 };
+
+// Cache policy of the full-attention ring kernel's loads.  Non-temporal
+// rows stream past the caches: for rows read once, so that they do not
+// evict lines a later pass reads again.
+enum FaCachePolicy {
+  FA_CACHE_DEFAULT = 0,  // every row cacheable
+  FA_STREAM_V = 1,       // V non-temporal, K cacheable
+  FA_STREAM_KV = 2,      // K and V non-temporal
+  FA_STREAM_K_HEAD = 3,  // V non-temporal, K non-temporal before k_stream_tokens of each token group
+};
+// Policies built for each query row tile count: one row tile takes no
+// per-tile branch (it is latency-sensitive), more row tiles take the split one.
+constexpr bool fa_cache_policy_built(int rt, int kp) {
+  return kp == FA_CACHE_DEFAULT || (rt == 1 ? (kp == FA_STREAM_V || kp == FA_STREAM_KV) : kp == FA_STREAM_K_HEAD);
+}
 
 struct CombineArgs {
   const float* part_o;
@@ -59,6 +76,7 @@ struct PoolArgs {
   float c2;
   int B, C, Hq, Hkv, G, Gp, max_len, W;
   int split_tokens, n_split;
+  int k_stream;          // k_pool: K rows are read non-temporal (the last pass over them)
 };
 
 struct SelArgs {
