@@ -9,10 +9,19 @@ Default workload: 8-query verify chunk per sequence, batch 4, 131072-token
 context, 32 query / 4 KV heads, head_dim 128, top-k 4096 + window 256,
 1 full + 3 sparse layers (bf16 cache, fp32 accumulation).
 
+Caches: by default the KV cache is rotated over several identical copies on
+the device (at least 4, and at least 2 GiB in all), one copy per step in
+turn, so no step finds its cache in the 256 MB memory-side cache or the L2
+from an earlier step (a real decode step runs the model's other layers
+between two calls of this block).  --caches flush reads a 1 GiB buffer
+before every step instead; --caches warm replays one copy.
+
 Prints one JSON line (rank 0, N = 1).  Extra fields: achieved algorithmic
 GB/s of the step, the roofline of the dominant kernel (full-attention split
-kernel) from HIP events around its launches, per-kernel averages, and the
-CPU oracle timed on a bounded sample of the same workload.
+kernel) from HIP events around its launches, the measured streaming-read
+ceiling of the device (hs2_stream_read_probe), per-kernel averages,
+per-step percentiles, and the CPU oracle timed on a bounded sample of the
+same workload (all host threads, and one thread).
 """
 from __future__ import annotations
 
@@ -60,7 +69,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="budget of the oracle sample (half all threads, half one thread)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sa-sink-gate", action="store_true",
                     help="sparse layers with per-head sink logits and sigmoid output gates (hs2_sparse_attn_ex)")
@@ -70,8 +80,14 @@ def parse():
                     help="block-level selection with blocks of this many tokens (hs2_full_attn_score_select_blocks)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time its replays (no per-kernel host launches)")
-    ap.add_argument("--cold", action="store_true",
-                    help="evict the caches (read a 1 GiB buffer) before every step; steps timed one by one")
+    ap.add_argument("--caches", choices=("rotate", "flush", "warm"), default="rotate",
+                    help="rotate: a different copy of the KV cache every step (default); flush: read a 1 GiB buffer "
+                         "before every step (timed one by one); warm: the same cache every step")
+    ap.add_argument("--kv-copies", type=int, default=0,
+                    help="copies of the KV cache to rotate over (default: at least 4 and at least 2 GiB)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="only measure the streaming-read ceiling (hs2_stream_read_probe) and print it")
+    ap.add_argument("--no-stream-probe", action="store_true", help="leave the streaming-read probe out of the line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of COPY_BYTES (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
@@ -133,6 +149,52 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload
     print(json.dumps(rec))
 
 
+STREAM_PROBE_BYTES = 4 << 30
+STREAM_PROBE_MODES = {0: "register loads", 1: "register loads, non-temporal", 2: "direct-to-LDS loads",
+                      3: "direct-to-LDS loads, non-temporal"}
+
+
+def stream_probe(dev, reps: int = 8) -> dict:
+    """Streaming-read ceiling of the device: hs2_stream_read_probe over a
+    4 GiB buffer (16x the memory-side cache) in each load mode; the median of
+    `reps` timed launches per mode, the best mode's rate as the ceiling."""
+    import torch
+    from paper_2609_26368_amd import hs2
+    buf = torch.empty(STREAM_PROBE_BYTES // 4, dtype=torch.int32, device=dev)
+    buf.random_()
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream()
+    rates = {}
+    for mode in STREAM_PROBE_MODES:
+        for _ in range(2):
+            hs2.hs2_stream_read_probe(buf, mode, sink, st)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a_, b_ in ev:
+            a_.record(st)
+            hs2.hs2_stream_read_probe(buf, mode, sink, st)
+            b_.record(st)
+        torch.cuda.synchronize()
+        ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in ev]))
+        rates[mode] = STREAM_PROBE_BYTES / (ms * 1e-3) / 1e9
+    del buf
+    torch.cuda.empty_cache()
+    best = max(rates, key=rates.get)
+    return {"stream_peak_gbps": round(rates[best], 1), "mode": STREAM_PROBE_MODES[best],
+            "gbps_by_mode": {STREAM_PROBE_MODES[m]: round(r, 1) for m, r in rates.items()},
+            "bytes": STREAM_PROBE_BYTES, "launches_per_mode": reps}
+
+
+def kv_copies_for(kv_bytes: int, caches: str, requested: int) -> int:
+    """Copies of the KV cache the step rotates over: at least 4 and at least
+    2 GiB together (so that no step finds its cache in the 256 MB
+    memory-side cache), at most 1024; one when the caches are not rotated."""
+    if caches != "rotate":
+        return 1
+    if requested > 0:
+        return requested
+    return int(min(1024, max(4, -(-(2 << 30) // max(1, kv_bytes)))))
+
+
 def main():
     args = parse()
     if args.copy_calibration:
@@ -152,14 +214,20 @@ def main():
     if not os.path.exists(hs2.LIB_PATH):
         import __graft_entry__
         __graft_entry__.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.stream_probe:
+        print(json.dumps(stream_probe(dev)), flush=True)
+        return
+    probe = None if args.no_stream_probe else stream_probe(dev)
+    if probe:
+        log(f"[bench] streaming-read probe: {probe['stream_peak_gbps']} GB/s ({probe['mode']}); {probe['gbps_by_mode']}")
     w = W.WORKLOADS[args.workload]
     t = time.perf_counter()
     inp = W.make_inputs(w, kv=args.kv)
     log(f"[bench] inputs {w.name} ({args.kv} cache) generated in {time.perf_counter() - t:.1f}s lens={inp.lens.tolist()}")
     B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
     Lmax = inp.K.shape[2]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
 
     def to_dev(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
@@ -170,6 +238,10 @@ def main():
     else:
         K, V = to_dev(inp.K), to_dev(inp.V)
         kv_scales = None
+    kv_bytes = K.numel() * K.element_size() + V.numel() * V.element_size()
+    n_copies = kv_copies_for(kv_bytes, args.caches, args.kv_copies)
+    caches = [(K, V)] + [(K.clone(), V.clone()) for _ in range(n_copies - 1)]
+    log(f"[bench] caches: {args.caches}, {n_copies} KV cop{'y' if n_copies == 1 else 'ies'} of {kv_bytes / 1e9:.3f} GB")
     q_fa = to_dev(inp.q_fa)
     q_sa = [to_dev(x) for x in inp.q_sa]
     lens = torch.from_numpy(inp.lens).to(dev)
@@ -184,67 +256,77 @@ def main():
         sinks = [torch.randn(Hq, generator=g).to(dev) for _ in q_sa]
         gates = [torch.randn((B, C, Hq, D), generator=g).to(torch.bfloat16).to(dev) for _ in q_sa]
 
-    def step_on(st):
-        blk.full(q_fa, K, V, lens, out=out, idx=idx, stream=st, kv_scales=kv_scales, block=args.block)
+    def step_on(st, kv):
+        Kc, Vc = kv
+        blk.full(q_fa, Kc, Vc, lens, out=out, idx=idx, stream=st, kv_scales=kv_scales, block=args.block)
         for qs, o, sk, gt in zip(q_sa, sa_out, sinks, gates):
-            blk.sparse(qs, K, V, lens, idx, out=o, stream=st, sink=sk, gate=gt, kv_scales=kv_scales)
+            blk.sparse(qs, Kc, Vc, lens, idx, out=o, stream=st, sink=sk, gate=gt, kv_scales=kv_scales)
 
-    def step():
-        step_on(stream)
+    n_step = [0]
+
+    def step():  # the next copy of the cache in turn
+        step_on(stream, caches[n_step[0] % n_copies])
+        n_step[0] += 1
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} steps done")
     run_step = step
-    if args.graph:  # one step captured after the warmup (the library's set-up is done by then)
-        graph, cap = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    if args.graph:  # one graph per cache copy, captured after the warmup (the library's set-up is done by then)
+        graphs = []
+        cap = torch.cuda.Stream()
         cap.wait_stream(stream)
-        with torch.cuda.graph(graph, stream=cap):
-            step_on(cap)
+        for kv in caches:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=cap):
+                step_on(cap, kv)
+            graphs.append(gr)
         torch.cuda.synchronize()
-        run_step = graph.replay
-    tokens = B * C
-    # evicting by reading 1 GiB (a write would leave dirty lines whose
-    # write-back then overlaps the timed step)
-    flush = torch.ones(1 << 28, dtype=torch.int32, device=dev) if args.cold else None
-    if not args.cold:
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        e0.record(stream)
-        for _ in range(args.steps):
-            run_step()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        ev_ms = e0.elapsed_time(e1)
-        ms_per_step = ev_ms / args.steps
-        value = tokens * args.steps / wall
-        log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms")
 
-    # one event pair per step: percentiles (and, cold, the timing itself: the
-    # cache-evicting write before each step stays outside its events)
+        def run_step():
+            graphs[n_step[0] % n_copies].replay()
+            n_step[0] += 1
+    tokens = B * C
+    # flush: evicting by reading 1 GiB (a write would leave dirty lines whose
+    # write-back then overlaps the timed step); the read is outside the step's events
+    flush = torch.ones(1 << 28, dtype=torch.int32, device=dev) if args.caches == "flush" else None
+    # the timed steps, one event pair around each (mean, percentiles and the
+    # gaps between steps come from the same run)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
     for a_, b_ in ev:
         if flush is not None:
             flush.amax()
         a_.record(stream)
         run_step()
         b_.record(stream)
+    e1.record(stream)
     torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
     per_step = np.array([a_.elapsed_time(b_) for a_, b_ in ev])
-    if args.cold:
+    ev_ms = e0.elapsed_time(e1)
+    if flush is not None:  # steps timed one by one (the flush reads stay outside)
         ms_per_step = float(per_step.mean())
         value = tokens / (ms_per_step * 1e-3)
-        log(f"[bench] timed {args.steps} cold steps: {ms_per_step:.4f} ms mean")
+    else:
+        ms_per_step = ev_ms / args.steps
+        value = tokens * args.steps / wall
+    log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms, "
+        f"sum of per-step events {per_step.sum():.2f} ms")
     pct = {f"p{q}": round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)}
+    pct["mean"] = round(float(per_step.mean()), 4)
+    pct["first"] = round(float(per_step[0]), 4)
 
     # per-kernel durations (HIP events recorded by the library around each launch, same stream)
     hs2.hs2_timing_enable(True)
     hs2.hs2_timing_reset()
     for _ in range(args.steps):
+        if flush is not None:
+            flush.amax()
         step()
     torch.cuda.synchronize()
     per = hs2.hs2_timing_read()
@@ -271,11 +353,18 @@ def main():
     roofline = {"kernel": "fa_split", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": fa_bytes}
+    if probe:
+        roofline["stream_peak"] = probe["stream_peak_gbps"]
+        roofline["frac_of_stream_peak"] = round(achieved / probe["stream_peak_gbps"], 4)
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, inp, args.cpu_seconds)
 
+    cache_desc = {"rotate": f"KV cache rotated over {n_copies} copies ({n_copies * kv_bytes / 1e9:.2f} GB): "
+                            f"no step finds its cache in the memory-side cache or L2",
+                  "flush": "1 GiB read before every step (outside its events)",
+                  "warm": "the same KV cache every step"}[args.caches]
     rec = {"metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
@@ -285,29 +374,39 @@ def main():
                       "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
                       "selection": f"block{args.block}" if args.block else "token",
                       "launch": "graph" if args.graph else "eager",
-                      "caches": "evicted before every step" if args.cold else "as left by the previous step",
+                      "caches": cache_desc,
                       **({"sa_sink_gate": True} if args.sa_sink_gate else {})},
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
            "roofline": roofline,
+           "stream_peak_gbps": probe["stream_peak_gbps"] if probe else None,
+           "stream_probe": probe,
            "step_ms_percentiles": pct,
            "kernels_avg_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
            "cpu_baseline": cpu}
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(w, inp, budget_s: float) -> dict:
-    """The oracle on (sequence, KV head) groups of the same inputs until the
-    budget is spent; scaled to tokens/s of whole steps."""
-    from oracle import hs2_oracle as O
+def cpu_model() -> str:
+    """Host CPU model name (the 'model name' line lscpu reports), or ''."""
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:  # noqa: BLE001
-        threads = 1
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def _oracle_rate(w, inp, budget_s: float):
+    """Run the oracle on (sequence, KV head) groups of the inputs, cycling over
+    the step's groups, until the budget is spent; returns (tokens/s of whole
+    steps, group evaluations, seconds)."""
+    from oracle import hs2_oracle as O
     groups_all = [(b, g) for b in range(w.batch) for g in range(w.n_kv_heads)]
     n, t0 = 0, time.perf_counter()
-    while True:  # cycle over the groups (again if a step's groups take less than the budget)
+    while True:
         O.hybrid_block(inp.q_fa, inp.q_sa, inp.K, inp.V, inp.lens, w.k, w.window,
                        groups=[groups_all[n % len(groups_all)]], k_scale=inp.k_scale, v_scale=inp.v_scale)
         n += 1
@@ -315,11 +414,33 @@ def cpu_baseline(w, inp, budget_s: float) -> dict:
             break
     el = time.perf_counter() - t0
     step_s = el * len(groups_all) / n
-    log(f"[bench] oracle: {n} group evaluations ({len(groups_all)} per step) in {el:.1f}s")
-    return {"value": round(w.batch * w.n_queries / step_s, 4), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{n} (sequence, KV head) group evaluations, cycling over the {len(groups_all)} groups of "
-                      f"one step, full context, {el:.1f}s; scaled by {len(groups_all)}/{n}"}
+    return w.batch * w.n_queries / step_s, n, el
+
+
+def cpu_baseline(w, inp, budget_s: float) -> dict:
+    """The oracle on (sequence, KV head) groups of the same inputs until the
+    budget is spent, scaled to tokens/s of whole steps: once with every BLAS
+    thread the host offers, once pinned to one thread (half the budget each)."""
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        threadpool_limits, threads = None, 1
+    groups = w.batch * w.n_kv_heads
+    v_all, n_all, el_all = _oracle_rate(w, inp, budget_s / 2)
+    log(f"[bench] oracle, {threads} threads: {n_all} group evaluations ({groups} per step) in {el_all:.1f}s")
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            v_one, n_one, el_one = _oracle_rate(w, inp, budget_s / 2)
+    else:
+        v_one, n_one, el_one = v_all, n_all, el_all
+    log(f"[bench] oracle, 1 thread: {n_one} group evaluations in {el_one:.1f}s")
+    return {"value": round(v_all, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_all} (sequence, KV head) group evaluations, cycling over the {groups} groups of one "
+                      f"step, full context, {el_all:.1f}s; scaled by {groups}/{n_all}",
+            "cpu_model": cpu_model(), "cpu_count": os.cpu_count(),
+            "single_thread": {"value": round(v_one, 4), "unit": "tokens/s", "cores": 1,
+                              "sample": f"{n_one} group evaluations, {el_one:.1f}s, BLAS pinned to one thread"}}
 
 
 if __name__ == "__main__":

@@ -102,6 +102,12 @@ typedef struct hs2_dims {
 size_t hs2_workspace_bytes(const hs2_dims* dims, int32_t k, int32_t window);
 
 /* Full-attention layer + token scores + selection (the block's first layer).
+ * Passages: the full-attention layer attends over the whole cache and its
+ * exact attention scores select the tokens (Sec. "The Role of Full
+ * Attention"); the selection is the forced recent window followed by the
+ * highest-scoring tokens outside it, chosen per token (Sec. "Cross-Layer KV
+ * Reuse", paragraphs "Removing the Separate SWA Branch" and "Token-Level
+ * Sparse Selection").
  *
  *   q       [B, C, Hq, D] bf16         FA-layer queries
  *   K, V    cache, layout of hs2_dims  (read over [0, len[b]) per sequence)
@@ -127,6 +133,10 @@ hs2_status hs2_full_attn_score_select(const hs2_dims* dims, const uint16_t* q, c
                                       void* workspace, size_t workspace_bytes, void* stream);
 
 /* Sparse-attention layer reusing the FA layer's cache and selection.
+ * Passage: the sparse layers of a hybrid block reuse the preceding
+ * full-attention layer's KV cache and its selected indices and attend only
+ * over the selected tokens (Sec. "HySparse2 Overview"; Sec. "Cross-Layer KV
+ * Reuse", KV Reuse).
  *
  *   q       [B, C, Hq, D] bf16         this SA layer's own queries
  *   K, V    the same cache the FA layer read
@@ -224,6 +234,20 @@ hs2_status hs2_select_blocks_from_scores(const hs2_dims* dims, const float* scor
 hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, const int32_t* len, int32_t k,
                                   int32_t window, int32_t* idx, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/* Streaming-read probe (diagnostics): reads the `bytes` bytes at device
+ * address `src` once and xors a fold of them into *sink.  Over a buffer much
+ * larger than the 256 MB last-level cache its rate is the device's practical
+ * streaming-read ceiling, which the streaming kernels of this library are
+ * reported against next to the nominal HBM peak.
+ *   mode    0: 16-byte register loads; 1: the same with the non-temporal
+ *           hint; 2: 16-byte direct-to-LDS loads, the loads the
+ *           full-attention and score kernels issue; 3: the same
+ *           non-temporal (other values: HS2_ERR_SHAPE)
+ *   src     16-byte aligned, bytes a multiple of 16 (HS2_ERR_ALIGN), bytes > 0
+ *   sink    device pointer to one uint32 (HS2_ERR_NULL if NULL)
+ * Asynchronous on `stream`; launches one kernel.                              */
+hs2_status hs2_stream_read_probe(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream);
 
 /* Static description of a status code. */
 const char* hs2_status_string(int32_t status);

@@ -29,8 +29,9 @@ constexpr int kNBins = 1024;          // must match the kernels' first-level rad
 constexpr int kSelChunk = hs2::SEL_CHUNK;  // tokens per workgroup of the selection scans
 constexpr size_t kAlign = 256;
 // share of each full-attention token group whose K rows stay cacheable when
-// the score pass re-reads K (percent; the rest streams past the caches)
-constexpr int kFaKeepPercent = 75;
+// the score pass re-reads K (percent; the rest streams past the caches):
+// the last half of each group's part of the split
+constexpr int kFaKeepPercent = 50;
 constexpr int64_t kLastLevelCacheBytes = 256ll << 20;  // MI355X memory-side cache
 
 thread_local std::string g_last_error;
@@ -222,7 +223,10 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   {
     const int64_t kv_bytes = 2 * (int64_t)p.B * p.Hkv * p.Lmax * p.D * (kv8 ? 1 : 2);
     const bool stream = kv_bytes > kLastLevelCacheBytes;
-    const int part = p.fa_split / std::max(1, p.TG);
+    // K rows of a token group are streamed before offset fa_k_stream of the
+    // group's own part of the split (a ring kernel with two token groups
+    // streams two such parts per split)
+    const int part = p.fa_split / std::max(1, fa_ring_token_groups(p.RT, p.fa_variant));
     int keep = kFaKeepPercent;
     const int ek = env_int("HS2_FA_K_KEEP", -1);
     if (ek >= 0 && ek <= 100) keep = ek;
@@ -772,6 +776,18 @@ hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const ui
   if (!k_scale || !v_scale) return fail(HS2_ERR_NULL, "k_scale and v_scale are required for an FP8 cache");
   return sparse_impl(dims, q, K, V, k_scale, v_scale, len, idx, n_slots, sink, gate, out, workspace,
                      workspace_bytes, stream);
+}
+
+hs2_status hs2_stream_read_probe(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream) {
+  if (!src || !sink) return fail(HS2_ERR_NULL, "src and sink are required");
+  if (mode < 0 || mode > 3) return fail(HS2_ERR_SHAPE, "mode must be 0, 1, 2 or 3 (got %d)", mode);
+  if (bytes == 0) return fail(HS2_ERR_SHAPE, "bytes must be > 0");
+  if (!aligned(src, 16) || bytes % 16 || !aligned(sink, 4))
+    return fail(HS2_ERR_ALIGN, "src needs 16-byte alignment and a multiple of 16 bytes, sink 4-byte alignment");
+  hipStream_t s = (hipStream_t)stream;
+  const hipError_t e = launch_stream_probe(src, (int64_t)(bytes / 16), mode, sink, s);
+  if (e != hipSuccess) return fail(HS2_ERR_HIP, "stream probe launch: %s", hipGetErrorString(e));
+  return HS2_OK;
 }
 
 hs2_status hs2_timing_enable(int32_t on) {

@@ -1595,6 +1595,78 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
 }
 
+// ============================================================================ streaming-read probe
+// The device's practical streaming-read rate, the ceiling the streaming
+// kernels are measured against.  grid: any number of 256-thread
+// workgroups; the n16 16-byte words of src are cut into contiguous
+// per-workgroup slices.  MODE 0: register loads (8 in flight per lane), 1:
+// the same non-temporal, 2: 16-byte direct-to-LDS loads of 1 KB per wave as
+// the streaming kernels issue them (up to 8 in flight per wave into an 8 KB
+// ring, each piece read back from LDS once it has landed), 3: the same
+// non-temporal.  Every mode folds each 32-bit word of src exactly once
+// (xor), so *sink ^= the xor of the whole buffer (keeps the loads live and
+// lets a test check that every word was read once).
+template <int MODE>
+__global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ src, int64_t n16, uint32_t* sink) {
+  __shared__ __align__(16) unsigned char ring[4 * 8 * 1024];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t hi = max(lo, min(n16, lo + per));
+  uint32_t acc = 0;
+  int64_t i = lo + tid;  // register-load part: words i, i + 256, ...
+  if constexpr (MODE < 2) {
+    constexpr int U = 8;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4* s4 = (const u32x4*)src;
+    for (; i + (U - 1) * 256 < hi; i += U * 256) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if constexpr (MODE == 1)
+          v[u] = __builtin_nontemporal_load(&s4[i + u * 256]);
+        else
+          v[u] = s4[i + u * 256];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+  } else {
+    // wave w loads 1 KB pieces j = w, w + 4, ... of the slice (64 words
+    // each): its n-th piece into slot n % 8 of its ring
+    const unsigned char* wring = ring + wave * 8 * 1024;
+    const uint32_t wring_a = lds_addr(wring);
+    const int64_t npieces = (hi - lo) / 64;
+    auto fold = [&](int64_t n) {
+      const uint4 v = *(const uint4*)(wring + 1024 * (n & 7) + 16 * lane);
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    };
+    int64_t n = 0;
+    for (int64_t j = wave; j < npieces; j += 4, ++n) {
+      dma16_p<MODE == 3>(src + lo + 64 * j + lane, __builtin_amdgcn_readfirstlane(wring_a + 1024u * (uint32_t)(n & 7)));
+      __builtin_amdgcn_s_waitcnt(vmcnt_enc(7));  // at most 7 outstanding: piece n - 7 has landed
+      if (n >= 7) {
+        fold(n - 7);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): read back before the next load reuses the slot
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));
+    for (int64_t m = n > 7 ? n - 7 : 0; m < n; ++m) fold(m);
+    i = lo + 64 * npieces + tid;  // the slice's words after its whole pieces
+  }
+  for (; i < hi; i += 256) {
+    const uint4 v = src[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  acc ^= __shfl_xor(acc, 1);
+  acc ^= __shfl_xor(acc, 2);
+  acc ^= __shfl_xor(acc, 4);
+  acc ^= __shfl_xor(acc, 8);
+  acc ^= __shfl_xor(acc, 16);
+  acc ^= __shfl_xor(acc, 32);
+  if (lane == 0) atomicXor(sink, acc);
+}
+
 // ============================================================================ host launchers
 #define HS2_LAUNCH(kernel, grid, block, shmem, stream, arg) \
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
@@ -1634,6 +1706,14 @@ int fa_split_align(int RT, int variant) {
   HS2_RING_VARIANTS(HS2_RING_ALIGN)
 #undef HS2_RING_ALIGN
   return 64;
+}
+
+int fa_ring_token_groups(int RT, int variant) {
+#define HS2_RING_TGW(v, rt, nwv, tw, ns, tgw, hd) \
+  if (variant == v && RT == rt) return tgw;
+  HS2_RING_VARIANTS(HS2_RING_TGW)
+#undef HS2_RING_TGW
+  return 1;
 }
 
 int fa_token_groups(int RT, int variant) {
@@ -1923,6 +2003,21 @@ hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s) {
   HS2_SA_SHAPES(HS2_SA_LAUNCH)
 #undef HS2_SA_LAUNCH
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_stream_probe(const void* src, int64_t n16, int mode, uint32_t* sink, hipStream_t s) {
+  // 16 workgroups per compute unit of 256 (more than stay resident: the
+  // dispatcher keeps every CU busy to the end)
+  const dim3 grid(4096), block(256);
+  const uint4* p = (const uint4*)src;
+  switch (mode) {
+    case 0: hipLaunchKernelGGL(k_stream_probe<0>, grid, block, 0, s, p, n16, sink); break;
+    case 1: hipLaunchKernelGGL(k_stream_probe<1>, grid, block, 0, s, p, n16, sink); break;
+    case 2: hipLaunchKernelGGL(k_stream_probe<2>, grid, block, 0, s, p, n16, sink); break;
+    case 3: hipLaunchKernelGGL(k_stream_probe<3>, grid, block, 0, s, p, n16, sink); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace hs2

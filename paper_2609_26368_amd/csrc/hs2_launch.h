@@ -121,6 +121,9 @@ struct SaArgs {
 
 constexpr int kFaVariants = 9;             // full-attention kernel shapes (see HS2_RING_VARIANTS)
 int fa_token_groups(int RT, int variant);  // partial slots per token split
+// token groups that stream contiguous parts of one split through their own
+// rings (ring kernels; merged in LDS into one partial), 1 otherwise
+int fa_ring_token_groups(int RT, int variant);
 int fa_split_align(int RT, int variant);   // split lengths are multiples of this many tokens
 // head dim served by full-attention kernel (RT, variant) for the cache format, 0 if there is none
 int fa_variant_head_dim(int RT, int variant, bool kv8);
@@ -139,5 +142,9 @@ hipError_t launch_sel_hist(const SelArgs& a, int nchunks, hipStream_t s);
 hipError_t launch_select(const SelArgs& a, hipStream_t s);
 hipError_t launch_block_select(const BlockSelArgs& a, hipStream_t s);  // block sums + selection
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s);
+// streaming-read probe over n16 16-byte words (mode: 0 register loads, 1
+// non-temporal register loads, 2 direct-to-LDS loads, 3 non-temporal
+// direct-to-LDS loads); xors a fold of the data into *sink
+hipError_t launch_stream_probe(const void* src, int64_t n16, int mode, uint32_t* sink, hipStream_t s);
 
 }  // namespace hs2

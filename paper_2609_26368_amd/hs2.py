@@ -29,7 +29,8 @@ HS2_ERR_HIP = -6
 EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_sparse_attn_ex",
             "hs2_full_attn_score_select_fp8", "hs2_sparse_attn_fp8", "hs2_full_attn_score_select_blocks",
             "hs2_select_from_scores", "hs2_select_blocks_from_scores",
-            "hs2_status_string", "hs2_last_error", "hs2_timing_enable", "hs2_timing_reset", "hs2_timing_read"]
+            "hs2_stream_read_probe", "hs2_status_string", "hs2_last_error", "hs2_timing_enable",
+            "hs2_timing_reset", "hs2_timing_read"]
 
 
 class hs2_dims(ctypes.Structure):
@@ -76,6 +77,8 @@ def load() -> ctypes.CDLL:
     lib.hs2_select_blocks_from_scores.restype = I32
     lib.hs2_select_from_scores.argtypes = [D, P, P, I32, I32, P, P, SZ, P]
     lib.hs2_select_from_scores.restype = I32
+    lib.hs2_stream_read_probe.argtypes = [P, SZ, I32, P, P]
+    lib.hs2_stream_read_probe.restype = I32
     lib.hs2_status_string.argtypes = [I32]
     lib.hs2_status_string.restype = ctypes.c_char_p
     lib.hs2_last_error.argtypes = []
@@ -307,6 +310,17 @@ def hs2_select_from_scores(dims, scores, len, k, window, idx, workspace, stream=
     _check(load().hs2_select_from_scores(ctypes.byref(dims), _ptr(scores), _ptr(len), int(k), int(window), _ptr(idx),
                                          _ptr(workspace), workspace.numel() * workspace.element_size(),
                                          _stream(stream)))
+
+
+def hs2_stream_read_probe(src, mode, sink, stream=None):
+    """Streaming read of the whole of tensor src (device, contiguous) in the
+    given load mode; xors a fold of it into sink (one int32/uint32 element)."""
+    if not src.is_contiguous():
+        raise ValueError("src must be contiguous")
+    if sink.numel() < 1 or sink.element_size() != 4 or sink.device != src.device:
+        raise ValueError("sink: one 4-byte element on the device of src")
+    _check(load().hs2_stream_read_probe(_ptr(src), src.numel() * src.element_size(), int(mode), _ptr(sink),
+                                        _stream(stream)))
 
 
 def hs2_status_string(status: int) -> str:

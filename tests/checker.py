@@ -8,8 +8,14 @@
 * index rows: the valid prefix must be strictly ascending, followed by -1, and
   the counts equal; the sets may differ only by swaps of candidates whose
   oracle float32 scores differ by less than 1e-6 relative.
-* pooled scores: |gpu - ref| <= SCORE_RTOL * ref + SCORE_ATOL (see the design doc
-  for the derivation of the bound).
+* pooled scores: |gpu - ref| <= SCORE_RTOL * ref + SCORE_ATOL (the bound
+  covers fp32 logits from exact bf16 products, one rounding each for the
+  scaled logit, the row factor and a G-term fp32 sum).
+* index rows without an oracle (check_idx_structure): for query position pos
+  the row holds min(pos + 1, k + window) tokens, strictly ascending, all in
+  [0, pos], the whole window [max(0, pos - window + 1), pos] among them and
+  -1 after them; this needs no scores, so it runs on every row of a
+  full-size result.
 """
 from __future__ import annotations
 
@@ -67,6 +73,38 @@ def check_idx_row(gpu_row, ref_row, ref_scores, window_lo: int) -> int:
     gap = np.abs(pr[:, None] - pg[None, :]) / np.maximum(np.maximum(pr[:, None], pg[None, :]), 1e-300)
     assert gap.max() < TIE_RTOL, f"swap of tokens whose oracle scores differ by {gap.max():.3g} relative"
     return len(only_g)
+
+
+def check_idx_structure(gpu_idx, lens, C: int, k: int, window: int) -> dict:
+    """Oracle-free checks of every selection row of gpu_idx [B, Hkv, C, S]
+    (S = k + window): count, order, range, window membership, padding.
+    A query at a negative position (len < C) must have an all -1 row."""
+    gpu_idx = np.asarray(gpu_idx)
+    B, Hkv, Cq, S = gpu_idx.shape
+    assert Cq == C and S == k + window, f"idx shape {gpu_idx.shape} for C={C}, k + window={k + window}"
+    rows = 0
+    for b in range(B):
+        L = int(lens[b])
+        for c in range(C):
+            pos = L - C + c
+            want = 0 if pos < 0 else min(pos + 1, k + window)
+            wlo = max(0, pos - window + 1)
+            for g in range(Hkv):
+                r = gpu_idx[b, g, c].astype(np.int64)
+                n = int((r >= 0).sum())
+                where = f"(b={b}, g={g}, c={c}, pos={pos})"
+                assert n == want, f"row {where}: {n} tokens, expected min(pos + 1, k + window) = {want}"
+                assert (r[n:] == -1).all(), f"row {where}: -1 padding not contiguous or other negative values"
+                v = r[:n]
+                if n == 0:
+                    continue
+                assert (np.diff(v) > 0).all(), f"row {where}: not strictly ascending"
+                assert v[0] >= 0 and v[-1] <= pos, f"row {where}: index outside [0, pos]"
+                nwin = pos - wlo + 1
+                assert n >= nwin and np.array_equal(v[n - nwin:], np.arange(wlo, pos + 1)), \
+                    f"row {where}: window [{wlo}, {pos}] not all selected"
+                rows += 1
+    return {"rows_checked": rows}
 
 
 def check_idx(gpu_idx, ref_idx, ref_P, lens, C: int, window: int, groups=None) -> dict:

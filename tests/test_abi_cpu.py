@@ -240,3 +240,14 @@ def test_binding_checks_shapes_before_calling():
     idx = torch.zeros((1, 4, 1, 8), dtype=torch.int32)
     with pytest.raises(ValueError):
         hs2.hs2_full_attn_score_select(d, q, K_short, K_short, lens, 4, 4, out, idx, workspace=torch.zeros(16))
+
+
+def test_stream_probe_rejects_before_launch(lib):
+    vp = ctypes.c_void_p
+    assert lib.hs2_stream_read_probe(None, 1024, 0, vp(FAKE), None) == hs2.HS2_ERR_NULL
+    assert lib.hs2_stream_read_probe(vp(FAKE), 1024, 0, None, None) == hs2.HS2_ERR_NULL
+    assert lib.hs2_stream_read_probe(vp(FAKE), 1024, 4, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    assert lib.hs2_stream_read_probe(vp(FAKE), 1024, -1, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    assert lib.hs2_stream_read_probe(vp(FAKE), 0, 0, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    assert lib.hs2_stream_read_probe(vp(FAKE + 8), 1024, 0, vp(FAKE), None) == hs2.HS2_ERR_ALIGN
+    assert lib.hs2_stream_read_probe(vp(FAKE), 1000, 0, vp(FAKE), None) == hs2.HS2_ERR_ALIGN

@@ -75,7 +75,28 @@ def test_traffic_summary_calibrates_by_the_copy(tmp_path, monkeypatch):
 def test_cpu_baseline_fields():
     w = W.Workload("tiny", 1, 300, 2, 8, 2, 128, 32, 16, 1)
     inp = W.make_inputs(w, seed=3)
-    r = bench.cpu_baseline(w, inp, 0.2)
-    assert set(r) == {"value", "unit", "cores", "kind", "sample"}
+    r = bench.cpu_baseline(w, inp, 0.4)
+    assert set(r) == {"value", "unit", "cores", "kind", "sample", "cpu_model", "cpu_count", "single_thread"}
     assert r["kind"] == "oracle" and r["unit"] == "tokens/s"
     assert r["value"] > 0 and r["cores"] >= 1
+    assert r["cpu_count"] == os.cpu_count()
+    assert isinstance(r["cpu_model"], str)
+    one = r["single_thread"]
+    assert one["cores"] == 1 and one["unit"] == "tokens/s" and one["value"] > 0
+
+
+def test_cpu_model_is_the_lscpu_model_name():
+    m = bench.cpu_model()
+    if os.path.exists("/proc/cpuinfo") and "model name" in open("/proc/cpuinfo").read():
+        assert m and "\n" not in m
+
+
+def test_kv_copies_rotation_rule():
+    gib = 1 << 30
+    assert bench.kv_copies_for(int(1.07e9), "rotate", 0) == 4          # 4 copies of the 128K chunk cache
+    assert bench.kv_copies_for(4 * 1024 * 1024, "rotate", 0) == 512    # small caches: at least 2 GiB in all
+    assert bench.kv_copies_for(1024, "rotate", 0) == 1024              # capped
+    assert bench.kv_copies_for(4 * gib, "rotate", 0) == 4
+    assert bench.kv_copies_for(int(1.07e9), "warm", 0) == 1
+    assert bench.kv_copies_for(int(1.07e9), "flush", 0) == 1
+    assert bench.kv_copies_for(int(1.07e9), "rotate", 7) == 7

@@ -77,6 +77,23 @@ def run_gpu(inp, oracle_idx=None):
     return res
 
 
+def _v_absmax(inp) -> np.ndarray:
+    """max_t |V[b, g, t, d]| over each sequence's tokens, [B, Hkv, D] float64."""
+    w = inp.w
+    out = np.zeros((w.batch, w.n_kv_heads, w.head_dim))
+    for b in range(w.batch):
+        for g in range(w.n_kv_heads):
+            L = int(inp.lens[b])
+            if L > 0:
+                out[b, g] = np.abs(O.cache_rows(inp.V, b, g, slice(0, L), inp.v_scale)).max(axis=0)
+    return out
+
+
+def _check_out_hull(inp, vmax, out, what):
+    assert np.isfinite(out).all(), f"{what}: non-finite output"
+    assert (np.abs(out) <= vmax * (1 + 2 ** -8) + 1e-30).all(), f"{what}: output outside the hull of its V rows"
+
+
 def compare(inp, ref, gpu, groups=None):
     w = inp.w
     G = w.group
@@ -85,6 +102,14 @@ def compare(inp, ref, gpu, groups=None):
         rows = np.zeros((w.batch, w.n_queries, w.n_q_heads), dtype=bool)
         for b, g in groups:
             rows[b, :, g * G:(g + 1) * G] = True
+    # every row, sampled or not: oracle-free structure of the selection, and
+    # outputs finite and inside the hull of their value rows (an attention
+    # output is a convex combination of V rows: |out[d]| <= max_t |V[t, d]|)
+    r_struct = CK.check_idx_structure(gpu["idx"], inp.lens, w.n_queries, w.k, w.window)
+    vmax = np.repeat(_v_absmax(inp), w.group, axis=1)[:, None]  # [B, 1, Hq, D]
+    _check_out_hull(inp, vmax, gpu["out"], "full-attention out")
+    for li in range(len(inp.q_sa)):
+        _check_out_hull(inp, vmax, gpu["sa"][li], f"sparse layer {li}")
     r_out = CK.check_out(gpu["out"], ref["out"], "full-attention out", rows)
     # stats: M natural-log units, Z
     M, Z = gpu["stats"][..., 0], gpu["stats"][..., 1]
@@ -101,7 +126,7 @@ def compare(inp, ref, gpu, groups=None):
         CK.check_out(gpu["sa_ref_idx"][li], ref_sa, f"sparse layer {li} (oracle selection)", rows)
         if r_idx["swaps"] == 0:
             CK.check_out(gpu["sa"][li], ref_sa, f"sparse layer {li} (own selection)", rows)
-    return {**r_out, **r_sc, **r_idx}
+    return {**r_out, **r_sc, **r_idx, **r_struct}
 
 
 def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None, kv="bf16"):

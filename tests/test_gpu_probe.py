@@ -1,0 +1,25 @@
+"""GPU: the streaming-read probe reads every 32-bit word of its buffer exactly
+once in each load mode (its xor fold equals the host's), including a buffer
+whose size leaves partial pieces and empty workgroup slices."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("words16", [1 << 20, (1 << 20) + 3, 4096 * 64 + 17, 5])
+@pytest.mark.parametrize("mode", [0, 1, 2, 3])
+def test_stream_probe_reads_every_word_once(words16, mode):
+    from paper_2609_26368_amd import hs2
+    rng = np.random.default_rng(words16 + mode)
+    host = rng.integers(0, 2 ** 32, size=4 * words16, dtype=np.uint32)
+    buf = torch.from_numpy(host.view(np.int32)).cuda()
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    print(f"[probe] mode={mode} words16={words16}", flush=True)
+    hs2.hs2_stream_read_probe(buf, mode, sink)
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(host)
+    assert int(sink.cpu().numpy().view(np.uint32)[0]) == int(want)
