@@ -196,6 +196,23 @@ hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const ui
                                int32_t n_slots, const float* sink, const uint16_t* gate, uint16_t* out,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* hs2_sparse_attn without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the layer's scratch (its split
+ * partials) is a static device array of 16 MiB inside the library, one per
+ * GPU, held until the process ends.  The call itself allocates nothing.
+ *   - arguments, outputs and results as for hs2_sparse_attn (same kernels,
+ *     same splits: the output is bit-identical to hs2_sparse_attn's);
+ *   - a layer needing more than 16 MiB of scratch (rows B * Hkv * C times
+ *     its splits times the head rows) is rejected with HS2_ERR_WORKSPACE
+ *     before anything is launched; the benchmark shapes need 6-10 MiB;
+ *   - every call on one GPU uses that GPU's one array: calls that overlap on
+ *     one GPU (other streams, other host threads) race and must be ordered
+ *     by the caller; nothing in the array needs clearing between calls.   */
+hs2_status hs2_sparse_attn_noalloc(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                   const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out,
+                                   void* stream);
+
 /* Block-level selection: the granularity of the predecessor HySparse, which
  * the paper compares against (Sec. "Ablation 1: Token-Level versus
  * Block-Level Sparsity": blocks of 64 tokens, the same global budget and the

@@ -132,7 +132,16 @@ struct DeviceInfo {
   int cus = 256;
   int fa_wgs[2][4][kFaVariants] = {};  // [E4M3 cache][log2 RT][variant]; 0 = unknown
   int pool_wgs[2][2][4][7][17] = {};   // k_pool: [head dim 256][E4M3 cache][log2 RT][log2 Gp][C]; 0 = unknown
+  void* scratch = nullptr;             // this device's address of `scratch` (hs2_sparse_attn_noalloc)
 };
+
+// Scratch of the allocation-free sparse layer (hs2_sparse_attn_noalloc): its
+// split partials.  Every GPU the library runs on holds its own copy of this
+// array, at its own address, until the process ends; host code never uses
+// the array's name as a device address (it is a host-side stand-in), only
+// the address hipGetSymbolAddress gives for the current device.
+constexpr size_t kStaticScratchBytes = 16u << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 int ilog2(int v) {
   int l = 0;
@@ -309,8 +318,9 @@ std::mutex g_init_mu;
 bool g_dev_done[64] = {};
 DeviceInfo g_dev[64];
 
-// Per-device set-up (once): LDS limits of the kernels that need more than
-// 64 KB, and the occupancy figures the planner uses.
+// Per-device set-up (once, with that device current): LDS limits of the
+// kernels that need more than 64 KB, the occupancy figures the planner
+// uses, and this device's address of the static scratch array.
 hs2_status ensure_device_init(const DeviceInfo** info) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(HS2_ERR_HIP, "hipGetDevice failed");
@@ -334,6 +344,8 @@ hs2_status ensure_device_init(const DeviceInfo** info) {
                   hipSuccess)
                 return fail(HS2_ERR_HIP, "occupancy query: %s", hipGetErrorString(e));
       }
+    if ((e = hipGetSymbolAddress(&di.scratch, HIP_SYMBOL(scratch))) != hipSuccess || !di.scratch)
+      return fail(HS2_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
     g_dev[dev] = di;
     g_dev_done[dev] = true;
   }
@@ -767,6 +779,27 @@ hs2_status hs2_sparse_attn_ex(const hs2_dims* dims, const uint16_t* q, const uin
                               void* stream) {
   return sparse_impl(dims, q, K, V, nullptr, nullptr, len, idx, n_slots, sink, gate, out, workspace,
                      workspace_bytes, stream);
+}
+
+hs2_status hs2_sparse_attn_noalloc(const hs2_dims* dims, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                                   const int32_t* len, const int32_t* idx, int32_t n_slots, uint16_t* out,
+                                   void* stream) {
+  hs2_status st = check_dims(dims);
+  if (st != HS2_OK) return st;
+  if (n_slots < 1 || n_slots > kMaxLen) return fail(HS2_ERR_SHAPE, "n_slots must be in [1, 2^27]");
+  // the scratch this call needs, checked against the static array before
+  // anything touches the device (the sparse plan needs no device figures)
+  Plan p;
+  make_plan(dims, 0, n_slots, p, nullptr, false);
+  SaPlan sp;
+  make_sa_plan(p, n_slots, sp);
+  if (sp.bytes > kStaticScratchBytes)
+    return fail(HS2_ERR_WORKSPACE, "sparse layer needs %zu bytes of scratch; the static scratch holds %zu",
+                sp.bytes, kStaticScratchBytes);
+  const DeviceInfo* di = nullptr;
+  if ((st = ensure_device_init(&di)) != HS2_OK) return st;
+  return sparse_impl(dims, q, K, V, nullptr, nullptr, len, idx, n_slots, nullptr, nullptr, out, di->scratch,
+                     kStaticScratchBytes, stream);
 }
 
 hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const uint8_t* K, const uint8_t* V,

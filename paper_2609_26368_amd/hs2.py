@@ -29,7 +29,7 @@ HS2_ERR_HIP = -6
 EXPORTED = ["hs2_workspace_bytes", "hs2_full_attn_score_select", "hs2_sparse_attn", "hs2_sparse_attn_ex",
             "hs2_full_attn_score_select_fp8", "hs2_sparse_attn_fp8", "hs2_full_attn_score_select_blocks",
             "hs2_select_from_scores", "hs2_select_blocks_from_scores",
-            "hs2_stream_read_probe", "hs2_status_string", "hs2_last_error", "hs2_timing_enable",
+            "hs2_sparse_attn_noalloc", "hs2_stream_read_probe", "hs2_status_string", "hs2_last_error", "hs2_timing_enable",
             "hs2_timing_reset", "hs2_timing_read"]
 
 
@@ -77,6 +77,8 @@ def load() -> ctypes.CDLL:
     lib.hs2_select_blocks_from_scores.restype = I32
     lib.hs2_select_from_scores.argtypes = [D, P, P, I32, I32, P, P, SZ, P]
     lib.hs2_select_from_scores.restype = I32
+    lib.hs2_sparse_attn_noalloc.argtypes = [D, P, P, P, P, P, I32, P, P]
+    lib.hs2_sparse_attn_noalloc.restype = I32
     lib.hs2_stream_read_probe.argtypes = [P, SZ, I32, P, P]
     lib.hs2_stream_read_probe.restype = I32
     lib.hs2_status_string.argtypes = [I32]
@@ -192,6 +194,20 @@ def hs2_sparse_attn(dims, q, K, V, len, idx, n_slots, out, workspace, stream=Non
     _check(load().hs2_sparse_attn(ctypes.byref(dims), _ptr(q), _ptr(K), _ptr(V), _ptr(len), _ptr(idx), int(n_slots),
                                   _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
+
+
+def hs2_sparse_attn_noalloc(dims, q, K, V, len, idx, n_slots, out, stream=None):
+    """hs2_sparse_attn with the library's static per-GPU scratch instead of a
+    workspace (no allocation in the call; calls on one GPU must not overlap)."""
+    dev = q.device
+    B, C, Hq, Hkv, D = dims.batch, dims.n_queries, dims.n_q_heads, dims.n_kv_heads, dims.head_dim
+    _expect(q, "q", (B, C, Hq, D), _BF16, dev)
+    _check_kv(dims, K, V, dev)
+    _expect(len, "len", (B,), (torch.int32,), dev)
+    _expect(idx, "idx", (B, Hkv, C, n_slots), (torch.int32,), dev)
+    _expect(out, "out", (B, C, Hq, D), _BF16, dev)
+    _check(load().hs2_sparse_attn_noalloc(ctypes.byref(dims), _ptr(q), _ptr(K), _ptr(V), _ptr(len), _ptr(idx),
+                                          int(n_slots), _ptr(out), _stream(stream)))
 
 
 def hs2_sparse_attn_ex(dims, q, K, V, len, idx, n_slots, sink, gate, out, workspace, stream=None):

@@ -251,3 +251,17 @@ def test_stream_probe_rejects_before_launch(lib):
     assert lib.hs2_stream_read_probe(vp(FAKE), 0, 0, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
     assert lib.hs2_stream_read_probe(vp(FAKE + 8), 1024, 0, vp(FAKE), None) == hs2.HS2_ERR_ALIGN
     assert lib.hs2_stream_read_probe(vp(FAKE), 1000, 0, vp(FAKE), None) == hs2.HS2_ERR_ALIGN
+
+
+def test_noalloc_sparse_rejects_before_launch(lib):
+    vp = ctypes.c_void_p
+    d = dims()
+    st = lib.hs2_sparse_attn_noalloc(ctypes.byref(d), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), 0, vp(FAKE),
+                                     None)
+    assert st == hs2.HS2_ERR_SHAPE
+    # more scratch than the static array holds: 8192 selection rows of 8192 slots
+    big = dims(batch=64, n_queries=16, n_q_heads=64, n_kv_heads=8)
+    st = lib.hs2_sparse_attn_noalloc(ctypes.byref(big), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), vp(FAKE), 8192,
+                                     vp(FAKE), None)
+    assert st == hs2.HS2_ERR_WORKSPACE
+    assert "static scratch" in hs2.hs2_last_error()
