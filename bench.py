@@ -162,7 +162,7 @@ def stream_probe(dev, reps: int = 8) -> dict:
     from paper_2609_26368_amd import hs2
     buf = torch.empty(STREAM_PROBE_BYTES // 4, dtype=torch.int32, device=dev)
     buf.random_()
-    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    sink = torch.zeros(hs2.STREAM_PROBE_SINK_WORDS, dtype=torch.int32, device=dev)
     st = torch.cuda.current_stream()
     rates = {}
     for mode in STREAM_PROBE_MODES:
@@ -317,6 +317,12 @@ def main():
         value = tokens * args.steps / wall
     log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms, "
         f"sum of per-step events {per_step.sum():.2f} ms")
+    if n_copies > 1:  # step i of the timed run used copy (warmup + i) % n_copies
+        by_copy = {}
+        for i, ms in enumerate(per_step):
+            by_copy.setdefault((args.warmup + i) % n_copies, []).append(ms)
+        log("[bench] mean step ms by cache copy: " +
+            " ".join(f"{c}:{np.mean(v):.4f}" for c, v in sorted(by_copy.items())[:8]))
     pct = {f"p{q}": round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)}
     pct["mean"] = round(float(per_step.mean()), 4)
     pct["first"] = round(float(per_step[0]), 4)

@@ -262,8 +262,13 @@ hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, con
  *           full-attention and score kernels issue; 3: the same
  *           non-temporal (other values: HS2_ERR_SHAPE)
  *   src     16-byte aligned, bytes a multiple of 16 (HS2_ERR_ALIGN), bytes > 0
- *   sink    device pointer to one uint32 (HS2_ERR_NULL if NULL)
- * Asynchronous on `stream`; launches one kernel.                              */
+ *   sink    device array of HS2_STREAM_PROBE_SINK_WORDS uint32, 4-byte
+ *           aligned (HS2_ERR_NULL if NULL); overwritten
+ * Asynchronous on `stream`; launches one kernel of HS2_STREAM_PROBE_SINK_WORDS
+ * workgroups, each of which stores the xor of the 32-bit words of its slice
+ * to its own word of sink (the xor of all sink words is the xor of the
+ * buffer).                                                                    */
+#define HS2_STREAM_PROBE_SINK_WORDS 4096
 hs2_status hs2_stream_read_probe(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream);
 
 /* Static description of a status code. */

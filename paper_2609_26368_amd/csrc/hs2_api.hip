@@ -66,9 +66,9 @@ struct Plan {
   float c2;
   int RT, TG;                 // full-attention / pooling row tiles
   int fa_variant;             // ring kernel shape (0, 2, 3, 4) for RT <= 4; 1: workgroup kernel
-  int fa_split, fa_nsplit;
+  FaSplitPlan fa_sp;          // full-attention token splits (grid: fa_sp.n_items items)
   int fa_cache_policy;  // FaCachePolicy of the full-attention ring kernel
-  int fa_k_stream;      // FA_STREAM_K_HEAD: leading K rows of each token group read non-temporal
+  int fa_k_keep;        // FA_STREAM_K_HEAD: percent of each token group's K rows kept cacheable
   int logit_chunk;
   int pool_split, pool_nsplit;
   int64_t units;              // B * Hkv
@@ -191,19 +191,28 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   p.TG = fa_token_groups(p.RT, p.fa_variant);
   p.units = (int64_t)p.B * p.Hkv;
   p.rows = p.units * p.C;
-  // token splits: as many workgroups as stay resident at once on the device
-  // (one round, no tail), each a whole number of 64-token tiles and at least
-  // 256 tokens (a split's partial costs 16 RT rows of D + 4 floats)
+  // token splits: one item (sequence, KV head, split) per workgroup of a
+  // grid of as many workgroups as stay resident at once on the device (one
+  // round, no tail); the kernels derive the split length from the lengths
+  // on the device (the shortest whose items fill the grid: ragged lengths
+  // balance), a whole number of the kernel's token groups of 64-token tiles
+  // and at least 256 tokens (a split's partial costs 16 RT rows of D + 4
+  // floats).  HS2_FA_SPLIT fixes the length instead (grid: every split of
+  // the capacity).
   const int lrt = p.RT >= 8 ? 3 : p.RT >= 4 ? 2 : p.RT >= 2 ? 1 : 0;
   const int wgs_cu = di && di->fa_wgs[kv8][lrt][p.fa_variant] > 0 ? di->fa_wgs[kv8][lrt][p.fa_variant] : 4;
   const int64_t slots = (int64_t)(di ? di->cus : 256) * wgs_cu * std::max(1, env_int("HS2_FA_ROUNDS", 1));
-  const int64_t per_unit = std::max<int64_t>(1, slots / p.units);
   const int align = fa_split_align(p.RT, p.fa_variant);
-  int split = (int)std::max<int64_t>(256, round_up(cdiv(p.Lmax, per_unit), align));
-  split = env_int("HS2_FA_SPLIT", split);
-  split = (int)std::max<int64_t>(align, round_up(std::min<int64_t>(split, p.Lmax), align));
-  p.fa_split = split;
-  p.fa_nsplit = (int)cdiv(p.Lmax, split);
+  p.fa_sp.align = align;
+  p.fa_sp.min_split = (int)round_up(256, align);
+  const int fixed = env_int("HS2_FA_SPLIT", 0);
+  if (fixed > 0) {
+    p.fa_sp.fixed = (int)std::max<int64_t>(align, round_up(std::min<int64_t>(fixed, p.Lmax), align));
+    p.fa_sp.n_items = (int)(p.units * cdiv(p.Lmax, p.fa_sp.fixed));
+  } else {
+    p.fa_sp.fixed = 0;
+    p.fa_sp.n_items = (int)std::max<int64_t>(slots, p.units);
+  }
   // score pass over K: the same one-round rule for its own kernel; at most
   // 32768 tokens per split (16-bit histogram counters in LDS)
   const int pool_cu = di && p.C <= 16 ? di->pool_wgs[p.D == 256][kv8][lrt][ilog2(p.Gp)][p.C] : 0;
@@ -232,17 +241,16 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
   {
     const int64_t kv_bytes = 2 * (int64_t)p.B * p.Hkv * p.Lmax * p.D * (kv8 ? 1 : 2);
     const bool stream = kv_bytes > kLastLevelCacheBytes;
-    // K rows of a token group are streamed before offset fa_k_stream of the
-    // group's own part of the split (a ring kernel with two token groups
-    // streams two such parts per split)
-    const int part = p.fa_split / std::max(1, fa_ring_token_groups(p.RT, p.fa_variant));
+    // the kernel keeps the last `keep` percent of each token group's part of
+    // its split cacheable (a ring kernel with two token groups streams two
+    // such parts per split) and streams the K rows before them
     int keep = kFaKeepPercent;
     const int ek = env_int("HS2_FA_K_KEEP", -1);
     if (ek >= 0 && ek <= 100) keep = ek;
     p.fa_cache_policy = !stream ? FA_CACHE_DEFAULT
                         : p.RT == 1 ? (p.pool_logits ? FA_STREAM_KV : FA_STREAM_V)
                                     : FA_STREAM_K_HEAD;
-    p.fa_k_stream = part - (int)((int64_t)part * keep / 100);
+    p.fa_k_keep = keep;
     const int ep = env_int("HS2_FA_CACHE_POLICY", -1);
     if (ep >= 0 && fa_cache_policy_built(p.RT, ep)) p.fa_cache_policy = ep;
   }
@@ -252,10 +260,10 @@ void make_plan(const hs2_dims* d, int32_t k, int32_t window, Plan& p, const Devi
       4096, std::max<int64_t>(1024, round_up(cdiv(p.Lmax * p.units, 2 * (int64_t)(di ? di->cus : 256)), 1024)));
 
   const int64_t prow = 16 * p.RT;
-  const int64_t nslot = (int64_t)p.fa_nsplit * p.TG;
+  const int64_t nslot = (int64_t)p.fa_sp.n_items * p.TG;  // partial slots of the full-attention pass
   size_t cur = 0;
-  p.off_part_o = carve(cur, sizeof(float) * p.units * nslot * prow * p.D);
-  p.off_part_ml = carve(cur, sizeof(float) * p.units * nslot * prow * 4);
+  p.off_part_o = carve(cur, sizeof(float) * nslot * prow * p.D);
+  p.off_part_ml = carve(cur, sizeof(float) * nslot * prow * 4);
   p.off_stats = carve(cur, sizeof(float) * (size_t)p.B * p.C * p.Hq * 2);
   p.off_scores = carve(cur, sizeof(float) * p.rows * p.score_stride);
   p.off_hist = carve(cur, sizeof(uint32_t) * p.rows * kNBins);
@@ -532,12 +540,11 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   fa.G = p.G;
   fa.Gp = p.Gp;
   fa.max_len = p.Lmax;
-  fa.split_tokens = p.fa_split;
-  fa.n_split = p.fa_nsplit;
+  fa.sp = p.fa_sp;
   fa.logits = p.pool_logits ? (float*)(ws + p.off_logits) : nullptr;
   fa.logit_stride = p.logit_stride;
   fa.cache_policy = p.fa_cache_policy;
-  fa.k_stream_tokens = p.fa_k_stream;
+  fa.k_keep_pct = p.fa_k_keep;
   HS2_TRY_LAUNCH(KK_FA, s, launch_fa_split(fa, p.RT, p.fa_variant, s));
 
   CombineArgs ca{};
@@ -555,9 +562,9 @@ hs2_status full_attn_impl(const hs2_dims* dims, const uint16_t* q, const void* K
   ca.Gp = p.Gp;
   ca.max_len = p.Lmax;
   ca.rows = 16 * p.RT;
-  ca.nslot = p.fa_nsplit * p.TG;
+  ca.nslot = 0;  // per (sequence, KV head): derived in the kernel from the splits
   ca.tg = p.TG;
-  ca.split_tokens = p.fa_split;
+  ca.sp = p.fa_sp;
   ca.sa_mode = 0;
   // the histogram and the per-row counters (contiguous) start at zero
   ca.v_scale = v_scale;
@@ -759,7 +766,6 @@ hs2_status sparse_impl(const hs2_dims* dims, const uint16_t* q, const void* K, c
   ca.rows = 16 * sp.RT;
   ca.nslot = sp.nsplit * sp.TG;
   ca.tg = sp.TG;
-  ca.split_tokens = 0;
   ca.sa_mode = 1;
   ca.sink = sink;
   ca.gate = gate;
@@ -817,6 +823,7 @@ hs2_status hs2_stream_read_probe(const void* src, size_t bytes, int32_t mode, ui
   if (bytes == 0) return fail(HS2_ERR_SHAPE, "bytes must be > 0");
   if (!aligned(src, 16) || bytes % 16 || !aligned(sink, 4))
     return fail(HS2_ERR_ALIGN, "src needs 16-byte alignment and a multiple of 16 bytes, sink 4-byte alignment");
+  static_assert(HS2_STREAM_PROBE_SINK_WORDS == STREAM_PROBE_WORKGROUPS, "one sink word per probe workgroup");
   hipStream_t s = (hipStream_t)stream;
   const hipError_t e = launch_stream_probe(src, (int64_t)(bytes / 16), mode, sink, s);
   if (e != hipSuccess) return fail(HS2_ERR_HIP, "stream probe launch: %s", hipGetErrorString(e));

@@ -4,8 +4,9 @@
 // register staging), row-major, 16-byte chunks swizzled by the row index so
 // that the MFMA K-operand reads and the transposing V reads
 // (ds_read_b64_tr_b16) are free of bank conflicts without padding; E4M3
-// rows are staged raw (swizzled too) and converted in registers (K) or into
-// a bf16 tile of the same layout (V; K as well when several waves share it).
+// rows are staged raw (swizzled too); K is converted in registers (or into
+// a bf16 tile of the same layout when several waves share it), V is read
+// raw by an 8-bit transposing read and converted in registers.
 //
 // MFMA lane layouts used (checked on gfx950):
 //   16x16x32 bf16: lane l supplies A[l%16][8(l/16)+j] and B[8(l/16)+j][l%16],
@@ -67,9 +68,15 @@ __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ inline uint32_t score_key(float p) {
   return p < 1.17549435e-38f ? 0u : __float_as_uint(p);
 }
-__device__ inline int score_digit(uint32_t key) {
-  int d = (int)(key >> DIGIT_SHIFT) - DIGIT_BASE;
-  return d < 0 ? 0 : (d >= NBINS ? NBINS - 1 : d);
+// First-level radix digit (histogram bin) of a score: its key's top bits
+// clamped to the NBINS bins.  Taken straight from the float bits with one
+// clamp: a value below FLT_MIN (or negative) lands in bin 0 like its key
+// +0, so this equals the digit of score_key(p) for every input but NaNs
+// with the sign bit set (bin 0 here; no score is NaN).  Every histogram and
+// filter derives its bins with this one function.
+__device__ inline int score_digit(float p) {
+  const int x = __float_as_int(p) >> DIGIT_SHIFT;  // arithmetic shift: negative values stay negative
+  return min(max(x, DIGIT_BASE), DIGIT_BASE + NBINS - 1) - DIGIT_BASE;
 }
 
 // ---------------------------------------------------------------- wave-level attention state
@@ -362,12 +369,17 @@ constexpr int vmcnt_enc(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
 // Four E4M3 values (the bytes of w, low first) -> four bf16 in two packed
 // words, exactly (every E4M3 value is a bf16 value): gfx950's scaled
-// conversion with scale 1, bytes 0-1 and (op_sel) bytes 2-3.
+// conversion with scale 1 of bytes 0-1, then of bytes 2-3 shifted down.
+// Through the compiler builtin (its low-word form: the word-select form
+// produced the upper pair as a copy of the lower on this toolchain), not
+// inline assembly: the compiler then keeps the wait states an MFMA needs
+// before a VALU instruction overwrites one of its source registers, which
+// it does not do around inline assembly.
+__device__ inline uint32_t e4m3x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false));
+}
 __device__ inline uint2 e4m3x4_to_bf16x4(uint32_t w) {
-  uint32_t lo, hi;
-  asm("v_cvt_scalef32_pk_bf16_fp8 %0, %1, 1.0" : "=v"(lo) : "v"(w));
-  asm("v_cvt_scalef32_pk_bf16_fp8 %0, %1, 1.0 op_sel:[1,0,0]" : "=v"(hi) : "v"(w));
-  return make_uint2(lo, hi);
+  return make_uint2(e4m3x2_to_bf16x2(w), e4m3x2_to_bf16x2(w >> 16));
 }
 
 // Raw E4M3 rows of RB bytes are staged swizzled too: chunk c of row r at
@@ -413,11 +425,11 @@ __device__ inline void qk_block_e4m3(const unsigned char* raw, int blk, const ui
 }
 
 // LDS of a full-attention ring kernel: per token group an NS-stage ring of
-// TW K rows and TW V rows (bf16: 2 hd bytes a row; E4M3: hd bytes, plus a
-// converted bf16 V tile, and a converted K tile when the group has several
-// waves); at least the end-of-split merge of TGW groups.
+// TW K rows and TW V rows (bf16: 2 hd bytes a row; E4M3: hd bytes, plus
+// converted bf16 K and V tiles when the group has several waves); at least
+// the end-of-split merge of TGW groups.
 __device__ __host__ constexpr int fa_ring_group_bytes(int nwv, int tw, int ns, bool kv8, int hd) {
-  return ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 ? (nwv > 1 ? 2 : 1) * tw * 2 * hd : 0);
+  return ns * 2 * tw * (kv8 ? hd : 2 * hd) + (kv8 && nwv > 1 ? 2 * tw * 2 * hd : 0);
 }
 __device__ __host__ constexpr int fa_ring_merge_bytes(int rt, int tgw, int hd) {
   return tgw > 1 ? tgw * 16 * rt * 16 + (tgw - 1) * 16 * rt * hd * 4 : 0;
@@ -487,6 +499,65 @@ __device__ inline uint2 v_operand_tr_at(const unsigned char* vbase, int blk, int
   return __builtin_bit_cast(uint2, v);
 }
 
+
+// V operands of P.V straight from raw E4M3 V rows (RB bytes, chunk c of row
+// r at c ^ raw_swz(r)) by gfx950's 8-bit transposing LDS read: in each
+// 16-lane group, lane pair p supplies 8 bytes of one row and lane q receives
+// byte q of the group's 16-byte columns, i.e. one head dim of the 8 rows
+// (checked on the device).  Each lane pair names the row it wants, so the 8
+// tokens come in the k order of the P fragments: for a pair of 16-token
+// blocks, the lane group's 4 tokens of block 2 bp, then its 4 of block
+// 2 bp + 1 (as v_operand_tr_at twice); the 8 values are then converted to
+// bf16 in registers (exact).
+template <int RB>
+__device__ inline uint2 ds_read_tr8(const unsigned char* raw_v, int row, int nb, int lane) {
+  typedef int v2i __attribute__((ext_vector_type(2)));
+  const unsigned char* p = raw_v + row * RB + 16 * (nb ^ raw_swz<RB>(row)) + 8 * (lane & 1);
+  const v2i r = __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i*)(p));
+  return make_uint2((uint32_t)r.x, (uint32_t)r.y);
+}
+// head dims 16 nb .. 16 nb + 15 of blocks 2 bp, 2 bp + 1 (16x16x32 B operand)
+template <int RB>
+__device__ inline uint4 v_operand_e4m3_pair(const unsigned char* raw_v, int bp, int nb, int lane) {
+  const int g = lane >> 4, r = (lane & 15) >> 1;
+  const int row = 32 * bp + 16 * (r >> 2) + 4 * g + (r & 3);
+  const uint2 x = ds_read_tr8<RB>(raw_v, row, nb, lane);
+  const uint2 lo = e4m3x4_to_bf16x4(x.x), hi = e4m3x4_to_bf16x4(x.y);
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+// head dims 16 nb .. 16 nb + 15 of block bi (16x16x16 B operand: the lane
+// group's 4 tokens; the lane pairs 4 .. 7 repeat rows 0 .. 3)
+template <int RB>
+__device__ inline uint2 v_operand_e4m3(const unsigned char* raw_v, int bi, int nb, int lane) {
+  const int g = lane >> 4, r = (lane & 15) >> 1;
+  const uint2 x = ds_read_tr8<RB>(raw_v, 16 * bi + 4 * g + (r & 3), nb, lane);
+  return e4m3x4_to_bf16x4(x.x);
+}
+
+// O += P . V for the NB 16-token blocks of a raw E4M3 V tile (RB-byte rows).
+template <int RPW, int NB, int HDIM, int RB>
+__device__ inline void pv_tile_e4m3(WaveState<RPW, HDIM>& st, const PFrags<NB, RPW>& pf, const unsigned char* raw_v,
+                                    int lane) {
+  if constexpr (NB % 2 == 0) {
+#pragma unroll
+    for (int bp = 0; bp < NB / 2; ++bp)
+#pragma unroll
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint4 vb = v_operand_e4m3_pair<RB>(raw_v, bp, nb, lane);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k32(pf.w[bp][rr], vb, st.o[rr][nb]);
+      }
+  } else {
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+      for (int nb = 0; nb < HDIM / 16; ++nb) {
+        const uint2 vb = v_operand_e4m3<RB>(raw_v, bi, nb, lane);
+#pragma unroll
+        for (int rr = 0; rr < RPW; ++rr) st.o[rr][nb] = mfma_k16(pf.h[bi][rr], vb, st.o[rr][nb]);
+      }
+  }
+}
 
 // O += P . V for the NB 16-token blocks of a staged tile (V rows swizzled at
 // vbase).  With an even NB two blocks share one 16x16x32 product: k slots

@@ -52,8 +52,119 @@ __device__ inline void load_q_tile(uint4 (&q)[NKK], const uint16_t* __restrict__
   }
 }
 
+// ---------------------------------------------------------------------------- balanced token splits
+// The full-attention pass cuts each sequence's cache into splits of S tokens
+// and gives every (sequence, KV head, split) item one workgroup of a 1-D
+// grid of sp.n_items workgroups (one residency round).  The lengths live on
+// the device, so every workgroup of the pass and of its merge derives the
+// same S from len[]: the shortest multiple of sp.align, at least
+// sp.min_split, whose items number at most n_items -- ragged lengths then
+// fill the grid evenly instead of leaving the workgroups past a short
+// sequence's end idle.  sp.fixed > 0 fixes S instead (the grid then covers
+// every split of the capacity).  Items are numbered sequence-major, then KV
+// head, then split.  Each wave computes these wave-uniform values on its own
+// (lanes over sequences), so nothing is shared or cleared between launches.
+__device__ inline long long wave_sum_ll(long long v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// The clamped lengths of the sequences b = lane, lane + 64, ...: the first
+// held in a register (every sequence of a batch of up to 64), the rest
+// reloaded where a pass needs them.
+struct LaneLens {
+  const int32_t* len;
+  int B, max_len, l0;
+  __device__ LaneLens(const int32_t* len_, int B_, int max_len_) : len(len_), B(B_), max_len(max_len_) {
+    const int lane = threadIdx.x & 63;
+    l0 = lane < B ? clamp_len(len, lane, max_len) : 0;
+  }
+  // f(b, L) for each of this lane's sequences
+  template <class F>
+  __device__ void for_each(F&& f) const {
+    const int lane = threadIdx.x & 63;
+    if (lane < B) f(lane, l0);
+    for (int b = lane + 64; b < B; b += 64) f(b, clamp_len(len, b, max_len));
+  }
+};
+
+// (sequence, KV head, split) items of split length S
+__device__ inline long long fa_items_of(const LaneLens& ll, int Hkv, int S) {
+  long long n = 0;
+  ll.for_each([&](int, int L) { n += (L + S - 1) / S; });
+  return wave_sum_ll(n) * Hkv;
+}
+
+__device__ inline int fa_split_len(const LaneLens& ll, int Hkv, const FaSplitPlan& sp) {
+  if (sp.fixed > 0) return sp.fixed;
+  long long tot = 0;
+  ll.for_each([&](int, int L) { tot += L; });
+  tot = wave_sum_ll(tot) * Hkv;  // token rows over every (sequence, KV head)
+  const long long units = (long long)ll.B * Hkv;
+  const long long al = sp.align;
+  // items(S) >= tot / S, so S >= tot / n_items; items(S) <= tot / S + units,
+  // so S = tot / (n_items - units) fits (with n_items > units), as does any
+  // S of at least the capacity (the host makes n_items >= units)
+  const long long cap_u = (ll.max_len + al - 1) / al;
+  long long lo = max((sp.min_split + al - 1) / al, (tot + sp.n_items * al - 1) / (sp.n_items * al));
+  long long hi = sp.n_items > units ? (tot + (sp.n_items - units) * al - 1) / ((sp.n_items - units) * al) : cap_u;
+  hi = max(min(hi, cap_u), lo);  // items(lo) <= items(hi) when hi is raised to lo
+  while (lo < hi) {  // items(S) falls as S grows: the smallest S that fits
+    const long long mid = (lo + hi) / 2;
+    if (fa_items_of(ll, Hkv, (int)(mid * al)) <= sp.n_items)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  return __builtin_amdgcn_readfirstlane((int)(hi * al));
+}
+
+// The (sequence, KV head, split) of item `item` with split length S; false
+// if the item is past the last one (its workgroup has nothing to do).
+__device__ inline bool fa_locate(const LaneLens& ll, int Hkv, int S, int item, int& b, int& g, int& split) {
+  const int lane = threadIdx.x & 63;
+  int rem = item;
+  for (int b0 = 0; b0 < ll.B; b0 += 64) {
+    const int bb = b0 + lane;
+    const int L = b0 == 0 ? ll.l0 : (bb < ll.B ? clamp_len(ll.len, bb, ll.max_len) : 0);
+    const int nb = (L + S - 1) / S;
+    int incl = nb * Hkv;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    const unsigned long long hit = __ballot(incl > rem);
+    if (hit) {
+      const int l = __ffsll((long long)hit) - 1;
+      const int n = __shfl(nb, l);
+      const int r = rem - (__shfl(incl, l) - n * Hkv);  // item within sequence b0 + l
+      b = __builtin_amdgcn_readfirstlane(b0 + l);
+      g = __builtin_amdgcn_readfirstlane(r / n);
+      split = __builtin_amdgcn_readfirstlane(r % n);
+      return true;
+    }
+    rem -= __shfl(incl, 63);
+  }
+  return false;
+}
+
+// First item of (sequence b, KV head g) with split length S.
+__device__ inline int fa_first_item(const LaneLens& ll, int Hkv, int S, int b, int g) {
+  long long n = 0;
+  int nb = 0;  // splits of sequence b (on the lane holding it)
+  ll.for_each([&](int bb, int L) {
+    if (bb < b) n += (L + S - 1) / S;
+    if (bb == b) nb = (L + S - 1) / S;
+  });
+  n = wave_sum_ll(n) * Hkv;
+  nb = __shfl(nb, b & 63);  // lane b % 64 holds sequence b
+  return (int)n + g * nb;
+}
+
 // ============================================================================ full attention
-// grid (n_split, Hkv, B), 64 * NW threads, dynamic LDS = FA_STAGES * STAGE_BYTES.
+// grid (items), 64 * NW threads, dynamic LDS = FA_STAGES * STAGE_BYTES.
 // Cache rows stream global -> LDS with no register staging (16-byte direct
 // LDS loads), FA_STAGES - 1 tiles in flight while one is computed; a single
 // barrier per tile.  NW = 4 waves for up to 32 query rows, 8 above (two
@@ -75,12 +186,14 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
   constexpr int LPW = 16 / NW;
   extern __shared__ __align__(16) unsigned char smem[];
 
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const LaneLens ll(a.len, a.B, a.max_len);
+  const int S = fa_split_len(ll, a.Hkv, a.sp);
+  int b, g, split;
+  if (!fa_locate(ll, a.Hkv, S, blockIdx.x, b, g, split)) return;
   const int Lv = clamp_len(a.len, b, a.max_len);
-  const int t_begin = split * a.split_tokens;
-  if (t_begin >= Lv) return;
-  const int t_end = min(Lv, t_begin + a.split_tokens);
+  const int t_begin = split * S;
+  const int t_end = min(Lv, t_begin + S);
   const int ntiles = (t_end - t_begin + TILE - 1) / TILE;
   const int tg = wave / RTW;
   const int rt0 = (wave % RTW) * RPW;
@@ -147,9 +260,7 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
         }
     softmax_pv_swz<RPW, BPW>(st, stg, blk, S, lane);
   }
-  const int nslot = a.n_split * TG;
-  const int64_t unit = (int64_t)b * a.Hkv + g;
-  const int64_t slot_base_row = (unit * nslot + (int64_t)split * TG + tg) * (16 * RT);
+  const int64_t slot_base_row = ((int64_t)blockIdx.x * TG + tg) * (16 * RT);
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
 }
 
@@ -162,11 +273,13 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // partial (m, l, O) per split.
 // KV8: the cache is E4M3 bytes with one scale per KV head (k_scale folds
 // into the logit scale, v_scale is applied by the merge); each token group
-// stages raw rows in its ring (swizzled by raw_swz), reads the K operands
-// raw and converts them in registers, and converts the V rows of the
-// current tile into one bf16 tile (before the logits, so that the
-// conversion overlaps them; one barrier before P.V).  HDIM: head dim (128
-// or 256).  KP: cache policy of the stage loads (FaCachePolicy).
+// stages raw rows in its ring (swizzled by raw_swz).  A one-wave group reads
+// the K operands raw and the V operands raw by 8-bit transposing LDS reads,
+// both converted in registers (no tile, no barrier); a group of several
+// waves converts each tile's K and V rows once into shared bf16 tiles (one
+// barrier per tile), which its waves read as the bf16 path reads its stage
+// (each wave converting the whole tile itself measured 1.45x slower at 64
+// query rows per KV head).  HDIM: head dim (128 or 256).  KP: cache policy of the stage loads (FaCachePolicy).
 template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM, int KP>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
@@ -178,25 +291,29 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int LPM = TW * RB / 1024 / NWV;                // 1 KB loads per matrix per stage per wave
   constexpr int SB = 2 * TW * RB;                          // ring stage: K rows then V rows
   constexpr int GB = fa_ring_group_bytes(NWV, TW, NS, KV8, HDIM);  // LDS of one token group: ring + tiles
-  // E4M3 with several waves per group: K is converted once into a shared
-  // bf16 tile too (each wave would otherwise convert the whole tile for its
-  // own row tiles)
+  // E4M3 with several waves per group: K and V are converted once into
+  // shared bf16 tiles (each wave would otherwise convert the whole tile for
+  // its own row tiles)
   constexpr bool KCONV = KV8 && NWV > 1;
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads for every wave and stage");
   static_assert(TGW == 1 || RT > 1, "token groups are not combined with the logits output");
   extern __shared__ __align__(16) unsigned char smem[];
 
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & 63;
   const int tg = (threadIdx.x >> 6) / NWV, wave = (threadIdx.x >> 6) % NWV;  // token group, wave in it
+  const LaneLens ll(a.len, a.B, a.max_len);
+  const int S = fa_split_len(ll, a.Hkv, a.sp);
+  int b, g, split;
+  if (!fa_locate(ll, a.Hkv, S, blockIdx.x, b, g, split)) return;
   const int Lv = clamp_len(a.len, b, a.max_len);
-  if (split * a.split_tokens >= Lv) return;
   // token group tg streams the tg-th contiguous part of the split through its own ring
-  const int part = a.split_tokens / TGW;
-  const int t_begin = split * a.split_tokens + tg * part;
+  const int part = S / TGW;
+  const int t_begin = split * S + tg * part;
   const int t_end = min(Lv, t_begin + part);
   const int ntiles = t_end > t_begin ? (t_end - t_begin + TW - 1) / TW : 0;
-  const int nloop = (min(Lv, split * a.split_tokens + part) - split * a.split_tokens + TW - 1) / TW;  // group 0's
+  const int nloop = (min(Lv, split * S + part) - split * S + TW - 1) / TW;  // group 0's
+  // FA_STREAM_K_HEAD: K rows of the group before this offset are non-temporal
+  const int k_stream = part - (int)((int64_t)part * a.k_keep_pct / 100);
   const int rt0 = wave * RPW;
 
   uint4 q[RPW][NKK];
@@ -216,8 +333,8 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem) + (uint32_t)(tg * GB);
   unsigned char* ring_p = smem + tg * GB;
-  unsigned char* tile_p = ring_p + NS * SB;  // KV8: the converted V tile
-  unsigned char* tile_k = tile_p + TW * SRB;  // KCONV: the converted K tile
+  unsigned char* tile_k = ring_p + NS * SB;   // KCONV: the converted K tile
+  unsigned char* tile_v = tile_k + TW * SRB;  // KCONV: the converted V tile
   // logits output of a single row tile (C G <= 16 query rows): this lane's
   // row (c, h), or null.  Row-major [B*Hkv][C*G][logit_stride], log2 units.
   float* lrow = nullptr;
@@ -263,7 +380,7 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   };
   auto issue = [&](int tile) __attribute__((always_inline)) {
     if constexpr (KP == FA_STREAM_K_HEAD) {  // one scalar branch per tile
-      if (tile * TW < a.k_stream_tokens)
+      if (tile * TW < k_stream)
         issue_as(tile, std::true_type{});
       else
         issue_as(tile, std::false_type{});
@@ -286,12 +403,12 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     if (i < ntiles && i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = ring_p + (i % NS) * SB;
     if (i >= ntiles) {
-      if (KV8 && NWV * TGW > 1) __syncthreads();  // the other groups' V-tile barrier
+      if (KCONV) __syncthreads();  // the other groups' K-tile barrier
       continue;
     }
-    if constexpr (KV8) convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_p, 64 * wave + lane);
     if constexpr (KCONV) {
       convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, 64 * wave + lane);
+      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_v, 64 * wave + lane);
       __syncthreads();  // both tiles converted by every wave of the group
     }
     const int t0 = t_begin + i * TW;
@@ -326,12 +443,14 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
         }
     PFrags<NB, RPW> pf;
     online_softmax(st, S, pf, lane);
-    if (KV8 && !KCONV && NWV * TGW > 1) __syncthreads();  // V tile converted by every wave of the group
-    const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-    pv_tile<RPW, NB, HDIM>(st, pf, vbase, lane);
+    if constexpr (KCONV)
+      pv_tile<RPW, NB, HDIM>(st, pf, tile_v, lane);
+    else if constexpr (KV8)  // V read raw (transposing 8-bit reads) and converted in registers
+      pv_tile_e4m3<RPW, NB, HDIM, RB>(st, pf, stg + TW * RB, lane);
+    else
+      pv_tile<RPW, NB, HDIM>(st, pf, stg + TW * SRB, lane);
   }
-  const int64_t unit = (int64_t)b * a.Hkv + g;
-  const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
+  const int64_t slot_base_row = (int64_t)blockIdx.x * (16 * RT);  // one partial per item
   if constexpr (TGW == 1) {
     store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
   } else {
@@ -430,11 +549,14 @@ __global__ __launch_bounds__(256) void k_combine(CombineArgs a) {
   }
   if (c >= a.C || h >= a.G) return;
   int nvalid = a.nslot;
-  if (!a.sa_mode) {
+  int64_t base = unit * a.nslot * a.rows + r;
+  if (!a.sa_mode) {  // the full-attention items of (b, g): their slots are contiguous
+    const LaneLens ll(a.len, a.B, a.max_len);
+    const int S = fa_split_len(ll, a.Hkv, a.sp);
     const int Lv = clamp_len(a.len, b, a.max_len);
-    nvalid = ((Lv + a.split_tokens - 1) / a.split_tokens) * a.tg;
+    nvalid = ((Lv + S - 1) / S) * a.tg;
+    base = (int64_t)fa_first_item(ll, a.Hkv, S, b, g) * a.tg * a.rows + r;
   }
-  const int64_t base = unit * a.nslot * a.rows + r;
   // one pass over the partials: each slot group merges its slots online
   // (reference maximum m, sum l, output row, rescaled when m rises) with
   // every slot's loads issued together, then the groups are merged in LDS
@@ -591,6 +713,28 @@ __device__ __forceinline__ void pool_emit_block(const f32x4 (&acc)[RPW], float c
   }
 }
 
+// Scores of two 16-token blocks a and b of a one-row-tile wave (queries of
+// 8 or 16 heads; acc as in pool_emit_block), packed into one register: the
+// lane swap meets the odd lane groups of a with the even groups of b, so
+// lane group j ends up with the sum over its rows' pair of groups for block
+// j & 1 -- the same values, summed in the same order, as pool_emit_block.
+template <int GP>
+__device__ __forceinline__ float pool_pair_value(const f32x4& a, const f32x4& b, float c2, const float (&fac)[4],
+                                                 const float (&msub)[4]) {
+  float ea[4], eb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ea[i] = fast_exp2(a[i] * c2 - msub[i]) * fac[i];
+    eb[i] = fast_exp2(b[i] * c2 - msub[i]) * fac[i];
+  }
+  const float sa = (ea[0] + ea[1]) + (ea[2] + ea[3]);
+  const float sb = (eb[0] + eb[1]) + (eb[2] + eb[3]);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(sa), __float_as_uint(sb), false, false);
+  float v = __uint_as_float(r[0]) + __uint_as_float(r[1]);  // group j: block j & 1, rows of groups j & 2, (j & 2) + 1
+  if constexpr (GP == 16) v = sum_xor32(v);                // and of groups j ^ 2
+  return v;
+}
+
 // Row constants of rows 16 (rt0 + rr) + 4 (lane / 16) + i: p = exp2(s2 -
 // msub) * fac = exp2(s2 - M2) / Z (fac = exp2(-M2) / Z unless M2 is too large
 // for that, then msub = M2 and fac = 1 / Z).  Branch-free on purpose:
@@ -648,6 +792,9 @@ struct PoolShape {
   static constexpr int SB = TW * RB;                          // ring stage
   // E4M3 with several waves: K converted once into a shared bf16 tile
   static constexpr bool KCONV = KV8 && NWV > 1;
+  // one row tile per wave of queries of 8 or 16 heads: two blocks' scores
+  // are packed into the four lane groups and emitted together
+  static constexpr bool PACK2 = WPQ == 1 && RPW == 1 && (GP == 8 || GP == 16) && (TW / 16) % 2 == 0;
   static constexpr int LDS = NS * SB + (KCONV ? TW * SRB : 0);  // before the histograms
 };
 template <int RT, int GP, bool KV8, int HDIM>
@@ -734,7 +881,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
     if (c < a.C && t < nc0 + c) {
       scores[c * a.score_stride + t] = v;
       if (a.hist) {
-        const int dg = score_digit(score_key(v));
+        const int dg = score_digit(v);
         atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
       }
     }
@@ -754,8 +901,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
       convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, tid);
       __syncthreads();  // the K tile converted by every wave
     }
-#pragma unroll
-    for (int bi = 0; bi < NB; ++bi) {
+    // logits S = Q.K^T of 16-token block bi for this wave's row tiles
+    auto block_acc = [&](int bi, f32x4 (&acc)[RPW]) __attribute__((always_inline)) {
       const int row = 16 * bi + (lane & 15);
       uint4 k4[NKK];
       if constexpr (PS::KCONV) {
@@ -772,17 +919,36 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
         for (int kk = 0; kk < NKK; ++kk)
           k4[kk] = *(const uint4*)(rp + 16 * (k_chunk(kk, lane) ^ stage_swz(row)));
       }
-      f32x4 acc[RPW];
 #pragma unroll
       for (int rr = 0; rr < RPW; ++rr) {
         acc[rr] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) acc[rr] = mfma_k32(q[rr][kk], k4[kk], acc[rr]);
       }
-      if constexpr (PS::WPQ == 1)
-        pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
-      else
-        pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit_part);
+    };
+    if constexpr (PS::PACK2) {
+      // two blocks per emit: lane group j holds block bp + (j & 1); with 8
+      // heads per query groups 0, 1 hold query 2 rt0 and groups 2, 3 query
+      // 2 rt0 + 1, with 16 heads groups 2, 3 repeat groups 0, 1 (query rt0)
+      const int q4 = lane >> 4;
+#pragma unroll
+      for (int bp = 0; bp < NB; bp += 2) {
+        f32x4 acc_a[1], acc_b[1];
+        block_acc(bp, acc_a);
+        block_acc(bp + 1, acc_b);
+        const float v = pool_pair_value<GP>(acc_a[0], acc_b[0], c2, fac[0], msub[0]);
+        if (GP == 8 || q4 < 2) emit(v, GP == 8 ? 2 * rt0 + (q4 >> 1) : rt0, t0 + 16 * (bp + (q4 & 1)) + (lane & 15));
+      }
+    } else {
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi) {
+        f32x4 acc[RPW];
+        block_acc(bi, acc);
+        if constexpr (PS::WPQ == 1)
+          pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit);
+        else
+          pool_emit_block<RPW, GP>(acc, c2, fac, msub, rt0, t0 + 16 * bi + (lane & 15), lane, emit_part);
+      }
     }
     if constexpr (PS::WPQ > 1) {  // the query's first wave adds its waves' parts and emits
       __syncthreads();
@@ -860,7 +1026,7 @@ __global__ __launch_bounds__(NT) void k_pool_logits(PoolArgs a) {
         if (t + j < nc) {
           sr[j] = v[j];
           if (a.hist) {
-            const int dg = score_digit(score_key(v[j]));
+            const int dg = score_digit(v[j]);
             atomicAdd(&hist[c * (NBINS / 2) + (dg >> 1)], 1u << ((dg & 1) << 4));
           }
         }
@@ -914,7 +1080,7 @@ __global__ __launch_bounds__(NT) void k_sel_hist(SelArgs a) {
   for (int i = threadIdx.x; i < NBINS; i += NT) h[i] = 0;
   __syncthreads();
   const float* P = a.scores + row * a.score_stride;
-  for (int t = t0 + threadIdx.x; t < t1; t += NT) atomicAdd(&h[score_digit(score_key(P[t]))], 1u);
+  for (int t = t0 + threadIdx.x; t < t1; t += NT) atomicAdd(&h[score_digit(P[t])], 1u);
   __syncthreads();
   for (int i = threadIdx.x; i < NBINS; i += NT)
     if (h[i]) atomicAdd(&a.hist[row * NBINS + i], h[i]);
@@ -1145,7 +1311,7 @@ __device__ inline void filter_chunk(const SelArgs& a, int64_t row, const Thresho
     const int t = tb + lane;
     const bool valid = t < t1;
     const uint32_t key = score_key(v[j]);
-    const int d = score_digit(key);
+    const int d = score_digit(v[j]);
     const uint64_t sm = __ballot(valid && d > sel_above);
     if (lane == 0) bm[tb >> 6] = sm;
     const uint64_t cm = __ballot(valid && d == cand_digit);
@@ -1472,11 +1638,9 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
   constexpr int CPR = RB / 16;                  // 16-byte chunks per staged row
   constexpr int LPM = TW * RB / 1024 / NWV;
   constexpr int SB = 2 * TW * RB;
-  constexpr int TB = KV8 ? TW * SRB : 0;        // converted V tile
   static_assert(LPM >= 1 && TW * RB == 1024 * LPM * NWV, "whole 1 KB loads per wave and stage");
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* tile_p = smem + NS * SB;                  // KV8: the converted V tile
-  int32_t* sidx = (int32_t*)(smem + NS * SB + TB);        // [split_slots]
+  int32_t* sidx = (int32_t*)(smem + NS * SB);  // [split_slots]
 
   const int split = blockIdx.x;
   const int64_t unit = blockIdx.y;
@@ -1559,8 +1723,6 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
         if (k == (i + NS - 1) % NS) vmask[k] = mnew;
     }
     const unsigned char* stg = smem + (i % NS) * SB;
-    if constexpr (KV8)  // V tile complete at the barrier below (one wave: in order); K is read raw
-      convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_p, threadIdx.x);
     if (NWV > 1) {  // every wave's row bits
       __shared__ uint32_t s_mask[NWV];
       if (lane == 0) s_mask[wave] = m_i;
@@ -1588,8 +1750,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
         }
     PFrags<NB, RPW> pf;
     online_softmax(st, S, pf, lane);
-    const unsigned char* vbase = KV8 ? tile_p : stg + TW * SRB;
-    pv_tile<RPW, NB, HDIM>(st, pf, vbase, lane);
+    if constexpr (KV8)  // E4M3: K and V operands read raw and converted in registers
+      pv_tile_e4m3<RPW, NB, HDIM, RB>(st, pf, stg + TW * RB, lane);
+    else
+      pv_tile<RPW, NB, HDIM>(st, pf, stg + TW * SRB, lane);
   }
   const int64_t slot_base_row = (unit * a.n_split + split) * (16 * RT);
   store_partial<RPW>(st, a.part_o, a.part_ml, slot_base_row, rt0, lane);
@@ -1604,8 +1768,10 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 // the streaming kernels issue them (up to 8 in flight per wave into an 8 KB
 // ring, each piece read back from LDS once it has landed), 3: the same
 // non-temporal.  Every mode folds each 32-bit word of src exactly once
-// (xor), so *sink ^= the xor of the whole buffer (keeps the loads live and
-// lets a test check that every word was read once).
+// (xor); workgroup w stores the fold of its slice to sink[w] (keeps the
+// loads live and lets a test check that every word was read once: the xor
+// of sink[0, gridDim.x) is the xor of the whole buffer).  No atomics: the
+// same-address atomics of a whole grid serialise for ~0.2 ms.
 template <int MODE>
 __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ src, int64_t n16, uint32_t* sink) {
   __shared__ __align__(16) unsigned char ring[4 * 8 * 1024];
@@ -1664,7 +1830,10 @@ __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ 
   acc ^= __shfl_xor(acc, 8);
   acc ^= __shfl_xor(acc, 16);
   acc ^= __shfl_xor(acc, 32);
-  if (lane == 0) atomicXor(sink, acc);
+  __shared__ uint32_t s_fold[4];
+  if (lane == 0) s_fold[wave] = acc;
+  __syncthreads();
+  if (tid == 0) sink[blockIdx.x] = s_fold[0] ^ s_fold[1] ^ s_fold[2] ^ s_fold[3];
 }
 
 // ============================================================================ host launchers
@@ -1817,7 +1986,7 @@ hipError_t fa_wgs_per_cu(int RT, int variant, bool kv8, int* wgs) {
 }
 
 hipError_t launch_fa_split(const FaArgs& a, int RT, int variant, hipStream_t s) {
-  dim3 grid(a.n_split, a.Hkv, a.B);
+  dim3 grid(a.sp.n_items);
 #define HS2_RING_LAUNCH(v, rt, nwv, tw, ns, tgw, hd) \
   if (variant == v && RT == rt) return fa_ring_dispatch<rt, nwv, tw, ns, tgw, hd>(a, grid, s);
   HS2_RING_VARIANTS(HS2_RING_LAUNCH)
@@ -1984,7 +2153,7 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
 }
 
 size_t sa_smem_bytes(int split_slots, bool kv8, int hd) {
-  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? hd : 2 * hd) + (kv8 ? SAR_TW * 2 * hd : 0) +
+  return (size_t)SAR_NS * 2 * SAR_TW * (kv8 ? hd : 2 * hd) +
          sizeof(int32_t) * (size_t)((split_slots + SAR_TW - 1) / SAR_TW * SAR_TW);
 }
 
@@ -2007,8 +2176,8 @@ hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s) {
 
 hipError_t launch_stream_probe(const void* src, int64_t n16, int mode, uint32_t* sink, hipStream_t s) {
   // 16 workgroups per compute unit of 256 (more than stay resident: the
-  // dispatcher keeps every CU busy to the end)
-  const dim3 grid(4096), block(256);
+  // dispatcher keeps every CU busy to the end), one sink word each
+  const dim3 grid(STREAM_PROBE_WORKGROUPS), block(256);
   const uint4* p = (const uint4*)src;
   switch (mode) {
     case 0: hipLaunchKernelGGL(k_stream_probe<0>, grid, block, 0, s, p, n16, sink); break;

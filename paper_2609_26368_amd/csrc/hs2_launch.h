@@ -6,22 +6,31 @@
 
 namespace hs2 {
 
+// Token splits of the full-attention pass: fixed > 0 fixes the split
+// length; else every workgroup derives the balanced length from len[] (the
+// shortest multiple of align, at least min_split, whose (sequence, KV head,
+// split) items number at most n_items, the grid size).
+struct FaSplitPlan {
+  int fixed, align, min_split, n_items;
+};
+
 struct FaArgs {
   const uint16_t* q;
   const uint16_t* K;
   const uint16_t* V;
   const int32_t* len;
-  float* part_o;   // [B*Hkv][n_split*TG][16 RT][HD]
-  float* part_ml;  // [B*Hkv][n_split*TG][16 RT][4]: (m ref, l, m true, 0)
+  float* part_o;   // [n_items * TG][16 RT][HD]
+  float* part_ml;  // [n_items * TG][16 RT][4]: (m ref, l, m true, 0)
   int64_t stride_b, stride_h, stride_t;
   float c2;        // softmax scale * log2(e)
   int B, C, Hq, Hkv, G, Gp, max_len;
-  int split_tokens, n_split;
+  FaSplitPlan sp;  // grid: sp.n_items workgroups, one (sequence, KV head, split) item each
   float* logits;   // [B*Hkv][C*G][logit_stride] logits in log2 units (ring kernels), or null
   int64_t logit_stride;
   const float* k_scale;  // [Hkv] for an E4M3 cache (K, V are then byte arrays), else null
   int cache_policy;      // ring kernels: FaCachePolicy of the stage loads
-  int k_stream_tokens;   // FA_STREAM_K_HEAD: K rows of a token group before this offset are non-temporal
+  int k_keep_pct;        // FA_STREAM_K_HEAD: the last k_keep_pct % of each token group's K rows stay
+                         // cacheable, the rows before them are non-temporal
 };
 
 // Cache policy of the full-attention ring kernel's loads.  Non-temporal
@@ -31,7 +40,7 @@ enum FaCachePolicy {
   FA_CACHE_DEFAULT = 0,  // every row cacheable
   FA_STREAM_V = 1,       // V non-temporal, K cacheable
   FA_STREAM_KV = 2,      // K and V non-temporal
-  FA_STREAM_K_HEAD = 3,  // V non-temporal, K non-temporal before k_stream_tokens of each token group
+  FA_STREAM_K_HEAD = 3,  // V non-temporal, K non-temporal in the leading part of each token group
 };
 // Policies built for each query row tile count: one row tile takes no
 // per-tile branch (it is latency-sensitive), more row tiles take the split one.
@@ -50,7 +59,7 @@ struct CombineArgs {
   int rows;             // partial rows per slot
   int nslot;            // partial slots per unit
   int tg;               // slots per split (FA)
-  int split_tokens;     // FA split size (FA only)
+  FaSplitPlan sp;       // FA only: the full-attention pass's splits (partials of item i at slots i * tg ..)
   int sa_mode;
   uint4* clear;         // 16-byte words zeroed by the kernel as a side job, or null
   int64_t n_clear;
@@ -144,7 +153,8 @@ hipError_t launch_block_select(const BlockSelArgs& a, hipStream_t s);  // block 
 hipError_t launch_sa_split(const SaArgs& a, int RT, hipStream_t s);
 // streaming-read probe over n16 16-byte words (mode: 0 register loads, 1
 // non-temporal register loads, 2 direct-to-LDS loads, 3 non-temporal
-// direct-to-LDS loads); xors a fold of the data into *sink
+// direct-to-LDS loads); workgroup w stores a fold of its slice to sink[w]
+constexpr int STREAM_PROBE_WORKGROUPS = 4096;
 hipError_t launch_stream_probe(const void* src, int64_t n16, int mode, uint32_t* sink, hipStream_t s);
 
 }  // namespace hs2

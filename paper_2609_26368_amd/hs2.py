@@ -328,13 +328,18 @@ def hs2_select_from_scores(dims, scores, len, k, window, idx, workspace, stream=
                                          _stream(stream)))
 
 
+STREAM_PROBE_SINK_WORDS = 4096
+
+
 def hs2_stream_read_probe(src, mode, sink, stream=None):
     """Streaming read of the whole of tensor src (device, contiguous) in the
-    given load mode; xors a fold of it into sink (one int32/uint32 element)."""
+    given load mode; sink (STREAM_PROBE_SINK_WORDS int32 / uint32 elements)
+    receives one fold per workgroup, whose xor is the xor of src's words."""
     if not src.is_contiguous():
         raise ValueError("src must be contiguous")
-    if sink.numel() < 1 or sink.element_size() != 4 or sink.device != src.device:
-        raise ValueError("sink: one 4-byte element on the device of src")
+    if (sink.numel() < STREAM_PROBE_SINK_WORDS or sink.element_size() != 4 or sink.device != src.device
+            or not sink.is_contiguous()):
+        raise ValueError(f"sink: {STREAM_PROBE_SINK_WORDS} contiguous 4-byte elements on the device of src")
     _check(load().hs2_stream_read_probe(_ptr(src), src.numel() * src.element_size(), int(mode), _ptr(sink),
                                         _stream(stream)))
 

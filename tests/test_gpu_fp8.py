@@ -129,3 +129,53 @@ def test_fp8_equals_bf16_on_the_dequantised_cache(w, fa_split, pool_split, varia
             n = max(0, int(inp.lens[b]) - C + c - w.window + 1)
             assert torch.equal(sc8[b, :, c, :n], scb[b, :, c, :n]), ("scores", b, c)
     assert torch.equal(sa8.view(torch.int16), sab.view(torch.int16)), "sparse layer"
+
+
+# every finite E4M3 code (0x7F and 0xFF are NaN), in every head dim of K and V
+_CODES = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], dtype=np.uint8)
+EVERY_CODE = [  # (workload, FA kernel variant): 16- and 32-token tiles, one, two and four row tiles
+    (W.Workload("fp8_codes_16q2kv", 1, 1200, 1, 16, 2, 128, 200, 40, 1), 3),
+    (W.Workload("fp8_codes_16q2kv", 1, 1200, 1, 16, 2, 128, 200, 40, 1), 2),
+    (W.Workload("fp8_codes_c4_16q2kv", 1, 1200, 4, 16, 2, 128, 200, 40, 1), 5),
+    (W.Workload("fp8_codes_c8_32q4kv", 1, 1200, 8, 32, 4, 128, 200, 40, 1), 7),
+]
+
+
+@pytest.mark.parametrize("w,variant", EVERY_CODE, ids=[f"{w.name}-v{v}" for w, v in EVERY_CODE])
+def test_fp8_every_code_equals_bf16(w, variant, monkeypatch):
+    """Every finite E4M3 byte value in every head dim of K and V (power-of-two
+    scales): the E4M3 entry points must give the bits of the bf16 entry
+    points on the dequantised cache, which checks each code's conversion in
+    both the K and the (transposed) V operand reads."""
+    from paper_2609_26368_amd import hs2
+    monkeypatch.setenv("HS2_FA_VARIANT", str(variant))
+    monkeypatch.setenv("HS2_FA_SPLIT", "512")  # the same splits for both formats
+    monkeypatch.setenv("HS2_POOL_SPLIT", "512")
+    inp = W.make_inputs(w, seed=17, kv="fp8")
+    B, C, Hq, Hkv, D, L = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim, inp.K.shape[2]
+    t = np.arange(L)[None, None, :, None]
+    d = np.arange(D)[None, None, None, :]
+    g = np.arange(Hkv)[None, :, None, None]
+    K8h = _CODES[(t * 131 + d * 7 + g) % _CODES.size].astype(np.uint8) * np.ones((B, 1, 1, 1), dtype=np.uint8)
+    V8h = _CODES[(t * 37 + d * 11 + 3 * g) % _CODES.size].astype(np.uint8) * np.ones((B, 1, 1, 1), dtype=np.uint8)
+    ks = np.full(Hkv, 2.0 ** -9, dtype=np.float32)
+    vs = np.full(Hkv, 2.0 ** -4, dtype=np.float32)
+    Kb = W.f32_to_bf16_bits((O.e4m3_to_f64(K8h) * ks[None, :, None, None]).astype(np.float32))
+    Vb = W.f32_to_bf16_bits((O.e4m3_to_f64(V8h) * vs[None, :, None, None]).astype(np.float32))
+    note(f"[fp8 every code] {w.name} variant {variant} lens={inp.lens.tolist()}")
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, L, w.k, w.window)
+    lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
+    q, qs = dev_bf16(inp.q_fa), dev_bf16(inp.q_sa[0])
+    sc = (torch.from_numpy(ks).cuda(), torch.from_numpy(vs).cuda())
+    K8, V8 = torch.from_numpy(np.ascontiguousarray(K8h)).cuda(), torch.from_numpy(np.ascontiguousarray(V8h)).cuda()
+    Kd, Vd = dev_bf16(Kb), dev_bf16(Vb)
+    out8, idx8 = blk.full(q, K8, V8, lens, kv_scales=sc)
+    out8, idx8 = out8.clone(), idx8.clone()
+    outb, idxb = blk.full(q, Kd, Vd, lens)
+    sa8 = blk.sparse(qs, K8, V8, lens, idxb, kv_scales=sc).clone()
+    sab = blk.sparse(qs, Kd, Vd, lens, idxb)
+    torch.cuda.synchronize()
+    assert torch.isfinite(outb.float()).all() and torch.isfinite(sab.float()).all()
+    assert torch.equal(idx8, idxb), "selection"
+    assert torch.equal(out8.view(torch.int16), outb.view(torch.int16)), "full-attention output"
+    assert torch.equal(sa8.view(torch.int16), sab.view(torch.int16)), "sparse layer"

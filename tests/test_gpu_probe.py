@@ -1,5 +1,6 @@
 """GPU: the streaming-read probe reads every 32-bit word of its buffer exactly
-once in each load mode (its xor fold equals the host's), including a buffer
+once in each load mode (the xor of its per-workgroup folds equals the
+host's xor of the buffer), including a buffer
 whose size leaves partial pieces and empty workgroup slices."""
 from __future__ import annotations
 
@@ -17,9 +18,9 @@ def test_stream_probe_reads_every_word_once(words16, mode):
     rng = np.random.default_rng(words16 + mode)
     host = rng.integers(0, 2 ** 32, size=4 * words16, dtype=np.uint32)
     buf = torch.from_numpy(host.view(np.int32)).cuda()
-    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(hs2.STREAM_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
     print(f"[probe] mode={mode} words16={words16}", flush=True)
     hs2.hs2_stream_read_probe(buf, mode, sink)
     torch.cuda.synchronize()
     want = np.bitwise_xor.reduce(host)
-    assert int(sink.cpu().numpy().view(np.uint32)[0]) == int(want)
+    assert int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))) == int(want)
