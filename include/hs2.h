@@ -86,7 +86,8 @@ typedef struct hs2_dims {
   int32_t n_queries;   /* C: decode tokens per sequence, 1 .. 16                  */
   int32_t n_q_heads;   /* Hq >= 1                                                 */
   int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, G = Hq / Hkv <= 64,            */
-                       /*   C * (G rounded up to a power of two) <= 128           */
+                       /*   C * (G rounded up to a power of two) <= 128,          */
+                       /*   B * Hkv * C <= 65535 (HS2_ERR_UNSUPPORTED)            */
   int32_t head_dim;    /* D: 128, or 256 (the paper's head dim, Sec. "Experimental */
                        /*   Setup"); other values: HS2_ERR_UNSUPPORTED            */
   int32_t max_len;     /* Lmax: cache capacity per sequence, 1 .. 2^27 tokens     */

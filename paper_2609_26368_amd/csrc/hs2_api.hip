@@ -24,6 +24,7 @@ using namespace hs2;
 constexpr int kMaxQueries = 16;
 constexpr int kMaxRows = 128;           // C * Gp
 constexpr int kMaxGroup = 64;
+constexpr int64_t kMaxGridRows = 65535;  // largest grid y extent: the (b, g, c) rows
 constexpr int32_t kMaxLen = 1 << 27;
 constexpr int kNBins = 1024;          // must match the kernels' first-level radix bins
 constexpr int kSelChunk = hs2::SEL_CHUNK;  // tokens per workgroup of the selection scans
@@ -101,6 +102,9 @@ hs2_status check_dims(const hs2_dims* d) {
     return fail(HS2_ERR_UNSUPPORTED, "head_dim %d not supported (128 or 256)", d->head_dim);
   const int G = d->n_q_heads / d->n_kv_heads;
   if (G > kMaxGroup) return fail(HS2_ERR_UNSUPPORTED, "query heads per KV head %d > %d", G, kMaxGroup);
+  // one grid row per (b, g, c) in the selection and sparse kernels
+  if ((int64_t)d->batch * d->n_kv_heads * d->n_queries > kMaxGridRows)
+    return fail(HS2_ERR_UNSUPPORTED, "batch * n_kv_heads * n_queries exceeds %d", kMaxGridRows);
   if (d->n_queries * next_pow2(G) > kMaxRows)
     return fail(HS2_ERR_UNSUPPORTED, "n_queries * pow2(G) = %d exceeds %d query rows per KV head",
                 d->n_queries * next_pow2(G), kMaxRows);

@@ -1050,8 +1050,9 @@ struct RowInfo {
   int pos, N, keff;
 };
 __device__ inline RowInfo row_info(const SelArgs& a, int64_t row) {
-  const int c = (int)(row % a.C);
-  const int b = (int)(row / ((int64_t)a.C * a.Hkv));
+  const int r = (int)row;  // rows = B Hkv C fit an int (checked by the host)
+  const int c = r % a.C;
+  const int b = r / (a.C * a.Hkv);
   const int Lv = clamp_len(a.len, b, a.max_len);
   RowInfo ri;
   ri.pos = Lv - a.C + c;
@@ -1114,19 +1115,21 @@ __device__ inline int block_scan_1024(int v, int* lds16, int& total) {
 }
 
 // Selection from the pooled scores and their histogram, in two launches
-// (1024 threads per workgroup; every workgroup of a row derives the same
-// threshold bin b* and need = k_eff - #(keys in bins above b*)):
-//   k_sel_filter  grid (chunks of SEL_TOKENS tokens, rows): marks the tokens
-//                 above b* in the row bitmap and collects the tokens of b*
+// (every workgroup of a row derives the same threshold bin b* and
+// need = k_eff - #(keys in bins above b*)):
+//   k_sel_filter  grid (chunks of 8192 tokens, rows), 256 threads: marks the
+//                 tokens above b* in the row bitmap (raw-bit compares, one
+//                 ballot per 64-token word) and collects the tokens of b*
 //                 (gathered in LDS, one global slot reservation per
 //                 workgroup);
-//   k_sel_finish  grid (rows): selects the `need` largest candidates by
-//                 (key desc, index asc), i.e. by the 64-bit composite
-//                 (key << 32) | ~index, with an 8-bit radix select that stops
-//                 at the first digit whose keys are all taken, sets their
-//                 bits (in an LDS copy of the row's bitmap, rows up to 512K
-//                 tokens), then emits the bitmap's tokens in ascending
-//                 order, the window, and -1 padding.
+//   k_sel_finish  grid (rows), 1024 threads: selects the `need` largest
+//                 candidates by (key desc, index asc), i.e. by the 64-bit
+//                 composite (key << 32) | ~index, with an 11-bit radix
+//                 select over the bits b* leaves open that stops at the
+//                 first digit whose keys are all taken, sets their bits (in
+//                 an LDS copy of the row's bitmap, rows up to 512K tokens),
+//                 then emits the bitmap's tokens in ascending order, the
+//                 window, and -1 padding.
 // state: [3] candidates collected (starts at zero).
 constexpr int SELB = 1024;              // threads per selection workgroup
 constexpr int SEL_PER = 16;             // tokens per thread
@@ -1139,25 +1142,38 @@ constexpr size_t SEL_BM_LDS_MAX = 65536; // largest row bitmap kept in LDS (5242
 constexpr int SEL_FUSED_TOKENS = SEL_PER * SELB;
 static_assert(NBINS == SELB, "one histogram bin per thread");
 
+constexpr int RDX_BITS = 11;             // digit width of the candidates' radix select
+constexpr int RDX_BINS = 1 << RDX_BITS;  // two histogram bins per thread
+static_assert(RDX_BINS == 2 * SELB, "two radix bins per thread");
+
+// A workgroup's LDS list of threshold-bin tokens (n counts every claimed
+// slot, also those past the capacity, which went to global slots).
+template <int CAP>
+struct CandList {
+  uint32_t key[CAP];
+  int32_t idx[CAP];
+  int n;
+};
+
 struct SelShared {
   union {
-    struct {
-      uint32_t key[SEL_LDS_CAND];
-      int32_t idx[SEL_LDS_CAND];
-    } cand;
+    CandList<SEL_LDS_CAND> cand;
     uint64_t comp[RESOLVE_LDS_CAP];
   } u;
-  uint32_t h[256];
+  uint32_t h[RDX_BINS];
+  uint64_t small[64];  // the threshold's digit bucket, when it is this small
+  uint64_t thresh;
   int lds16[16];
-  int wsum[4];
-  int n, base, digit, rem, all, th[2];
+  int base, digit, rem, all, bucket, nsmall, th[2];
 };
 
 struct Threshold {
   int mode, bstar, need;  // mode 0: nothing to select, 1: every candidate, 2: threshold bin
 };
 
-__device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh) {
+// cnt: this thread's bin NBINS - 1 - threadIdx.x of the row's histogram
+// (bins from the top), loaded by the caller.
+__device__ inline Threshold find_threshold(int cnt, const RowInfo& ri, SelShared& sh) {
   Threshold th{0, -1, 0};
   if (ri.keff == 0) return th;
   if (ri.keff == ri.N) {
@@ -1169,7 +1185,6 @@ __device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const 
     sh.th[0] = 0;
     sh.th[1] = 0;
   }
-  const int cnt = (int)a.hist[row * NBINS + NBINS - 1 - tid];  // bins from the top
   int total;
   const int above = block_scan_1024(cnt, sh.lds16, total);
   if (above < ri.keff && above + cnt >= ri.keff) {
@@ -1182,12 +1197,50 @@ __device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const 
   th.need = sh.th[1];
   return th;
 }
+__device__ inline Threshold find_threshold(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh) {
+  return find_threshold((int)a.hist[row * NBINS + NBINS - 1 - threadIdx.x], ri, sh);
+}
+
+// The digit tests of a row on the raw score bits x (a signed integer), for
+// mode 2 (threshold bin b*): score_digit(x) > b*  <=>  x > above_gt and
+// score_digit(x) >= b*  <=>  x >= cand_ge.  score_digit floors x by
+// 2^DIGIT_SHIFT and clamps the result to [DIGIT_BASE, DIGIT_BASE + NBINS - 1],
+// so for 1 <= d <= NBINS - 1 the digit is at least d exactly when
+// x >= (d + DIGIT_BASE) << DIGIT_SHIFT; every digit is at least 0 (cand_ge
+// the smallest int) and none exceeds NBINS - 1 (above_gt the largest).
+struct DigitBounds {
+  int above_gt, cand_ge, mode;
+};
+__device__ inline DigitBounds digit_bounds(const Threshold& th) {
+  DigitBounds d{0x7FFFFFFF, 0x7FFFFFFF, th.mode};
+  if (th.mode == 2) {
+    if (th.bstar < NBINS - 1) d.above_gt = ((th.bstar + 1 + DIGIT_BASE) << DIGIT_SHIFT) - 1;
+    d.cand_ge = th.bstar > 0 ? (th.bstar + DIGIT_BASE) << DIGIT_SHIFT : (int)0x80000000;
+  }
+  return d;
+}
+
+// Where the radix select over a row's candidates starts.  With
+// 1 <= b* <= NBINS - 2 every candidate is a normal float whose key is its
+// bits, with the top 32 - DIGIT_SHIFT bits equal to b* + DIGIT_BASE: the
+// composites (key << 32) | ~index agree above bit 32 + DIGIT_SHIFT.
+struct RadixStart {
+  uint64_t prefix, pmask;
+  int hi;  // composite bits [0, hi) are still open
+};
+__device__ inline RadixStart radix_start(int bstar) {
+  if (bstar >= 1 && bstar <= NBINS - 2)
+    return {(uint64_t)(bstar + DIGIT_BASE) << (32 + DIGIT_SHIFT), ~0ull << (32 + DIGIT_SHIFT), 32 + DIGIT_SHIFT};
+  return {0ull, 0ull, 64};
+}
 
 // The need largest of the m candidates get their bitmap bits (in the row's
-// LDS copy sbm when given, else in the global bitmap).
-__device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, SelShared& sh,
-                                   uint64_t* sbm, bool comp_ready = false) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+// LDS copy sbm when given, else in the global bitmap).  Radix select on the
+// open composite bits, RDX_BITS at a time from the top; it stops at the
+// first digit whose candidates are all taken.
+__device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int m, const RadixStart& rs,
+                                   SelShared& sh, uint64_t* sbm, bool comp_ready = false) {
+  const int tid = threadIdx.x;
   const uint32_t* ck = a.cand_key + row * a.cand_cap;
   const int32_t* ci = a.cand_idx + row * a.cand_cap;
   uint32_t* bm32 = (uint32_t*)(a.bitmap + row * a.bitmap_words);
@@ -1200,48 +1253,67 @@ __device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int 
     for (int i = tid; i < m; i += SELB) sh.u.comp[i] = ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]);
   uint64_t thresh = 0;  // composite of the need-th largest (0: take every candidate)
   if (need < m) {
-    uint64_t prefix = 0, pmask = 0;
+    uint64_t prefix = rs.prefix, pmask = rs.pmask;
     int rem = need;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      if (tid < 256) sh.h[tid] = 0;
+    if (tid == 0) sh.nsmall = 0;  // (ordered before its use by the pass's barriers)
+    for (int hi = rs.hi; hi > 0;) {
+      const int width = hi < RDX_BITS ? hi : RDX_BITS;
+      const int shift = hi - width;
+      const uint32_t dmask = (1u << width) - 1u;
+      sh.h[2 * tid] = 0;
+      sh.h[2 * tid + 1] = 0;
       __syncthreads();
       for (int i = tid; i < m; i += SELB) {
         const uint64_t cv = composite(i);
-        if ((cv & pmask) == prefix) atomicAdd(&sh.h[(cv >> shift) & 255], 1u);
+        if ((cv & pmask) == prefix) atomicAdd(&sh.h[(uint32_t)(cv >> shift) & dmask], 1u);
       }
       __syncthreads();
-      // suffix sums from the top digit: thread t < 256 holds digit 255 - t
-      int x = 0, hv = 0;
-      if (tid < 256) {
-        hv = (int)sh.h[255 - tid];
-        x = hv;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(x, o);
-          if (lane >= o) x += y;
-        }
-        if (lane == 63) sh.wsum[w] = x;
-      }
-      __syncthreads();
-      if (tid < 256) {
-        int incl = x;
-        for (int i = 0; i < w; ++i) incl += sh.wsum[i];
-        const int excl = incl - hv;  // keys with a larger digit
-        if (excl < rem && incl >= rem) {
-          sh.digit = 255 - tid;
-          sh.rem = rem - excl;
-          sh.all = hv == rem - excl;  // the whole digit is taken
-        }
+      // thread t holds digits RDX_BINS - 1 - 2t and RDX_BINS - 2 - 2t (from the top)
+      const int d1 = RDX_BINS - 1 - 2 * tid;
+      const int h1 = (int)sh.h[d1], h0 = (int)sh.h[d1 - 1];
+      int total;
+      const int excl = block_scan_1024(h1 + h0, sh.lds16, total);  // keys with a larger digit
+      if (excl < rem && excl + h1 >= rem) {
+        sh.digit = d1;
+        sh.rem = rem - excl;
+        sh.bucket = h1;
+        sh.all = h1 == rem - excl;  // the whole digit is taken
+      } else if (excl + h1 < rem && excl + h1 + h0 >= rem) {
+        sh.digit = d1 - 1;
+        sh.rem = rem - excl - h1;
+        sh.bucket = h0;
+        sh.all = h0 == rem - excl - h1;
       }
       __syncthreads();
       prefix |= (uint64_t)sh.digit << shift;
-      pmask |= (uint64_t)255 << shift;
+      pmask |= (uint64_t)dmask << shift;
       rem = sh.rem;
       const bool done = sh.all;
+      const int bucket = sh.bucket;
       __syncthreads();
       // every candidate under the prefix is taken: prefix with zero low bits
       // is the threshold (all larger composites are taken too)
       if (done) break;
+      hi = shift;
+      if (bucket <= 64 && in_lds) {
+        // a small bucket: its rem-th largest composite (the one with exactly
+        // rem - 1 larger in the bucket; composites are distinct) is the
+        // threshold, ranked by one wave instead of further passes
+        for (int i = tid; i < m; i += SELB) {
+          const uint64_t cv = sh.u.comp[i];
+          if ((cv & pmask) == prefix) sh.small[atomicAdd(&sh.nsmall, 1)] = cv;
+        }
+        __syncthreads();
+        if (tid < bucket) {
+          const uint64_t c = sh.small[tid];
+          int larger = 0;
+          for (int j = 0; j < bucket; ++j) larger += sh.small[j] > c;
+          if (larger == rem - 1) sh.thresh = c;
+        }
+        __syncthreads();
+        prefix = sh.thresh;
+        break;
+      }
     }
     thresh = prefix;
   } else {
@@ -1259,30 +1331,40 @@ __device__ inline void resolve_row(const SelArgs& a, int64_t row, int need, int 
   }
 }
 
-// Ascending emission into the row's index slots, from the row's LDS copy of
-// the bitmap when given; else the global words are read with agent-scope
-// atomic loads: this workgroup has just set bits in them with device atomics
-// (ordered before these loads by the block barrier).
+// Ascending emission into the row's index slots, two bitmap words per thread
+// and block scan, from the row's LDS copy of the bitmap when given; else the
+// global words are read with agent-scope atomic loads: this workgroup has
+// just set bits in them with device atomics (ordered before these loads by
+// the block barrier).
 __device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri, SelShared& sh,
                                 const uint64_t* sbm) {
   int32_t* out = a.idx + row * a.S;
   uint64_t* bm = a.bitmap + row * a.bitmap_words;
   const int tid = threadIdx.x;
   const int nwords = (ri.N + 63) >> 6;
-  int base = 0;
-  for (int w0 = 0; w0 < nwords; w0 += SELB) {
-    const int w = w0 + tid;
-    uint64_t bits = w >= nwords ? 0ull
-                    : sbm       ? sbm[w]
-                                : __hip_atomic_load(&bm[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  auto word = [&](int w) -> uint64_t {
+    if (w >= nwords) return 0ull;
+    uint64_t bits = sbm ? sbm[w] : __hip_atomic_load(&bm[w], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (w == nwords - 1 && (ri.N & 63)) bits &= (1ull << (ri.N & 63)) - 1ull;  // tail bits are not maintained
+    return bits;
+  };
+  int base = 0;
+  for (int w0 = 0; w0 < nwords; w0 += 2 * SELB) {
+    const int w = w0 + 2 * tid;
+    uint64_t b0 = word(w), b1 = word(w + 1);
     int total;
-    int off = block_scan_1024(__popcll(bits), sh.lds16, total);
-    while (bits) {
-      const int bit = __ffsll((long long)bits) - 1;
-      bits &= bits - 1;
-      const int p = base + off++;
+    int p = base + block_scan_1024(__popcll(b0) + __popcll(b1), sh.lds16, total);
+    while (b0) {
+      const int bit = __ffsll((long long)b0) - 1;
+      b0 &= b0 - 1;
       if (p < a.S) out[p] = 64 * w + bit;
+      ++p;
+    }
+    while (b1) {
+      const int bit = __ffsll((long long)b1) - 1;
+      b1 &= b1 - 1;
+      if (p < a.S) out[p] = 64 * (w + 1) + bit;
+      ++p;
     }
     base += total;
   }
@@ -1293,88 +1375,192 @@ __device__ inline void emit_row(const SelArgs& a, int64_t row, const RowInfo& ri
   for (int j = base + nw + tid; j < a.S; j += SELB) out[j] = -1;
 }
 
-// One chunk of a row's candidates [t0, t1) (the thread's SEL_PER scores in
-// v, token t0 + SELB j + threadIdx.x): sets the bitmap words of the tokens
-// above b* (bm: global or LDS) and appends the tokens of b* to the LDS list
-// (sh.n; past its capacity to global slots reserved in state[3]).
-__device__ inline void filter_chunk(const SelArgs& a, int64_t row, const Threshold& th, int t0, int t1,
-                                    const float (&v)[SEL_PER], SelShared& sh, int* st, uint64_t* bm) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // per mode: tokens with digit > sel_above are taken, those equal to
-  // cand_digit are candidates (mode 0: none; 1: every valid token)
-  const int sel_above = th.mode == 2 ? th.bstar : (th.mode == 1 ? -1 : NBINS);
-  const int cand_digit = th.mode == 2 ? th.bstar : -2;
+// Raw score bits of the wave's NW words from token wt0 (row scores P,
+// tokens below t1 read): v[j] holds token wt0 + 64 j + lane.
+template <int NW>
+__device__ inline void load_wave(const float* P, int wt0, int t1, int (&v)[NW]) {
+  const int lane = threadIdx.x & 63;
+  const int* src = (const int*)P + wt0;
+  const int n = t1 - wt0;  // tokens from src on that may be read
+  if (n >= 64 * NW) {
 #pragma unroll
-  for (int j = 0; j < SEL_PER; ++j) {
-    const int tb = t0 + SELB * j + 64 * wave;  // this wave's 64 tokens: one bitmap word
-    if (tb >= t1) break;  // uniform across the wave
-    const int t = tb + lane;
-    const bool valid = t < t1;
-    const uint32_t key = score_key(v[j]);
-    const int d = score_digit(v[j]);
-    const uint64_t sm = __ballot(valid && d > sel_above);
-    if (lane == 0) bm[tb >> 6] = sm;
-    const uint64_t cm = __ballot(valid && d == cand_digit);
-    if (cm) {  // wave-uniform: lane 0 claims the wave's slots
-      // LDS slots [off, off + cnt) are claimed; those at or past the LDS
-      // capacity go to global slots reserved here (LDS slots below the
-      // capacity are then all written exactly once)
-      const int cnt = __popcll(cm);
-      int off = 0;
-      if (lane == 0) off = atomicAdd(&sh.n, cnt);
-      off = __builtin_amdgcn_readfirstlane(off);
-      const int excess = off + cnt - max(off, SEL_LDS_CAND);
-      int gbase = 0;
-      if (excess > 0) {
-        if (lane == 0) gbase = atomicAdd(&st[3], excess);
-        gbase = __builtin_amdgcn_readfirstlane(gbase);
-      }
+    for (int j = 0; j < NW; ++j) v[j] = src[64 * j + lane];
+  } else {
+#pragma unroll
+    for (int j = 0; j < NW; ++j) v[j] = 64 * j + lane < n ? src[64 * j + lane] : 0;
+  }
+}
+
+// Filters one wave's NW bitmap words from token wt0 (v from load_wave).  A word's taken bits are one compare's ballot and its
+// threshold-bin tokens another's; both masks are parked in lane j of two
+// register pairs, the taken words stored by lanes 0 .. NW - 1 together
+// (bm: global or LDS).  The threshold-bin tokens then get consecutive slots:
+// in the workgroup's LDS list cl when CAP > 0 (past its capacity, and always
+// when CAP == 0, in global slots reserved in state[3]).  FAST: mode 2 and
+// every token of the NW words valid (no validity masks).
+template <bool FAST, int CAP, int NW>
+__device__ inline void filter_wave(const SelArgs& a, int64_t row, const DigitBounds& db, int wt0, int t1,
+                                   const int (&v)[NW], CandList<CAP>* cl, int* st, uint64_t* bm) {
+  static_assert(NW <= 64, "one word per lane");
+  const int lane = threadIdx.x & 63;
+  int wlo = 0, whi = 0, clo = 0, chi = 0;
+  int count = 0;  // threshold-bin tokens of the wave
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {
+    uint64_t sm, cm;
+    if constexpr (FAST) {
+      sm = __ballot(v[j] > db.above_gt);
+      cm = __ballot(v[j] >= db.cand_ge) & ~sm;
+    } else {
+      const int tb = wt0 + 64 * j;
+      if (tb >= t1) break;  // uniform across the wave
+      const uint64_t vm = t1 - tb >= 64 ? ~0ull : (1ull << (t1 - tb)) - 1ull;
+      sm = db.mode == 1 ? vm : (db.mode == 2 ? __ballot(v[j] > db.above_gt) & vm : 0ull);
+      cm = db.mode == 2 ? __ballot(v[j] >= db.cand_ge) & vm & ~sm : 0ull;
+    }
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(wlo) : "s"((uint32_t)sm), "i"(j));
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(whi) : "s"((uint32_t)(sm >> 32)), "i"(j));
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(clo) : "s"((uint32_t)cm), "i"(j));
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(chi) : "s"((uint32_t)(cm >> 32)), "i"(j));
+    count += __popcll(cm);
+  }
+  const int nw = FAST ? NW : min(NW, max(0, (t1 - wt0 + 63) >> 6));
+  if (lane < nw) bm[(wt0 >> 6) + lane] = ((uint64_t)(uint32_t)whi << 32) | (uint32_t)wlo;
+  if (count == 0) return;  // uniform
+  // slots [off, off + count): below CAP in LDS, the rest in global slots
+  // reserved here from gbase on
+  int off = 0, gbase = 0;
+  if constexpr (CAP > 0) {
+    if (lane == 0) off = atomicAdd(&cl->n, count);
+    off = __builtin_amdgcn_readfirstlane(off);
+  }
+  const int excess = off + count - max(off, CAP);
+  if (excess > 0) {
+    if (lane == 0) gbase = atomicAdd(&st[3], excess);
+    gbase = __builtin_amdgcn_readfirstlane(gbase);
+  }
+  uint32_t* ck = a.cand_key + row * a.cand_cap;
+  int32_t* ci = a.cand_idx + row * a.cand_cap;
+  int run = off;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {
+    const uint64_t cm = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(chi, j) << 32) |
+                        (uint32_t)__builtin_amdgcn_readlane(clo, j);
+    if (cm) {  // uniform
       if ((cm >> lane) & 1ull) {
-        const int slot = off + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+        const int slot = run + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
-        if (slot < SEL_LDS_CAND) {
-          sh.u.cand.key[slot] = key;
-          sh.u.cand.idx[slot] = t;
+        const uint32_t key = score_key(__int_as_float(v[j]));
+        const int t = wt0 + 64 * j + lane;
+        if (CAP > 0 && slot < CAP) {
+          cl->key[slot] = key;
+          cl->idx[slot] = t;
         } else {
-          const int64_t gs = row * a.cand_cap + gbase + (slot - max(off, SEL_LDS_CAND));
-          a.cand_key[gs] = key;
-          a.cand_idx[gs] = t;
+          const int gs = gbase + slot - max(off, CAP);
+          ck[gs] = key;
+          ci[gs] = t;
         }
       }
+      run += __popcll(cm);
     }
   }
 }
 
-__global__ __launch_bounds__(SELB) void k_sel_filter(SelArgs a) {
-  __shared__ SelShared sh;
-  const int64_t row = blockIdx.y;
-  const RowInfo ri = row_info(a, row);
-  const int t0 = blockIdx.x * SEL_TOKENS;
-  if (t0 >= ri.N) return;
-  const int t1 = min(ri.N, t0 + SEL_TOKENS);
-  const float* P = a.scores + row * a.score_stride;
-  uint64_t* bm = a.bitmap + row * a.bitmap_words;
-  int* st = a.state + row * 8;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  float v[SEL_PER];
+// The threshold of a row by one wave (the filter's workgroups are small):
+// lane l holds bins NBINS - 16 - 16 l .. NBINS - 1 - 16 l (load_hist16, issued
+// with the score loads); a wave scan gives the keys above each lane's bins,
+// and the lane whose bins reach k_eff walks them from the top.  Same result
+// as find_threshold.
+__device__ inline void load_hist16(const SelArgs& a, int64_t row, uint32_t (&c)[16]) {
+  const int lane = threadIdx.x & 63;
+  const uint4* h4 = (const uint4*)(a.hist + row * NBINS + NBINS - 16 - 16 * lane);  // ascending
 #pragma unroll
-  for (int j = 0; j < SEL_PER; ++j) {
-    const int t = t0 + SELB * j + tid;
-    v[j] = t < t1 ? P[t] : 0.f;
+  for (int q = 0; q < 4; ++q) {
+    const uint4 x = h4[q];
+    c[4 * q] = x.x;
+    c[4 * q + 1] = x.y;
+    c[4 * q + 2] = x.z;
+    c[4 * q + 3] = x.w;
   }
-  if (tid == 0) sh.n = 0;
-  const Threshold th = find_threshold(a, row, ri, sh);
-  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
-  filter_chunk(a, row, th, t0, t1, v, sh, st, bm);
+}
+__device__ inline void threshold_by_wave(const uint32_t (&c)[16], int keff, int* th2) {
+  const int lane = threadIdx.x & 63;
+  int sum = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) sum += (int)c[i];
+  int incl = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  int above = incl - sum;
+  if (lane == 0) {  // defaults if the histogram held fewer than k_eff keys (it cannot)
+    th2[0] = 0;
+    th2[1] = 0;
+  }
+  if (above < keff && incl >= keff) {  // one lane: the crossing is in its bins
+#pragma unroll
+    for (int i = 15; i >= 0; --i) {
+      if (above + (int)c[i] >= keff) {
+        th2[0] = NBINS - 16 - 16 * lane + i;
+        th2[1] = keff - above;
+        break;
+      }
+      above += (int)c[i];
+    }
+  }
+}
+
+constexpr int SELF = 256;                          // threads per filter workgroup
+constexpr int SELF_WORDS = 32;                     // bitmap words per filter wave
+constexpr int SELF_TOKENS = SELF * SELF_WORDS;     // tokens per filter workgroup
+constexpr int SELF_LDS_CAND = 2048;                // candidates a filter workgroup gathers in LDS
+
+// grid (chunks of SELF_TOKENS tokens, rows), SELF threads: small workgroups
+// (up to eight per CU) whose score, histogram and length loads all leave
+// before the first wait (the scores up to the row's max_len, which the row
+// always holds); the threshold-bin tokens are gathered in LDS and leave in
+// one coalesced copy per workgroup (scattered one-lane global stores cost
+// as much as the rest of the filter where the bin is dense).
+__global__ __launch_bounds__(SELF) void k_sel_filter(SelArgs a) {
+  __shared__ CandList<SELF_LDS_CAND> cl;
+  __shared__ int th2[2], base;
+  const int64_t row = blockIdx.y;
+  const int t0 = blockIdx.x * SELF_TOKENS;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wt0 = t0 + 64 * SELF_WORDS * wave;
+  int v[SELF_WORDS];
+  load_wave(a.scores + row * a.score_stride, wt0, a.max_len, v);
+  uint32_t c[16];
+  if (wave == 0) load_hist16(a, row, c);
+  const RowInfo ri = row_info(a, row);
+  if (t0 >= ri.N) return;  // uniform across the workgroup
+  const int t1 = min(ri.N, t0 + SELF_TOKENS);
+  const int tid = threadIdx.x;
+  if (tid == 0) cl.n = 0;
+  Threshold th{ri.keff == ri.N ? 1 : 0, -1, 0};
+  if (ri.keff > 0 && ri.keff < ri.N && wave == 0) threshold_by_wave(c, ri.keff, th2);
+  __syncthreads();  // the list initialised, th2 written
+  if (ri.keff > 0 && ri.keff < ri.N) th = Threshold{2, th2[0], th2[1]};
+  int* st = a.state + row * 8;
+  if (wt0 < t1) {  // uniform across the wave
+    const DigitBounds db = digit_bounds(th);
+    uint64_t* bm = a.bitmap + row * a.bitmap_words;
+    if (db.mode == 2 && wt0 + 64 * SELF_WORDS <= t1)
+      filter_wave<true>(a, row, db, wt0, t1, v, &cl, st, bm);
+    else
+      filter_wave<false>(a, row, db, wt0, t1, v, &cl, st, bm);
+  }
   __syncthreads();
-  const int n = min(sh.n, SEL_LDS_CAND);
+  const int n = min(cl.n, SELF_LDS_CAND);
   if (n > 0) {
-    if (tid == 0) sh.base = atomicAdd(&st[3], n);
+    if (tid == 0) base = atomicAdd(&st[3], n);
     __syncthreads();
-    const int64_t dst = row * a.cand_cap + sh.base;
-    for (int i = tid; i < n; i += SELB) {
-      a.cand_key[dst + i] = sh.u.cand.key[i];
-      a.cand_idx[dst + i] = sh.u.cand.idx[i];
+    const int64_t dst = row * a.cand_cap + base;
+    for (int i = tid; i < n; i += SELF) {
+      a.cand_key[dst + i] = cl.key[i];
+      a.cand_idx[dst + i] = cl.idx[i];
     }
   }
 }
@@ -1387,16 +1573,39 @@ __global__ __launch_bounds__(SELB) void k_sel_finish(SelArgs a) {
   __shared__ SelShared sh;
   extern __shared__ __align__(16) uint64_t sbm[];
   const int64_t row = blockIdx.x;
-  const RowInfo ri = row_info(a, row);
+  const int tid = threadIdx.x;
+  // every independent load first: count, histogram bin, bitmap, length
   const int m = min(a.state[row * 8 + 3], (int)a.cand_cap);
+  const int cnt = (int)a.hist[row * NBINS + NBINS - 1 - tid];
+  const RowInfo ri = row_info(a, row);
   if constexpr (BM_LDS) {
     const uint64_t* bm = a.bitmap + row * a.bitmap_words;
     const int nwords = (ri.N + 63) >> 6;
-    for (int w = threadIdx.x; w < nwords; w += SELB) sbm[w] = bm[w];
+    for (int w = tid; w < nwords; w += SELB) sbm[w] = bm[w];
   }
-  const Threshold th = find_threshold(a, row, ri, sh);
-  __syncthreads();  // the LDS bitmap complete (find_threshold may return before its barriers)
-  if (th.mode == 2) resolve_row(a, row, th.need, m, sh, BM_LDS ? sbm : nullptr);
+  // the candidates' composites (when they fit in LDS), loaded before the
+  // threshold's scan so that the loads overlap its barriers
+  constexpr int CR = RESOLVE_LDS_CAP / SELB;
+  static_assert(CR * SELB == RESOLVE_LDS_CAP, "whole rounds of candidates");
+  const bool comp_lds = m <= RESOLVE_LDS_CAP;
+  uint64_t cv[CR];
+  if (comp_lds) {
+    const uint32_t* ck = a.cand_key + row * a.cand_cap;
+    const int32_t* ci = a.cand_idx + row * a.cand_cap;
+#pragma unroll
+    for (int r = 0; r < CR; ++r) {
+      const int i = tid + SELB * r;
+      cv[r] = i < m ? ((uint64_t)ck[i] << 32) | (uint32_t)(~ci[i]) : 0ull;
+    }
+  }
+  const Threshold th = find_threshold(cnt, ri, sh);
+  if (comp_lds) {
+#pragma unroll
+    for (int r = 0; r < CR; ++r)
+      if (tid + SELB * r < m) sh.u.comp[tid + SELB * r] = cv[r];
+  }
+  __syncthreads();  // LDS bitmap and composites complete (find_threshold may return before its barriers)
+  if (th.mode == 2) resolve_row(a, row, th.need, m, radix_start(th.bstar), sh, BM_LDS ? sbm : nullptr, comp_lds);
   __syncthreads();
   emit_row(a, row, ri, sh, BM_LDS ? sbm : nullptr);
 }
@@ -1413,21 +1622,22 @@ __global__ __launch_bounds__(SELB) void k_sel_fused(SelArgs a) {
   const float* P = a.scores + row * a.score_stride;
   int* st = a.state + row * 8;
   const int tid = threadIdx.x;
-  if (tid == 0) sh.n = 0;
+  if (tid == 0) sh.u.cand.n = 0;
   const Threshold th = find_threshold(a, row, ri, sh);
-  __syncthreads();  // sh.n initialised (find_threshold may return before its barriers)
+  const DigitBounds db = digit_bounds(th);
+  __syncthreads();  // the list initialised (find_threshold may return before its barriers)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   for (int t0 = 0; t0 < ri.N; t0 += SEL_TOKENS) {
     const int t1 = min(ri.N, t0 + SEL_TOKENS);
-    float v[SEL_PER];
-#pragma unroll
-    for (int j = 0; j < SEL_PER; ++j) {
-      const int t = t0 + SELB * j + tid;
-      v[j] = t < t1 ? P[t] : 0.f;
+    const int wt0 = t0 + 64 * SEL_PER * wave;
+    if (wt0 < t1) {  // uniform across the wave
+      int v[SEL_PER];
+      load_wave(P, wt0, t1, v);
+      filter_wave<false, SEL_LDS_CAND>(a, row, db, wt0, t1, v, &sh.u.cand, st, sbm);
     }
-    filter_chunk(a, row, th, t0, t1, v, sh, st, sbm);
   }
   __syncthreads();
-  const int n = sh.n;
+  const int n = sh.u.cand.n;
   if (th.mode == 2 && n > 0) {
     if (n <= SEL_LDS_CAND) {  // every candidate in LDS: composites in place, through registers
       uint64_t cv[SEL_LDS_CAND / SELB];
@@ -1441,7 +1651,7 @@ __global__ __launch_bounds__(SELB) void k_sel_fused(SelArgs a) {
       for (int r = 0; r < SEL_LDS_CAND / SELB; ++r)
         if (tid + SELB * r < n) sh.u.comp[tid + SELB * r] = cv[r];
       __syncthreads();
-      resolve_row(a, row, th.need, n, sh, sbm, true);
+      resolve_row(a, row, th.need, n, radix_start(th.bstar), sh, sbm, true);
     } else {  // the LDS part joins the overflow in global memory
       if (tid == 0) sh.base = atomicAdd(&st[3], SEL_LDS_CAND);
       __syncthreads();
@@ -1452,7 +1662,7 @@ __global__ __launch_bounds__(SELB) void k_sel_fused(SelArgs a) {
       }
       __threadfence_block();
       __syncthreads();
-      resolve_row(a, row, th.need, min(n, (int)a.cand_cap), sh, sbm);
+      resolve_row(a, row, th.need, min(n, (int)a.cand_cap), radix_start(th.bstar), sh, sbm);
     }
   }
   __syncthreads();
@@ -2140,8 +2350,8 @@ hipError_t launch_select(const SelArgs& a, hipStream_t s) {
     HS2_LAUNCH(k_sel_fused, dim3((unsigned)a.rows), dim3(SELB), (size_t)a.bitmap_words * sizeof(uint64_t), s, a);
     return hipGetLastError();
   }
-  const int64_t chunks = ((int64_t)a.max_len + SEL_TOKENS - 1) / SEL_TOKENS;
-  HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELB), 0, s, a);
+  const int64_t chunks = ((int64_t)a.max_len + SELF_TOKENS - 1) / SELF_TOKENS;
+  HS2_LAUNCH(k_sel_filter, dim3((unsigned)chunks, (unsigned)a.rows), dim3(SELF), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t bm_bytes = (size_t)a.bitmap_words * sizeof(uint64_t);

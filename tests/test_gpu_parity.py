@@ -301,7 +301,21 @@ SEL = [
     ("lognormal_long", 1, 2, 1, 200000, 4096, 256, "lognormal"),
     ("k_equals_N", 1, 1, 1, 1000, 990, 10, "uniform"),
     ("k_zero", 1, 1, 2, 1000, 0, 10, "uniform"),
+    # scores on both sides of first-level bin edges (and -0.0): the filter
+    # tests raw bits against per-row bounds; two-kernel and one-workgroup rows
+    ("bin_edges", 2, 2, 2, 40000, 3000, 32, "edges"),
+    ("bin_edges_one_chunk", 1, 2, 1, 12000, 800, 16, "edges"),
+    # threshold in the top clamped bin, and in the bottom bin
+    ("top_clamp_bin", 1, 2, 1, 30000, 300, 16, "top"),
+    ("bottom_bin", 1, 1, 2, 30000, 2000, 16, "bottom"),
 ]
+
+# First-level bin edges of the selection's histogram: bin d >= 1 starts at
+# the float whose bits are (d + 1120) << 19 (an 8-exponent-bit, 4-mantissa-bit
+# prefix; bins 0 and 1023 are clamped).
+_EDGE_BITS = [((d + 1120) << 19) + o for d in (1, 2, 300, 917, 1000, 1022, 1023) for o in (-1, 0, 1)]
+_EDGES = np.concatenate([np.array(_EDGE_BITS, dtype=np.uint32).view(np.float32),
+                         np.array([0.0, -0.0, 1e-30, 3e-39], dtype=np.float32)])
 
 
 @pytest.mark.parametrize("name,B,Hkv,C,Lmax,k,win,kind", SEL, ids=[s[0] for s in SEL])
@@ -316,6 +330,13 @@ def test_select_from_scores_exact(name, B, Hkv, C, Lmax, k, win, kind):
         s = np.full(shape, 0.25, dtype=np.float32)
     elif kind == "tiny":
         s = rng.choice(np.array([0.0, 1e-40, 3e-39, 1e-38, 2e-38, 1.0], dtype=np.float32), size=shape)
+    elif kind == "edges":
+        s = rng.choice(_EDGES, size=shape)
+    elif kind == "top":  # most scores at or above 124 (the top clamped bin)
+        s = np.where(rng.random(shape) < 0.3, rng.random(shape), 124.0 + 1e4 * rng.random(shape)).astype(np.float32)
+    elif kind == "bottom":  # most scores below 7e-18 (bin 0), a few above
+        tiny = rng.choice(np.array([0.0, -0.0, 1e-38, 1e-30, 1e-20, 6e-18], dtype=np.float32), size=shape)
+        s = np.where(rng.random(shape) < 0.02, rng.random(shape).astype(np.float32), tiny).astype(np.float32)
     else:
         s = (np.exp(rng.standard_normal(shape)) / Lmax).astype(np.float32)
     lens = np.array([Lmax - 17 * b for b in range(B)], dtype=np.int32)
