@@ -93,7 +93,7 @@ typedef struct hs2_dims {
   int32_t max_len;     /* Lmax: cache capacity per sequence, 1 .. 2^27 tokens     */
   int64_t kv_stride_b; /* elements; multiple of 8                                 */
   int64_t kv_stride_h; /* elements; multiple of 8                                 */
-  int64_t kv_stride_t; /* elements; >= head_dim, multiple of 8                    */
+  int64_t kv_stride_t; /* elements; >= head_dim, multiple of 8, <= 2^24           */
   float scale;         /* softmax scale; <= 0 selects 1/sqrt(head_dim)            */
 } hs2_dims;
 

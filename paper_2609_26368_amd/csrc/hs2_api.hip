@@ -25,6 +25,7 @@ constexpr int kMaxQueries = 16;
 constexpr int kMaxRows = 128;           // C * Gp
 constexpr int kMaxGroup = 64;
 constexpr int64_t kMaxGridRows = 65535;  // largest grid y extent: the (b, g, c) rows
+constexpr int64_t kMaxTokenStride = 1 << 24;  // elements: 64 token rows stay below 2^31 bytes
 constexpr int32_t kMaxLen = 1 << 27;
 constexpr int kNBins = 1024;          // must match the kernels' first-level radix bins
 constexpr int kSelChunk = hs2::SEL_CHUNK;  // tokens per workgroup of the selection scans
@@ -111,6 +112,10 @@ hs2_status check_dims(const hs2_dims* d) {
   if (d->kv_stride_t < d->head_dim || d->kv_stride_t % 8 || d->kv_stride_h < 0 || d->kv_stride_h % 8 ||
       d->kv_stride_b < 0 || d->kv_stride_b % 8)
     return fail(HS2_ERR_ALIGN, "KV strides must be non-negative multiples of 8 elements, kv_stride_t >= head_dim");
+  // the streaming kernels address a tile of up to 64 token rows by 32-bit offsets
+  if (d->kv_stride_t > kMaxTokenStride)
+    return fail(HS2_ERR_UNSUPPORTED, "kv_stride_t %lld exceeds %lld elements", (long long)d->kv_stride_t,
+                (long long)kMaxTokenStride);
   if (!std::isfinite(d->scale)) return fail(HS2_ERR_SHAPE, "scale must be finite");
   return HS2_OK;
 }

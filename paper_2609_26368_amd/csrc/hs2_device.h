@@ -262,6 +262,23 @@ __device__ inline void dma16_p(const void* src, uint32_t lds_base) {
     dma16(src, lds_base);
 }
 
+// The same load from a wave-uniform base (scalar registers) plus this lane's
+// 32-bit byte offset: no per-lane 64-bit address arithmetic.
+__device__ inline const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+template <bool NTH>
+__device__ inline void dma16_s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  sbase = uniform_ptr(sbase);  // (free where the base is already scalar)
+  if constexpr (NTH)
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt" : : "v"(voff), "s"(sbase), "s"(lds_base) : "memory");
+  else
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "s"(lds_base) : "memory");
+}
+
 __device__ inline uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }

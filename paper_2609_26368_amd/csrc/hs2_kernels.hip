@@ -300,12 +300,18 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int lane = threadIdx.x & 63;
-  const int tg = (threadIdx.x >> 6) / NWV, wave = (threadIdx.x >> 6) % NWV;  // token group, wave in it
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tg = wid / NWV, wave = wid % NWV;  // token group, wave in it
   const LaneLens ll(a.len, a.B, a.max_len);
-  const int S = fa_split_len(ll, a.Hkv, a.sp);
+  const int S = __builtin_amdgcn_readfirstlane(fa_split_len(ll, a.Hkv, a.sp));
   int b, g, split;
   if (!fa_locate(ll, a.Hkv, S, blockIdx.x, b, g, split)) return;
-  const int Lv = clamp_len(a.len, b, a.max_len);
+  // uniform by construction; said so, so that every address derived from
+  // them stays in scalar registers
+  b = __builtin_amdgcn_readfirstlane(b);
+  g = __builtin_amdgcn_readfirstlane(g);
+  split = __builtin_amdgcn_readfirstlane(split);
+  const int Lv = __builtin_amdgcn_readfirstlane(clamp_len(a.len, b, a.max_len));
   // token group tg streams the tg-th contiguous part of the split through its own ring
   const int part = S / TGW;
   const int t_begin = split * S + tg * part;
@@ -345,15 +351,17 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       lrow = a.logits + (((int64_t)b * a.Hkv + g) * a.C * a.G + c * a.G + h) * a.logit_stride;
   }
 
-  // per-lane part of each load's byte offset: a 1 KB load covers RPL rows of
-  // CPR chunks (lane / CPR = row, lane % CPR = chunk slot); bf16 rows are
-  // swizzled, E4M3 rows raw
+  // per-lane part of each load's byte offset from its tile's first row (32
+  // bits: a tile spans TW rows, and the host keeps TW token strides below
+  // 2^31 bytes): a 1 KB load covers RPL rows of CPR chunks (lane / CPR =
+  // row, lane % CPR = chunk slot); bf16 rows are swizzled, E4M3 rows raw.
+  // The tile's first row is a wave-uniform base in scalar registers.
   constexpr int RPL = 1024 / RB;  // rows per 1 KB load
-  auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
-               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ stage_swz(row));
+  auto lane_offset = [&](int row, int dt) -> uint32_t {
+    return (uint32_t)(dt * (int)stride_t) +
+           16u * (uint32_t)((lane % CPR) ^ (KV8 ? raw_swz<RB>(row) : stage_swz(row)));
   };
-  int64_t lane_off[LPM];
+  uint32_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
     const int row = RPL * (wave * LPM + u) + lane / CPR;
@@ -365,17 +373,18 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
     const int t0 = t_begin + tile * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
-    const int64_t tile_off = (int64_t)t0 * stride_t;
+    const unsigned char* kt = Kbg + (int64_t)t0 * stride_t;
+    const unsigned char* vt = Vbg + (int64_t)t0 * stride_t;
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
-      int64_t off = tile_off + lane_off[u];
+      uint32_t off = lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; masked below
         const int row = RPL * n + lane / CPR;
-        off = lane_offset(row, min(t0 + row, t_end - 1));
+        off = lane_offset(row, min(t0 + row, t_end - 1) - t0);
       }
-      dma16_p<decltype(k_nt)::value>(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
-      dma16_p<KP != FA_CACHE_DEFAULT>(Vbg + off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
+      dma16_s<decltype(k_nt)::value>(kt, off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16_s<KP != FA_CACHE_DEFAULT>(vt, off, __builtin_amdgcn_readfirstlane(base + TW * RB + 1024 * n));
     }
   };
   auto issue = [&](int tile) __attribute__((always_inline)) {
@@ -810,8 +819,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
   uint32_t* hist = (uint32_t*)(smem + PS::LDS);       // [C][NBINS/2]
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Lv = clamp_len(a.len, b, a.max_len);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int Lv = __builtin_amdgcn_readfirstlane(clamp_len(a.len, b, a.max_len));
   // candidates of query c: [0, Lv - C + c - W + 1); their union ends at Lv - W
   const int n_cand_max = Lv - a.W;
   const int t_begin = split * a.split_tokens;
@@ -833,11 +842,12 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
   const float c2 = KV8 ? a.c2 * a.k_scale[g] : a.c2;
   const uint32_t ring = lds_addr(smem);
   constexpr int RPL = PS::RPL;  // rows per 1 KB load
-  auto lane_offset = [&](int row, int t) -> int64_t {
-    return KV8 ? (int64_t)t * stride_t + 16 * ((lane % CPR) ^ raw_swz<RB>(row))
-               : (int64_t)t * stride_t + 16 * ((lane % CPR) ^ stage_swz(row));
+  // per-lane offsets from the tile's first row, as in the full-attention ring
+  auto lane_offset = [&](int row, int dt) -> uint32_t {
+    return (uint32_t)(dt * (int)stride_t) +
+           16u * (uint32_t)((lane % CPR) ^ (KV8 ? raw_swz<RB>(row) : stage_swz(row)));
   };
-  int64_t lane_off[LPM];
+  uint32_t lane_off[LPM];
 #pragma unroll
   for (int u = 0; u < LPM; ++u) {
     const int row = RPL * (wave * LPM + u) + lane / CPR;
@@ -852,16 +862,16 @@ __global__ __attribute__((amdgpu_flat_work_group_size(64, 64 * PoolShape<RT, GP,
     const int t0 = t_begin + (ntiles - 1 - tile) * TW;
     const uint32_t base = ring + (uint32_t)((tile % NS) * SB);
     const bool whole = t0 + TW <= t_end;
-    const int64_t tile_off = (int64_t)t0 * stride_t;
+    const unsigned char* kt = Kbg + (int64_t)t0 * stride_t;
 #pragma unroll
     for (int u = 0; u < LPM; ++u) {
       const int n = wave * LPM + u;
-      int64_t off = tile_off + lane_off[u];
+      uint32_t off = lane_off[u];
       if (!whole) {  // rows past the range repeat the last valid row; never emitted
         const int row = RPL * n + lane / CPR;
-        off = lane_offset(row, min(t0 + row, t_end - 1));
+        off = lane_offset(row, min(t0 + row, t_end - 1) - t0);
       }
-      dma16_p<decltype(k_nt)::value>(Kbg + off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
+      dma16_s<decltype(k_nt)::value>(kt, off, __builtin_amdgcn_readfirstlane(base + 1024 * n));
     }
   };
   auto issue = [&](int tile) __attribute__((always_inline)) {  // one scalar branch per tile

@@ -61,6 +61,9 @@ def test_workspace_bytes(lib):
     assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_q_heads=64, n_kv_heads=1), 1024, 128) > 0
     assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=2, n_q_heads=64, n_kv_heads=1), 16, 8) > 0
     assert hs2.hs2_workspace_bytes(dims(head_dim=256, n_queries=4, n_q_heads=64, n_kv_heads=1), 16, 8) == 0
+    # token stride at most 2^24 elements (tiles of 64 rows use 32-bit offsets)
+    assert hs2.hs2_workspace_bytes(dims(kv_strides=(0, 0, 1 << 24)), 8, 8) > 0
+    assert hs2.hs2_workspace_bytes(dims(kv_strides=(0, 0, (1 << 24) + 8)), 8, 8) == 0
     # one grid row per (b, g, c) selection row: at most 65535 of them
     assert hs2.hs2_workspace_bytes(dims(batch=4095, n_queries=4, n_q_heads=16, n_kv_heads=4, max_len=64), 8, 8) > 0
     assert hs2.hs2_workspace_bytes(dims(batch=4096, n_queries=4, n_q_heads=16, n_kv_heads=4, max_len=64), 8, 8) == 0
