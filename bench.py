@@ -291,36 +291,48 @@ def main():
     # flush: evicting by reading 1 GiB (a write would leave dirty lines whose
     # write-back then overlaps the timed step); the read is outside the step's events
     flush = torch.ones(1 << 28, dtype=torch.int32, device=dev) if args.caches == "flush" else None
-    # the timed steps, one event pair around each (mean, percentiles and the
-    # gaps between steps come from the same run)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall = ev_ms = None
+    if flush is None:
+        # the timed steps: back to back between one event pair (no marker
+        # between steps: on this stack an event record costs a few us of GPU
+        # time, which at the 4K decode shape is ~12 % of a step)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev_ms = e0.elapsed_time(e1)
+        ms_per_step = ev_ms / args.steps
+        value = tokens * args.steps / wall
+    # single-step times: a second run of as many steps with an event pair
+    # around each (percentiles, the first step after a synchronisation; with
+    # --caches flush these are the timed steps, the flush reads outside them)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    first_copy = n_step[0]
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    e0.record(stream)
     for a_, b_ in ev:
         if flush is not None:
             flush.amax()
         a_.record(stream)
         run_step()
         b_.record(stream)
-    e1.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     per_step = np.array([a_.elapsed_time(b_) for a_, b_ in ev])
-    ev_ms = e0.elapsed_time(e1)
-    if flush is not None:  # steps timed one by one (the flush reads stay outside)
+    if flush is not None:
         ms_per_step = float(per_step.mean())
         value = tokens / (ms_per_step * 1e-3)
+        log(f"[bench] timed {args.steps} steps one by one (flushed): mean {ms_per_step:.4f} ms")
     else:
-        ms_per_step = ev_ms / args.steps
-        value = tokens * args.steps / wall
-    log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms, "
-        f"sum of per-step events {per_step.sum():.2f} ms")
-    if n_copies > 1:  # step i of the timed run used copy (warmup + i) % n_copies
+        log(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {ev_ms:.2f} ms; "
+            f"single steps (second run) sum to {per_step.sum():.2f} ms")
+    if n_copies > 1:  # step i of the single-step run used copy (first_copy + i) % n_copies
         by_copy = {}
         for i, ms in enumerate(per_step):
-            by_copy.setdefault((args.warmup + i) % n_copies, []).append(ms)
+            by_copy.setdefault((first_copy + i) % n_copies, []).append(ms)
         log("[bench] mean step ms by cache copy: " +
             " ".join(f"{c}:{np.mean(v):.4f}" for c, v in sorted(by_copy.items())[:8]))
     pct = {f"p{q}": round(float(np.percentile(per_step, q)), 4) for q in (10, 50, 90)}
