@@ -1144,7 +1144,7 @@ __device__ inline int block_scan_1024(int v, int* lds16, int& total) {
 constexpr int SELB = 1024;              // threads per selection workgroup
 constexpr int SEL_PER = 16;             // tokens per thread
 constexpr int SEL_TOKENS = SELB * SEL_PER;
-constexpr int SEL_LDS_CAND = 2048;      // candidates a workgroup gathers in LDS
+constexpr int SEL_LDS_CAND = 2048;      // candidates a one-row workgroup (k_sel_fused) gathers in LDS
 constexpr int RESOLVE_LDS_CAP = 6144;   // candidates the resolver keeps in LDS
 constexpr size_t SEL_BM_LDS_MAX = 65536; // largest row bitmap kept in LDS (524288 tokens)
 // longest rows selected by one workgroup (one chunk: with two, the 32K
