@@ -279,7 +279,8 @@ __global__ __launch_bounds__(512) void k_fa_split(FaArgs a) {
 // waves converts each tile's K and V rows once into shared bf16 tiles (one
 // barrier per tile), which its waves read as the bf16 path reads its stage
 // (each wave converting the whole tile itself measured 1.45x slower at 64
-// query rows per KV head).  HDIM: head dim (128 or 256).  KP: cache policy of the stage loads (FaCachePolicy).
+// query rows per KV head).  HDIM: head dim (128 or 256).  KP: cache policy
+// of the stage loads (FaCachePolicy).
 template <int RT, int NWV, int TW, int NS, int TGW, bool KV8, int HDIM, int KP>
 __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   constexpr int RPW = RT / NWV;
@@ -1401,9 +1402,10 @@ __device__ inline void load_wave(const float* P, int wt0, int t1, int (&v)[NW]) 
   }
 }
 
-// Filters one wave's NW bitmap words from token wt0 (v from load_wave).  A word's taken bits are one compare's ballot and its
-// threshold-bin tokens another's; both masks are parked in lane j of two
-// register pairs, the taken words stored by lanes 0 .. NW - 1 together
+// Filters one wave's NW bitmap words from token wt0 (v from load_wave).  A
+// word's taken bits are one compare's ballot and its threshold-bin tokens
+// another's; both masks are parked in lane j of two register pairs, the
+// taken words stored by lanes 0 .. NW - 1 together
 // (bm: global or LDS).  The threshold-bin tokens then get consecutive slots:
 // in the workgroup's LDS list cl when CAP > 0 (past its capacity, and always
 // when CAP == 0, in global slots reserved in state[3]).  FAST: mode 2 and
