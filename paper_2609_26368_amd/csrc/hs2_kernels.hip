@@ -319,6 +319,10 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
   const int t_end = min(Lv, t_begin + part);
   const int ntiles = t_end > t_begin ? (t_end - t_begin + TW - 1) / TW : 0;
   const int nloop = (min(Lv, split * S + part) - split * S + TW - 1) / TW;  // group 0's
+  // a located item's split starts below the length, so group 0 has a tile:
+  // without a zero-trip path the accumulators leave the loop in their own
+  // registers (with it the compiler copied all of O at every tile)
+  __builtin_assume(nloop >= 1);
   // FA_STREAM_K_HEAD: K rows of the group before this offset are non-temporal
   const int k_stream = part - (int)((int64_t)part * a.k_keep_pct / 100);
   const int rt0 = wave * RPW;
@@ -404,18 +408,17 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
     if (i < ntiles) issue(i);
-  // every wave runs group 0's tile count (the barrier count must match); a
-  // group past its own tiles only takes part in the barrier
-  for (int i = 0; i < nloop; ++i) {
+  // every wave runs group 0's tile count of barrier rounds (the counts must
+  // match): its own tiles here, then barrier-only rounds for the rest (a
+  // loop of its own, so that the tile loop has no path that leaves the
+  // accumulators untouched: with one, the compiler copied all of O into a
+  // second register set at every tile)
+  for (int i = 0; i < ntiles; ++i) {
     // logits stores also count in vmcnt; they only make this wait longer
-    if (i < ntiles) wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
+    wait_ring<2 * LPM>(min(NS - 2, ntiles - 1 - i));
     if (NWV * TGW > 1) __syncthreads();
-    if (i < ntiles && i + NS - 1 < ntiles) issue(i + NS - 1);
+    if (i + NS - 1 < ntiles) issue(i + NS - 1);
     const unsigned char* stg = ring_p + (i % NS) * SB;
-    if (i >= ntiles) {
-      if (KCONV) __syncthreads();  // the other groups' K-tile barrier
-      continue;
-    }
     if constexpr (KCONV) {
       convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg, tile_k, 64 * wave + lane);
       convert_rows_e4m3<TW, 64 * NWV, HDIM>(stg + TW * RB, tile_v, 64 * wave + lane);
@@ -459,6 +462,10 @@ __global__ __launch_bounds__(64 * NWV * TGW) void k_fa_ring(FaArgs a) {
       pv_tile_e4m3<RPW, NB, HDIM, RB>(st, pf, stg + TW * RB, lane);
     else
       pv_tile<RPW, NB, HDIM>(st, pf, stg + TW * SRB, lane);
+  }
+  for (int i = ntiles; i < nloop; ++i) {  // a group past its own tiles: group 0's barriers
+    if (NWV * TGW > 1) __syncthreads();
+    if (KCONV) __syncthreads();  // its K-tile barrier
   }
   const int64_t slot_base_row = (int64_t)blockIdx.x * (16 * RT);  // one partial per item
   if constexpr (TGW == 1) {
