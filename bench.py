@@ -16,6 +16,11 @@ from an earlier step (a real decode step runs the model's other layers
 between two calls of this block).  --caches flush reads a 1 GiB buffer
 before every step instead; --caches warm replays one copy.
 
+Cache layout: by default K and V of a token sit side by side, one 2 D
+record per (sequence, KV head, token), passed to the library as two
+strided views; --kv-layout split allocates K and V as two [B, Hkv, T, D]
+tensors (whose distance is then a large power of two at these sizes).
+
 Prints one JSON line (rank 0, N = 1).  Extra fields: achieved algorithmic
 GB/s of the step, the roofline of the dominant kernel (full-attention split
 kernel) from HIP events around its launches, the measured streaming-read
@@ -83,6 +88,8 @@ def parse():
     ap.add_argument("--caches", choices=("rotate", "flush", "warm"), default="rotate",
                     help="rotate: a different copy of the KV cache every step (default); flush: read a 1 GiB buffer "
                          "before every step (timed one by one); warm: the same cache every step")
+    ap.add_argument("--kv-layout", choices=("interleaved", "split"), default="interleaved",
+                    help="interleaved: K and V of a token in one 2 D record (default); split: two [B, Hkv, T, D] tensors")
     ap.add_argument("--kv-copies", type=int, default=0,
                     help="copies of the KV cache to rotate over (default: at least 4 and at least 2 GiB)")
     ap.add_argument("--stream-probe", action="store_true",
@@ -240,12 +247,20 @@ def main():
         kv_scales = None
     kv_bytes = K.numel() * K.element_size() + V.numel() * V.element_size()
     n_copies = kv_copies_for(kv_bytes, args.caches, args.kv_copies)
-    caches = [(K, V)] + [(K.clone(), V.clone()) for _ in range(n_copies - 1)]
+    if args.kv_layout == "interleaved":  # one [B, Hkv, T, 2 D] tensor: K in the first D of each record, V after it
+        kv_strides = (Hkv * Lmax * 2 * D, Lmax * 2 * D, 2 * D)
+        records = [torch.cat([K, V], dim=-1).contiguous()]
+        del K, V
+        records += [records[0].clone() for _ in range(n_copies - 1)]
+        caches = [(r[..., :D], r[..., D:]) for r in records]
+    else:
+        kv_strides = None
+        caches = [(K, V)] + [(K.clone(), V.clone()) for _ in range(n_copies - 1)]
     log(f"[bench] caches: {args.caches}, {n_copies} KV cop{'y' if n_copies == 1 else 'ies'} of {kv_bytes / 1e9:.3f} GB")
     q_fa = to_dev(inp.q_fa)
     q_sa = [to_dev(x) for x in inp.q_sa]
     lens = torch.from_numpy(inp.lens).to(dev)
-    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window, device=dev)
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window, device=dev, kv_strides=kv_strides)
     out = torch.empty((B, C, Hq, D), dtype=torch.bfloat16, device=dev)
     idx = torch.empty((B, Hkv, C, w.slots), dtype=torch.int32, device=dev)
     sa_out = [torch.empty_like(out) for _ in q_sa]
@@ -390,6 +405,8 @@ def main():
                       "queries_per_seq": C, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D, "k": w.k,
                       "window": w.window, "sparse_layers": w.n_sparse, "needles": w.needles,
                       "kv_cache": "e4m3" if args.kv == "fp8" else "bf16",
+                      "kv_layout": ("K and V interleaved: one 2 D record per (sequence, KV head, token)"
+                                    if args.kv_layout == "interleaved" else "K and V in two [B, Hkv, T, D] tensors"),
                       "selection": f"block{args.block}" if args.block else "token",
                       "launch": "graph" if args.graph else "eager",
                       "caches": cache_desc,

@@ -164,14 +164,13 @@ int ilog2(int v) {
 // (four waves), 32-token tiles in 2 stages and two token groups; the
 // workgroup kernel for eight.  Head dim 256: one row tile per wave, four
 // row tiles in 32-token tiles and 2 stages, fewer in 16-token tiles and 3
-// stages.  E4M3 cache with one row tile: 16-token tiles in 3 stages (the
-// small ring and converted tile keep many one-wave workgroups resident,
-// which the per-tile conversion needs: 125 us against 218 us with the bf16
-// shape on the ragged 128K workload).
+// stages.  The one-row-tile shape serves both cache formats (E4M3 at 512K:
+// 0.624 ms per step against 0.639 with 16-token tiles in 3 stages, whose
+// stored logits also make the score pass slower, 69 against 59 us).
 int default_fa_variant(int RT, int hd, bool kv8) {
   if (hd == 256) return RT >= 4 ? 8 : 6;
   if (RT >= 8) return kv8 ? 7 : 1;
-  if (RT == 1) return kv8 ? 3 : 2;
+  if (RT == 1) return 2;
   if (RT == 4) return 7;
   return 5;
 }

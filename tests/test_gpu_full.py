@@ -1,6 +1,7 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times (same workloads, same seeded inputs, the planner's default
-kernels and splits), checked on sampled (sequence, KV head) groups.
+kernels and splits, K and V interleaved in one 2 D record per token),
+checked on sampled (sequence, KV head) groups.
 
 The oracle computes only the sampled groups (each a whole context: up to
 524,288 tokens); every output row of those groups is held to the same bar
@@ -37,4 +38,4 @@ FULL = [
 
 @pytest.mark.parametrize("name,kv,groups", FULL, ids=[f"{n}-{kv}" for n, kv, _ in FULL])
 def test_full_size_sampled_groups(name, kv, groups):
-    parity_case(WL[name], groups=groups, kv=kv)
+    parity_case(WL[name], groups=groups, kv=kv, interleaved=True)

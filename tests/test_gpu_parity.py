@@ -48,14 +48,20 @@ def dev_cache(inp):
             (torch.from_numpy(inp.k_scale).cuda(), torch.from_numpy(inp.v_scale).cuda()))
 
 
-def run_gpu(inp, oracle_idx=None):
-    """Hybrid block on the GPU; returns host copies of every result."""
+def run_gpu(inp, oracle_idx=None, interleaved=False):
+    """Hybrid block on the GPU; returns host copies of every result.  With
+    interleaved, K and V of a token share one 2 D record: one [B, Hkv, Lmax,
+    2 D] tensor passed as two strided views."""
     hs2 = _hs2()
     w = inp.w
     B, C, Hq, Hkv, D = w.batch, w.n_queries, w.n_q_heads, w.n_kv_heads, w.head_dim
     Lmax = inp.K.shape[2]
-    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window)
+    strides = (Hkv * Lmax * 2 * D, Lmax * 2 * D, 2 * D) if interleaved else None
+    blk = hs2.HybridBlock(B, C, Hq, Hkv, D, Lmax, w.k, w.window, kv_strides=strides)
     K, V, sc = dev_cache(inp)
+    if interleaved:
+        KV = torch.cat([K, V], dim=-1).contiguous()
+        K, V = KV[..., :D], KV[..., D:]
     lens = torch.from_numpy(inp.lens.astype(np.int32)).cuda()
     stats = torch.empty((B, C, Hq, 2), dtype=torch.float32, device="cuda")
     scores = torch.zeros((B, Hkv, C, Lmax), dtype=torch.float32, device="cuda")
@@ -129,13 +135,13 @@ def compare(inp, ref, gpu, groups=None):
     return {**r_out, **r_sc, **r_idx, **r_struct}
 
 
-def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None, kv="bf16"):
+def parity_case(w, seed=W.BASE_SEED, lmax=None, groups=None, kv="bf16", interleaved=False):
     inp = W.make_inputs(w, seed=seed, lmax=lmax, kv=kv)
     note(f"[parity] {w.name} kv={kv} seed={seed} lens={inp.lens.tolist()} C={w.n_queries} Hq={w.n_q_heads} "
-         f"Hkv={w.n_kv_heads} k={w.k} W={w.window}")
+         f"Hkv={w.n_kv_heads} k={w.k} W={w.window}" + (" interleaved K|V" if interleaved else ""))
     ref = O.full_attn_score_select(inp.q_fa, inp.K, inp.V, inp.lens, w.k, w.window, groups=groups,
                                    k_scale=inp.k_scale, v_scale=inp.v_scale)
-    gpu = run_gpu(inp, oracle_idx=ref["idx"])
+    gpu = run_gpu(inp, oracle_idx=ref["idx"], interleaved=interleaved)
     r = compare(inp, ref, gpu, groups)
     note(f"[parity] {w.name}: {r}")
     return inp, ref, gpu
@@ -231,6 +237,19 @@ def test_strided_cache_layout():
     CK.check_idx(idx.cpu().numpy(), ref["idx"], ref["P"], inp.lens, C, w.window)
     if (idx.cpu().numpy() == ref["idx"]).all():
         CK.check_out(CK.bf16_bits_to_f64(host_bits(sa)), O.sparse_attention(inp.q_sa[0], inp.K, inp.V, ref["idx"]))
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+@pytest.mark.parametrize("w", [SMALL[2], SMALL[3]], ids=[SMALL[2].name, SMALL[3].name])
+def test_interleaved_cache_layout(w, kv):
+    """K and V of a token in one 2 D record (the benchmark's layout): the
+    oracle's bar, and bit for bit the results of two separate tensors."""
+    inp, ref, gpu = parity_case(w, seed=13, kv=kv, interleaved=True)
+    split = run_gpu(inp, oracle_idx=ref["idx"])
+    for key in ("out", "idx", "stats", "scores", "out_with_scores", "idx_with_scores"):
+        np.testing.assert_array_equal(gpu[key], split[key], err_msg=key)
+    for a, b in zip(gpu["sa"] + gpu["sa_ref_idx"], split["sa"] + split["sa_ref_idx"]):
+        np.testing.assert_array_equal(a, b)
 
 
 @pytest.mark.parametrize("w", [SMALL[0], SMALL[2]], ids=[SMALL[0].name, SMALL[2].name])
