@@ -24,7 +24,8 @@ tensors (whose distance is then a large power of two at these sizes).
 Prints one JSON line (rank 0, N = 1).  Extra fields: achieved algorithmic
 GB/s of the step, the roofline of the dominant kernel (full-attention split
 kernel) from HIP events around its launches, the measured streaming-read
-ceiling of the device (hs2_stream_read_probe), per-kernel averages,
+and gather ceilings of the device (hs2_stream_read_probe), the sparse
+layer's roofline against the gather ceiling, per-kernel averages,
 per-step percentiles, and the CPU oracle timed on a bounded sample of the
 same workload (all host threads, and one thread).
 """
@@ -157,6 +158,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload
 
 
 STREAM_PROBE_BYTES = 4 << 30
+GATHER_PROBE_MODE = 4  # 512-byte records in a scattered order
 STREAM_PROBE_MODES = {0: "register loads", 1: "register loads, non-temporal", 2: "direct-to-LDS loads",
                       3: "direct-to-LDS loads, non-temporal"}
 
@@ -183,11 +185,23 @@ def stream_probe(dev, reps: int = 8) -> dict:
         torch.cuda.synchronize()
         ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in ev]))
         rates[mode] = STREAM_PROBE_BYTES / (ms * 1e-3) / 1e9
+    best = max(rates, key=rates.get)
+    # the gather ceiling: the same buffer as 512-byte records read once each
+    # in a scattered order (the sparse layers' access pattern)
+    for _ in range(2):
+        hs2.hs2_stream_read_probe(buf, GATHER_PROBE_MODE, sink, st)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a_, b_ in ev:
+        a_.record(st)
+        hs2.hs2_stream_read_probe(buf, GATHER_PROBE_MODE, sink, st)
+        b_.record(st)
+    torch.cuda.synchronize()
+    gather = STREAM_PROBE_BYTES / (float(np.median([a_.elapsed_time(b_) for a_, b_ in ev])) * 1e-3) / 1e9
     del buf
     torch.cuda.empty_cache()
-    best = max(rates, key=rates.get)
     return {"stream_peak_gbps": round(rates[best], 1), "mode": STREAM_PROBE_MODES[best],
             "gbps_by_mode": {STREAM_PROBE_MODES[m]: round(r, 1) for m, r in rates.items()},
+            "gather_peak_gbps": round(gather, 1), "gather_record_bytes": 512,
             "bytes": STREAM_PROBE_BYTES, "launches_per_mode": reps}
 
 
@@ -389,6 +403,16 @@ def main():
     if probe:
         roofline["stream_peak"] = probe["stream_peak_gbps"]
         roofline["frac_of_stream_peak"] = round(achieved / probe["stream_peak_gbps"], 4)
+    # the sparse layer: the unique selected rows of each (sequence, KV head)
+    # read once, against the gather ceiling
+    sa_bytes = uniq * kv_row
+    sa_achieved = sa_bytes / (kernels["sa_split"]["avg_us"] * 1e-6) / 1e9
+    sa_roofline = {"kernel": "sa_split", "bound": "hbm (gathers)", "achieved": round(sa_achieved, 1),
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(sa_achieved / HBM_PEAK_GBS, 4),
+                   "algorithmic_bytes_per_launch": int(sa_bytes)}
+    if probe:
+        sa_roofline["gather_peak"] = probe["gather_peak_gbps"]
+        sa_roofline["frac_of_gather_peak"] = round(sa_achieved / probe["gather_peak_gbps"], 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -414,6 +438,7 @@ def main():
            "achieved_gbps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
            "algorithmic_bytes_per_step": int(step_bytes),
            "roofline": roofline,
+           "sa_roofline": sa_roofline,
            "stream_peak_gbps": probe["stream_peak_gbps"] if probe else None,
            "stream_probe": probe,
            "step_ms_percentiles": pct,

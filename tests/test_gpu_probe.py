@@ -1,7 +1,9 @@
 """GPU: the streaming-read probe reads every 32-bit word of its buffer exactly
 once in each load mode (the xor of its per-workgroup folds equals the
 host's xor of the buffer), including a buffer
-whose size leaves partial pieces and empty workgroup slices."""
+whose size leaves partial pieces and empty workgroup slices; the gather
+mode over record counts that give whole pieces, an odd record per slice,
+and empty slices."""
 from __future__ import annotations
 
 import numpy as np
@@ -21,6 +23,20 @@ def test_stream_probe_reads_every_word_once(words16, mode):
     sink = torch.zeros(hs2.STREAM_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
     print(f"[probe] mode={mode} words16={words16}", flush=True)
     hs2.hs2_stream_read_probe(buf, mode, sink)
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(host)
+    assert int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))) == int(want)
+
+
+@pytest.mark.parametrize("records", [1 << 15, 1 << 13, 1 << 12, 1 << 10, 1])
+def test_stream_probe_gather_reads_every_word_once(records):
+    from paper_2609_26368_amd import hs2
+    rng = np.random.default_rng(records)
+    host = rng.integers(0, 2 ** 32, size=128 * records, dtype=np.uint32)  # 512-byte records
+    buf = torch.from_numpy(host.view(np.int32)).cuda()
+    sink = torch.zeros(hs2.STREAM_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
+    print(f"[probe] mode=4 records={records}", flush=True)
+    hs2.hs2_stream_read_probe(buf, 4, sink)
     torch.cuda.synchronize()
     want = np.bitwise_xor.reduce(host)
     assert int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))) == int(want)
