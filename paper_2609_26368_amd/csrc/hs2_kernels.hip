@@ -805,7 +805,10 @@ struct PoolShape {
   // 4 % at 64 rows per KV head), RPL NWV when more
   static constexpr int TW_MIN = KV8 ? 16 : 32;
   static constexpr int TW = RPL * NWV > TW_MIN ? RPL * NWV : TW_MIN;
-  static constexpr int NS = 3;
+  // 3 stages; 2 for a bf16 cache of head dim 256 (16 KB stages: one more
+  // workgroup per CU, the MQA 64/1 pass 85 -> 83 us; at head dim 128 two
+  // stages lose 94 -> 105 us)
+  static constexpr int NS = !KV8 && HDIM == 256 ? 2 : 3;
   static constexpr int SB = TW * RB;                          // ring stage
   // E4M3 with several waves: K converted once into a shared bf16 tile
   static constexpr bool KCONV = KV8 && NWV > 1;
