@@ -2109,7 +2109,7 @@ __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ 
   hipLaunchKernelGGL(kernel, grid, block, shmem, (hipStream_t)(stream), arg)
 
 // Full attention kernel variants (the planner's defaults: head dim 128 with
-// RT = 1 -> 2 (E4M3: 3), RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1 (E4M3: 7);
+// RT = 1 -> 2, RT = 2 -> 5, RT = 4 -> 7, RT = 8 -> 1 (E4M3: 7);
 // head dim 256 with RT = 4, 8 -> 8, else 6):
 //   1: workgroup kernel (64-row stages shared by 4 or 8 waves), head dim 128
 //   0, 2, 3, 5, 7: ring kernels of head dim 128; 6, 8: head dim 256
