@@ -261,11 +261,12 @@ hs2_status hs2_select_from_scores(const hs2_dims* dims, const float* scores, con
  *   mode    0: 16-byte register loads; 1: the same with the non-temporal
  *           hint; 2: 16-byte direct-to-LDS loads, the loads the
  *           full-attention and score kernels issue; 3: the same
- *           non-temporal; 4: gathers, the rate of the sparse layers' access
- *           pattern -- the buffer as 512-byte records (bytes must be 512
- *           times a power of two, else HS2_ERR_SHAPE) read in a scattered
- *           order (a fixed permutation, each record once) by the same
- *           direct-to-LDS loads, two records per 1 KB wave load
+ *           non-temporal; 4 and 5: gathers, the rate of the sparse
+ *           layers' access pattern -- the buffer as records of 512 (mode 4:
+ *           a token's K and V in a bf16 cache of head dim 128) or 256 bytes
+ *           (mode 5: E4M3) read in a scattered order (a fixed permutation,
+ *           each record once) by the same direct-to-LDS loads; bytes must
+ *           be the record size times a power of two, else HS2_ERR_SHAPE
  *           (other modes: HS2_ERR_SHAPE)
  *   src     16-byte aligned, bytes a multiple of 16 (HS2_ERR_ALIGN), bytes > 0
  *   sink    device array of HS2_STREAM_PROBE_SINK_WORDS uint32, 4-byte

@@ -827,10 +827,12 @@ hs2_status hs2_sparse_attn_fp8(const hs2_dims* dims, const uint16_t* q, const ui
 
 hs2_status hs2_stream_read_probe(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream) {
   if (!src || !sink) return fail(HS2_ERR_NULL, "src and sink are required");
-  if (mode < 0 || mode > 4) return fail(HS2_ERR_SHAPE, "mode must be 0, 1, 2, 3 or 4 (got %d)", mode);
+  if (mode < 0 || mode > 5) return fail(HS2_ERR_SHAPE, "mode must be in [0, 5] (got %d)", mode);
   if (bytes == 0) return fail(HS2_ERR_SHAPE, "bytes must be > 0");
-  if (mode == 4 && (bytes % 512 || ((bytes / 512) & (bytes / 512 - 1))))
-    return fail(HS2_ERR_SHAPE, "mode 4 reads 512-byte records: bytes must be 512 times a power of two");
+  const size_t rec = mode == 4 ? 512 : 256;  // gather modes: record bytes
+  if (mode >= 4 && (bytes % rec || ((bytes / rec) & (bytes / rec - 1))))
+    return fail(HS2_ERR_SHAPE, "mode %d reads %zu-byte records: bytes must be %zu times a power of two", mode, rec,
+                rec);
   if (!aligned(src, 16) || bytes % 16 || !aligned(sink, 4))
     return fail(HS2_ERR_ALIGN, "src needs 16-byte alignment and a multiple of 16 bytes, sink 4-byte alignment");
   static_assert(HS2_STREAM_PROBE_SINK_WORDS == STREAM_PROBE_WORKGROUPS, "one sink word per probe workgroup");

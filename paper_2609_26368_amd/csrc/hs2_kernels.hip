@@ -1999,12 +1999,12 @@ __global__ __launch_bounds__(64 * NWV) void k_sa_ring(SaArgs a) {
 // the same non-temporal, 2: 16-byte direct-to-LDS loads of 1 KB per wave as
 // the streaming kernels issue them (up to 8 in flight per wave into an 8 KB
 // ring, each piece read back from LDS once it has landed), 3: the same
-// non-temporal; 4: gathers -- the buffer is R = n16 / 32 records of 512
-// bytes (R a power of two, checked by the host) read in a scattered order,
-// logical record r at position (r * 0x9E3779B97F4A7C15) mod R (an odd
-// multiplier: a permutation), each 1 KB direct-to-LDS wave load covering
-// two records (32 lanes each), as a sparse layer gathers a token's K and V
-// rows from an interleaved cache.  Every mode folds each 32-bit word of src exactly once
+// non-temporal; 4 and 5: gathers -- the buffer is R records of 512 (mode
+// 4) or 256 (mode 5) bytes, R a power of two (checked by the host), read in
+// a scattered order, logical record r at position (r * 0x9E3779B97F4A7C15)
+// mod R (an odd multiplier: a permutation), each 1 KB direct-to-LDS wave
+// load covering 2 or 4 records, as a sparse layer gathers a token's K and V
+// rows from an interleaved bf16 or E4M3 cache.  Every mode folds each 32-bit word of src exactly once
 // (xor); workgroup w stores the fold of its slice to sink[w] (keeps the
 // loads live and lets a test check that every word was read once: the xor
 // of sink[0, gridDim.x) is the xor of the whole buffer).  No atomics: the
@@ -2034,8 +2034,10 @@ __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ 
 #pragma unroll
       for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
     }
-  } else if constexpr (MODE == 4) {
-    const int64_t R = n16 / 32;
+  } else if constexpr (MODE >= 4) {
+    constexpr int RW = MODE == 4 ? 32 : 16;  // 16-byte words per record
+    constexpr int RPP = 64 / RW;             // records per 1 KB piece
+    const int64_t R = n16 / RW;
     const uint64_t rmask = (uint64_t)R - 1;
     auto perm = [&](int64_t r) { return (int64_t)(((uint64_t)r * 0x9E3779B97F4A7C15ull) & rmask); };
     const int64_t rper = (R + gridDim.x - 1) / gridDim.x;
@@ -2043,15 +2045,15 @@ __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ 
     const int64_t rhi = max(rlo, min(R, rlo + rper));
     const unsigned char* wring = ring + wave * 8 * 1024;
     const uint32_t wring_a = lds_addr(wring);
-    const int64_t npieces = (rhi - rlo) / 2;  // two records per 1 KB piece
+    const int64_t npieces = (rhi - rlo) / RPP;
     auto fold = [&](int64_t n) {
       const uint4 v = *(const uint4*)(wring + 1024 * (n & 7) + 16 * lane);
       acc ^= v.x ^ v.y ^ v.z ^ v.w;
     };
     int64_t n = 0;
     for (int64_t j = wave; j < npieces; j += 4, ++n) {
-      const int64_t rec = perm(rlo + 2 * j + (lane >> 5));
-      dma16_p<false>(src + 32 * rec + (lane & 31), __builtin_amdgcn_readfirstlane(wring_a + 1024u * (uint32_t)(n & 7)));
+      const int64_t rec = perm(rlo + RPP * j + lane / RW);
+      dma16_p<false>(src + RW * rec + lane % RW, __builtin_amdgcn_readfirstlane(wring_a + 1024u * (uint32_t)(n & 7)));
       __builtin_amdgcn_s_waitcnt(vmcnt_enc(7));  // at most 7 outstanding: piece n - 7 has landed
       if (n >= 7) {
         fold(n - 7);
@@ -2060,8 +2062,9 @@ __global__ __launch_bounds__(256) void k_stream_probe(const uint4* __restrict__ 
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_enc(0));
     for (int64_t m = n > 7 ? n - 7 : 0; m < n; ++m) fold(m);
-    if (((rhi - rlo) & 1) && tid < 32) {  // an odd record left in the slice
-      const uint4 v = src[32 * perm(rhi - 1) + tid];
+    // the slice's records after its whole pieces (fewer than RPP): register loads
+    for (int64_t k = rlo + RPP * npieces + tid / RW; k < rhi && tid < RPP * RW; k += RPP) {
+      const uint4 v = src[RW * perm(k) + tid % RW];
       acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
     i = hi;  // no word tail: the records cover the buffer
@@ -2453,6 +2456,7 @@ hipError_t launch_stream_probe(const void* src, int64_t n16, int mode, uint32_t*
     case 2: hipLaunchKernelGGL(k_stream_probe<2>, grid, block, 0, s, p, n16, sink); break;
     case 3: hipLaunchKernelGGL(k_stream_probe<3>, grid, block, 0, s, p, n16, sink); break;
     case 4: hipLaunchKernelGGL(k_stream_probe<4>, grid, block, 0, s, p, n16, sink); break;
+    case 5: hipLaunchKernelGGL(k_stream_probe<5>, grid, block, 0, s, p, n16, sink); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -252,10 +252,12 @@ def test_stream_probe_rejects_before_launch(lib):
     vp = ctypes.c_void_p
     assert lib.hs2_stream_read_probe(None, 1024, 0, vp(FAKE), None) == hs2.HS2_ERR_NULL
     assert lib.hs2_stream_read_probe(vp(FAKE), 1024, 0, None, None) == hs2.HS2_ERR_NULL
-    assert lib.hs2_stream_read_probe(vp(FAKE), 1024, 5, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
-    # the gather mode reads 512-byte records, a power of two of them
+    assert lib.hs2_stream_read_probe(vp(FAKE), 1024, 6, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    # the gather modes read 512- (mode 4) or 256-byte records (mode 5), a power of two of them
     assert lib.hs2_stream_read_probe(vp(FAKE), 3 * 512, 4, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
     assert lib.hs2_stream_read_probe(vp(FAKE), 1024 + 16, 4, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    assert lib.hs2_stream_read_probe(vp(FAKE), 256, 4, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
+    assert lib.hs2_stream_read_probe(vp(FAKE), 3 * 256, 5, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
     assert lib.hs2_stream_read_probe(vp(FAKE), 1024, -1, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
     assert lib.hs2_stream_read_probe(vp(FAKE), 0, 0, vp(FAKE), None) == hs2.HS2_ERR_SHAPE
     assert lib.hs2_stream_read_probe(vp(FAKE + 8), 1024, 0, vp(FAKE), None) == hs2.HS2_ERR_ALIGN

@@ -2,8 +2,8 @@
 once in each load mode (the xor of its per-workgroup folds equals the
 host's xor of the buffer), including a buffer
 whose size leaves partial pieces and empty workgroup slices; the gather
-mode over record counts that give whole pieces, an odd record per slice,
-and empty slices."""
+modes (512- and 256-byte records) over record counts that give whole
+pieces, partial pieces per slice, and empty slices."""
 from __future__ import annotations
 
 import numpy as np
@@ -28,15 +28,16 @@ def test_stream_probe_reads_every_word_once(words16, mode):
     assert int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))) == int(want)
 
 
-@pytest.mark.parametrize("records", [1 << 15, 1 << 13, 1 << 12, 1 << 10, 1])
-def test_stream_probe_gather_reads_every_word_once(records):
+@pytest.mark.parametrize("records", [1 << 15, 1 << 13, 1 << 12, 1 << 11, 1 << 10, 1])
+@pytest.mark.parametrize("mode,record_bytes", [(4, 512), (5, 256)])
+def test_stream_probe_gather_reads_every_word_once(mode, record_bytes, records):
     from paper_2609_26368_amd import hs2
-    rng = np.random.default_rng(records)
-    host = rng.integers(0, 2 ** 32, size=128 * records, dtype=np.uint32)  # 512-byte records
+    rng = np.random.default_rng(records + mode)
+    host = rng.integers(0, 2 ** 32, size=record_bytes // 4 * records, dtype=np.uint32)
     buf = torch.from_numpy(host.view(np.int32)).cuda()
     sink = torch.zeros(hs2.STREAM_PROBE_SINK_WORDS, dtype=torch.int32, device="cuda")
-    print(f"[probe] mode=4 records={records}", flush=True)
-    hs2.hs2_stream_read_probe(buf, 4, sink)
+    print(f"[probe] mode={mode} records={records}", flush=True)
+    hs2.hs2_stream_read_probe(buf, mode, sink)
     torch.cuda.synchronize()
     want = np.bitwise_xor.reduce(host)
     assert int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))) == int(want)
