@@ -1,7 +1,8 @@
 """GPU parity on seeded random shapes: batch, query chunk, group size (also
 not a power of two), KV heads, head dim, ragged lengths, budget and window
 drawn from a fixed generator (the same 24 shapes every run), each in both
-cache formats, held to the oracle's bar like the hand-picked cases.  Sizes
+cache formats and every other one with K and V interleaved per token, held
+to the oracle's bar like the hand-picked cases.  Sizes
 stay small (at most ~3000 tokens per sequence) so that the oracle keeps up."""
 from __future__ import annotations
 
@@ -45,6 +46,7 @@ SHAPES = random_shapes()
 
 
 @pytest.mark.parametrize("kv", ["bf16", "fp8"])
-@pytest.mark.parametrize("w", SHAPES, ids=[w.name for w in SHAPES])
-def test_random_shape_parity(w, kv):
-    parity_case(w, seed=31, kv=kv)
+@pytest.mark.parametrize("i", range(len(SHAPES)), ids=[w.name for w in SHAPES])
+def test_random_shape_parity(i, kv):
+    # every other shape with K and V interleaved in one record per token
+    parity_case(SHAPES[i], seed=31, kv=kv, interleaved=i % 2 == 1)
